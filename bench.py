@@ -1,0 +1,325 @@
+"""Decode throughput of the Radar path on one MI355X.
+
+A step is one pass of the whole path for one token of every sequence:
+radar_append (k/v row write, plus the summary refresh when a segment fills)
+followed by radar_decode (phi(q), segment scores, top-k, union, gather
+attention, combine) for every (batch, query head). Inputs are seeded
+synthetic tensors already resident in HBM; the default workload is the
+long-context MHA layer: batch 8, 32 heads, head_dim 128, 128K context,
+segment length 256, top-16 segments, 256 random features, recent window 256,
+bf16 K/V, clustered keys.
+
+Prints one JSON line: tokens/s (batch x steps / time) with the algorithmic
+HBM bytes of the step, the roofline of the gather-attention kernel (per-launch
+algorithmic K/V bytes over its event-timed duration), the index build's MFMA
+utilisation, and the fp64 oracle timed on a bounded sample on the host.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import paper_2503_10571_amd as radar  # noqa: E402
+import workloads  # noqa: E402
+
+METRIC = ("decode attention tokens/sec (all heads) + achieved HBM GB/s at "
+          "128K context")
+HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
+BF16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def window_split(t, c, w):
+    ws = c * (max(0, t - w) // c)
+    return ws, ws // c
+
+
+class Stepper:
+    """Direct C-ABI calls with pre-marshalled arguments (the per-step host
+    cost stays small next to the GPU time)."""
+
+    def __init__(self, cfg, inp, K, V, summ, ws, out, k):
+        self.L = radar.lib()
+        self.cfg_c = cfg.c_struct()
+        self.cfgp = ctypes.byref(self.cfg_c)
+        self.inp = inp
+        P = ctypes.c_void_p
+        self.K, self.V = P(K.data_ptr()), P(V.data_ptr())
+        self.om = P(inp.omega.data_ptr())
+        self.summ = P(summ.data_ptr())
+        self.ws, self.ws_n = P(ws.data_ptr()), ws.numel()
+        self.out = P(out.data_ptr())
+        self.k = k
+        self.stream = P(torch.cuda.current_stream().cuda_stream)
+        self.kn = [P(inp.k_new[i].data_ptr()) for i in range(inp.k_new.shape[0])]
+        self.vn = [P(inp.v_new[i].data_ptr()) for i in range(inp.v_new.shape[0])]
+        self.q = [P(inp.q[i].data_ptr()) for i in range(inp.q.shape[0])]
+        self.t0 = inp.wl.t0
+
+    def step(self, i, sel=None):
+        t = self.t0 + i
+        st = self.L.radar_append(self.cfgp, self.K, self.V, self.kn[i],
+                                 self.vn[i], self.om, t, self.summ, self.stream)
+        if st:
+            raise radar.RadarError("radar_append", st)
+        st = self.L.radar_decode(self.cfgp, self.q[i], self.K, self.V, self.om,
+                                 self.summ, t + 1, self.k, self.out, sel, None,
+                                 self.ws, self.ws_n, self.stream)
+        if st:
+            raise radar.RadarError("radar_decode", st)
+
+
+def union_sizes(sel, G):
+    """sel [B][Hq][k] int32 -> union size per (b, kv head) [B * Hkv]."""
+    B, Hq, k = sel.shape
+    Hkv = Hq // G
+    g = sel.reshape(B, Hkv, G * k)
+    out = np.empty(B * Hkv, dtype=np.int64)
+    for i, row in enumerate(g.reshape(B * Hkv, G * k)):
+        out[i] = len(set(int(x) for x in row if x >= 0))
+    return out
+
+
+def step_bytes(wl, t, U, s_kv):
+    """Algorithmic HBM bytes of one step whose decode runs at length t (the
+    append wrote row t - 1). U: union size per (b, kv head)."""
+    c, d, n = wl.seg_len, wl.head_dim, wl.n_features
+    ws, n_cand = window_split(t, c, wl.window)
+    W = t - ws
+    BH = wl.batch * wl.n_kv_heads
+    summ = BH * n_cand * n * 4
+    kv = int(np.sum(U * c + W)) * d * 2 * s_kv
+    qo = wl.batch * wl.n_q_heads * d * 2 * s_kv
+    om = n * d * 4
+    app = BH * 2 * d * s_kv
+    close = BH * (c * d * s_kv + n * 4) if t % c == 0 else 0
+    return summ + kv + qo + om + app + close, kv
+
+
+def blas_threads():
+    try:
+        from threadpoolctl import threadpool_info
+        n = [i.get("num_threads", 0) for i in threadpool_info()
+             if i.get("user_api") == "blas"]
+        if n:
+            return int(max(n))
+    except Exception:
+        pass
+    return int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+
+
+def cpu_baseline(wl, inp, first_step, n_steps, n_heads, budget_s=20.0):
+    """The fp64 oracle (as it stands) on `n_heads` sampled (b, q head) pairs
+    for up to `n_steps` steps: per step a segment-close refresh when one is
+    due, then phi(q), scores, top-k and exact attention. Scaled to the
+    workload's tokens/s (all heads)."""
+    from oracle import radar_oracle as orc
+    G, c = wl.group, wl.seg_len
+    rng = np.random.default_rng(5)
+    pairs = [(int(b), int(h)) for b, h in
+             zip(rng.integers(0, wl.batch, n_heads),
+                 rng.integers(0, wl.n_q_heads, n_heads))]
+    om = inp.omega.double().cpu().numpy()
+    last = first_step + n_steps
+    state = []
+    for b, h in pairs:
+        g = h // G
+        keys = inp.keys_at(last, b, g).double().cpu().numpy()
+        vals = inp.values_at(last, b, g).double().cpu().numpy()
+        t_start = wl.t0 + first_step
+        summ = orc.segment_summaries(keys[:t_start], om, c)   # index (untimed)
+        state.append([b, h, keys, vals, summ])
+    qs = inp.q[first_step:last].double().cpu().numpy()
+    done = 0
+    t_begin = time.perf_counter()
+    for i in range(n_steps):
+        t = wl.t0 + first_step + i + 1
+        for st in state:
+            b, h, keys, vals, summ = st
+            if t % c == 0:                  # the appended row closed a segment
+                new = orc.segment_summaries(keys[:t], om, c, first=t // c - 1)
+                st[4] = summ = np.concatenate([summ, new], 0)
+            ws, n_cand = orc.window_split(t, c, wl.window)
+            phi_q = orc.random_features(qs[i, b, h], om)
+            _, sel = orc.decode_head(phi_q, summ, n_cand, wl.top_k)
+            toks = orc.attended_tokens(sel, c, ws, t)
+            orc.attend(qs[i, b, h], keys, vals, toks)
+            done += 1
+        if time.perf_counter() - t_begin > budget_s:
+            break
+    el = time.perf_counter() - t_begin
+    per_head_step = el / done
+    step_s = per_head_step * wl.batch * wl.n_q_heads
+    return {"value": wl.batch / step_s, "unit": "tokens/s",
+            "cores": blas_threads(), "kind": "oracle",
+            "sample": (f"{len(state)} sampled (batch, q head) pairs x "
+                       f"{done // len(state)} decode steps ({done} head-steps, "
+                       f"{el:.1f} s), scaled to all {wl.batch * wl.n_q_heads} "
+                       "heads; the index build before the sample is untimed")}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=512)
+    ap.add_argument("--warmup", type=int, default=16)
+    ap.add_argument("--workload", default="mha_128k",
+                    choices=sorted(workloads.WORKLOADS))
+    ap.add_argument("--cpu-baseline", type=int, default=1)
+    ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--build-reps", type=int, default=3)
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the decode path has no multi-GPU "
+              "mode in this build (run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+
+    wl = workloads.WORKLOADS[args.workload]
+    W, Ksteps = args.warmup, args.steps
+    total = W + Ksteps
+    log(f"[bench] generating {wl.name} inputs ({total} steps)")
+    inp = workloads.make_inputs(wl, "cuda", steps=total)
+    cfg = radar.Config(wl.batch, wl.n_q_heads, wl.n_kv_heads, wl.head_dim,
+                       wl.n_features, wl.seg_len, wl.window, wl.t0 + total,
+                       wl.torch_dtype())
+    s_kv = 2 if wl.dtype == "bf16" else 4
+    K, V = inp.K, inp.V
+    summ = radar.new_summaries(cfg, K.device)
+    ws = radar.new_workspace(cfg, wl.top_k, K.device)
+    out = torch.empty_like(inp.q[0])
+    torch.cuda.synchronize()
+
+    # ---- index build (Eq. 4-5 over the whole prefix) --------------------
+    log("[bench] index build")
+    radar.build_index(cfg, K, inp.omega, wl.t0, summ)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.build_reps):
+        radar.build_index(cfg, K, inp.omega, wl.t0, summ)
+    e1.record()
+    torch.cuda.synchronize()
+    build_ms = e0.elapsed_time(e1) / args.build_reps
+    n_keys = wl.batch * wl.n_kv_heads * (wl.t0 // wl.seg_len) * wl.seg_len
+    build_flop = 2.0 * n_keys * wl.n_features * wl.head_dim
+    build_tflops = build_flop / (build_ms * 1e-3) / 1e12
+
+    # ---- decode steps ----------------------------------------------------
+    stp = Stepper(cfg, inp, K, V, summ, ws, out, wl.top_k)
+    sel_log = torch.empty(Ksteps, wl.batch, wl.n_q_heads, wl.top_k,
+                          dtype=torch.int32, device=K.device)
+    log(f"[bench] warmup {W} steps")
+    for i in range(W):
+        stp.step(i)
+    torch.cuda.synchronize()
+    log(f"[bench] timing {Ksteps} steps")
+    e0.record()
+    for j in range(Ksteps):
+        stp.step(W + j, ctypes.c_void_p(sel_log[j].data_ptr()))
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+    ms_step = ms / Ksteps
+
+    # the same steps again with every kernel bracketed by HIP events
+    radar.profile_enable(True)
+    for j in range(Ksteps):
+        stp.step(W + j)
+    torch.cuda.synchronize()
+    prof = radar.profile_read()
+    radar.profile_enable(False)
+
+    # ---- algorithmic bytes ------------------------------------------------
+    sel_np = sel_log.cpu().numpy()
+    tot_bytes, kv_bytes = 0, 0
+    for j in range(Ksteps):
+        t = wl.t0 + W + j + 1
+        U = union_sizes(sel_np[j], wl.group)
+        b_all, b_kv = step_bytes(wl, t, U, s_kv)
+        tot_bytes += b_all
+        kv_bytes += b_kv
+    step_gbps = tot_bytes / (ms * 1e-3) / 1e9
+    att_ms, att_n = prof["attend"]
+    att_avg_ms = att_ms / max(att_n, 1)
+    att_gbps = (kv_bytes / Ksteps) / (att_avg_ms * 1e-3) / 1e9
+    tokens_s = wl.batch * Ksteps / (ms * 1e-3)
+
+    kern = {k: {"avg_us": round(v[0] / max(v[1], 1) * 1e3, 2), "launches": v[1]}
+            for k, v in prof.items() if v[1]}
+    log("[bench] kernels: " + json.dumps(kern))
+
+    cpu = None
+    if args.cpu_baseline:
+        log("[bench] cpu baseline (fp64 oracle)")
+        cpu = cpu_baseline(wl, inp, W, Ksteps, n_heads=4,
+                           budget_s=args.cpu_budget)
+
+    line = {
+        "metric": METRIC,
+        "value": round(tokens_s, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": Ksteps,
+        "warmup": W,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic",
+        "config": {
+            "workload": (f"{wl.name}: batch {wl.batch}, {wl.n_q_heads} q / "
+                         f"{wl.n_kv_heads} kv heads, head_dim {wl.head_dim}, "
+                         f"context {wl.t0}+, c {wl.seg_len}, top-k "
+                         f"{wl.top_k}, n {wl.n_features}, window {wl.window}, "
+                         f"{wl.dtype} K/V, {wl.keys} keys"),
+            "batch": wl.batch, "context": wl.t0, "seg_len": wl.seg_len,
+            "top_k": wl.top_k, "n_features": wl.n_features,
+            "window": wl.window,
+        },
+        "hbm_GBps": round(step_gbps, 1),
+        "hbm_frac": round(step_gbps / HBM_PEAK_GBPS, 4),
+        "bytes_per_step": int(tot_bytes // Ksteps),
+        "roofline": {
+            "kernel": "k_attend",
+            "bound": "hbm",
+            "achieved": round(att_gbps, 1),
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": round(att_gbps / HBM_PEAK_GBPS, 4),
+            "traffic": None,
+            "bytes_per_launch": int(kv_bytes // Ksteps),
+            "avg_us": round(att_avg_ms * 1e3, 2),
+        },
+        "kernels_us": {k: v["avg_us"] for k, v in kern.items()},
+        "index_build": {
+            "ms": round(build_ms, 3),
+            "tflops": round(build_tflops, 1),
+            "mfma_frac": round(build_tflops / BF16_MFMA_PEAK_TFLOPS, 4),
+            "keys": n_keys,
+        },
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,182 @@
+/*
+ * radar.h -- C ABI of the Radar decode path on MI355X (gfx950).
+ *
+ * Radar ("Radar: Fast Long-Context Decoding for Any Transformer", ICLR 2025)
+ * keeps a two-level index over the key cache: the keys are cut into segments
+ * of c tokens and every segment is summarised by the mean of the positive
+ * random features of its keys (Section 2.2, Eq. 4 and Eq. 5). A decode query
+ * is mapped to the same random features, every segment is scored by one dot
+ * product (Eq. 6), the top-k segments are selected, and exact softmax
+ * attention (Section 2.1, Eq. 1-2) runs over the selected segments' tokens
+ * together with the recent tokens that belong to no summarised segment
+ * (Appendix A, Algorithm 1).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - Every tensor argument is a DEVICE pointer owned by the caller; `cfg` is a
+ *    host pointer. The library allocates no device memory, keeps no state
+ *    between calls, never synchronises, and launches only on `stream`.
+ *  - Layouts are dense, row-major, element type `kv_dtype` for q / K / V /
+ *    k_new / v_new / out, fp32 for Omega, summaries and scores, int32 for
+ *    segment ids:
+ *        q, out          [B][Hq][d]
+ *        K, V            [B][Hkv][capacity][d]     (token-major per head)
+ *        k_new, v_new    [B][Hkv][d]
+ *        omega           [n][d]                    (row i is omega_i)
+ *        summaries       [B][Hkv][capacity / c][n]
+ *        selected        [B][Hq][k]   int32, -1 padded
+ *        scores          [B][Hq][k]   fp32,  NaN padded
+ *  - Every pointer must be 16-byte aligned.
+ *  - Positions are 0-based. "t" is the current context length: tokens
+ *    0 .. t-1 are valid in K and V.
+ *  - Errors: every argument is checked before anything is launched, so a
+ *    call that returns an error has no side effect. A failed launch returns
+ *    RADAR_EHIP; radar_last_error() then holds the HIP error text. No C++
+ *    exception crosses this boundary.
+ *
+ * Numerical contract
+ * ------------------
+ *  phi(x)_i = n^(-1/2) exp(omega_i . x' - |x'|^2 / 2),  x' = x / d^(1/4)
+ *  (Eq. 4; omega_i is the i-th row of Omega, and queries and keys are both
+ *  scaled by d^(-1/4)). Summaries hold the Eq. 5 means, scores the Eq. 6
+ *  dot products, both in fp32. All accumulation is fp32. For bf16 caches the
+ *  projection runs on bf16 matrix cores with Omega rounded to bf16 (round to
+ *  nearest even); pass a bf16-representable Omega for results that do not
+ *  depend on that rounding. exp arguments must stay below ~88 (fp32 range);
+ *  unit-scale keys and queries keep them far below.
+ *
+ * Segments, window and candidates
+ * -------------------------------
+ *  Segment s covers tokens [s*c, s*c + c); only full segments are summarised.
+ *  At a decode step with context length t the recent window is
+ *  W = [ws, t) with ws = c * floor(max(0, t - w) / c); it is always attended.
+ *  The candidate segments are the n_cand = ws / c segments wholly before ws.
+ *  Each query head selects k_eff = min(k, n_cand) of them, ordered by score
+ *  descending and then by segment index ascending. With grouped-query
+ *  attention (Hq = G * Hkv) every query head of a group attends the union of
+ *  the group's selections plus W.
+ */
+#ifndef RADAR_H
+#define RADAR_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define RADAR_ABI_VERSION 1
+
+typedef enum {
+  RADAR_OK = 0,
+  RADAR_EINVAL = 1,       /* null pointer, bad shape, misaligned pointer    */
+  RADAR_ECAPACITY = 2,    /* t or a position outside [.., capacity]         */
+  RADAR_EUNSUPPORTED = 3, /* valid but outside the instantiated shapes      */
+  RADAR_EHIP = 4,         /* a HIP launch failed; see radar_last_error()    */
+  RADAR_EWORKSPACE = 5    /* workspace null or smaller than required        */
+} radar_status;
+
+typedef enum { RADAR_F32 = 0, RADAR_BF16 = 1 } radar_dtype;
+
+typedef struct {
+  int32_t batch;       /* B >= 1                                            */
+  int32_t n_q_heads;   /* Hq; Hq % Hkv == 0, G = Hq / Hkv in {1, 2, 4, 8}   */
+  int32_t n_kv_heads;  /* Hkv >= 1                                          */
+  int32_t head_dim;    /* d in {64, 128}                                    */
+  int32_t n_features;  /* n in {64, 128, 256, 512}                          */
+  int32_t seg_len;     /* c >= 1 (any value; need not divide anything)      */
+  int32_t window;      /* w >= 0                                            */
+  int64_t capacity;    /* token rows per head in K and V (>= 1)             */
+  radar_dtype kv_dtype;
+} radar_config;
+
+/* Index build (Eq. 4 and Eq. 5; Algorithm 1's restructuring step that
+ * pre-computes the segment embeddings). Writes summaries rows
+ * 0 .. floor(t / c) - 1 of every (b, kv head) from K[:, :, 0:t). Rows at and
+ * beyond floor(t / c) are not touched. Requires 1 <= t <= capacity. */
+radar_status radar_build_index(const radar_config* cfg, const void* K,
+                               const float* omega, int64_t t,
+                               float* summaries, hipStream_t stream);
+
+/* Append one token (Algorithm 1: the new key joins the buffer W). Writes
+ * k_new / v_new ([B][Hkv][d]) to row t of K / V. If the row completes a
+ * segment ((t + 1) % c == 0) the summary of segment (t + 1) / c - 1 is
+ * computed with exactly the code path of radar_build_index, so appending
+ * and rebuilding give bit-identical summaries. Requires 0 <= t < capacity;
+ * the caller's context length becomes t + 1. */
+radar_status radar_append(const radar_config* cfg, void* K, void* V,
+                          const void* k_new, const void* v_new,
+                          const float* omega, int64_t t, float* summaries,
+                          hipStream_t stream);
+
+/* Decode one query per (b, q head) (Algorithm 1, querying step): phi(q)
+ * (Eq. 4), scores of the n_cand candidate segments (Eq. 6), top-k, and exact
+ * softmax attention (Eq. 1-2) over the selected segments plus W, with the
+ * softmax scale 1/sqrt(d). t is the context length including the query's own
+ * token (append first, then decode). k >= 1.
+ * `selected` and `scores` may be NULL. `workspace` must hold at least
+ * radar_decode_workspace_bytes(cfg, k) bytes; its contents on entry do not
+ * matter and it must not be used by another call at the same time. */
+radar_status radar_decode(const radar_config* cfg, const void* q,
+                          const void* K, const void* V, const float* omega,
+                          const float* summaries, int64_t t, int32_t k,
+                          void* out, int32_t* selected, float* scores,
+                          void* workspace, size_t workspace_bytes,
+                          hipStream_t stream);
+
+/* Scratch bytes radar_decode and radar_attend_selected need for this shape
+ * and k (0 if cfg is invalid). */
+size_t radar_decode_workspace_bytes(const radar_config* cfg, int32_t k);
+
+/* Exact attention over caller-chosen segments (the last step of Algorithm 1
+ * with the selection supplied): selected [B][Hq][k] holds segment ids, -1
+ * for none; ids outside [0, n_cand) are ignored. Each query head attends the
+ * union of its group's ids plus W, exactly as radar_decode does. */
+radar_status radar_attend_selected(const radar_config* cfg, const void* q,
+                                   const void* K, const void* V,
+                                   const int32_t* selected, int32_t k,
+                                   int64_t t, void* out, void* workspace,
+                                   size_t workspace_bytes,
+                                   hipStream_t stream);
+
+/* Kernel kinds reported by the measurement hook below. */
+typedef enum {
+  RADAR_K_APPEND = 0,   /* k/v row write                                 */
+  RADAR_K_BUILD = 1,    /* segment summaries (build or segment close)    */
+  RADAR_K_PHI_Q = 2,    /* phi(q)                                        */
+  RADAR_K_SCORE = 3,    /* Eq. 6 segment scores                          */
+  RADAR_K_TOPK = 4,     /* top-k and per-kv-head union                   */
+  RADAR_K_ATTEND = 5,   /* gather-attention partials                     */
+  RADAR_K_COMBINE = 6,  /* merge of the partials                         */
+  RADAR_K_COUNT = 7
+} radar_kernel;
+
+/* Measurement hook (not part of the method). While enabled on the calling
+ * host thread, every kernel the library launches is bracketed by a HIP event
+ * pair recorded at that kernel's start and end on its stream. Results do not
+ * change. radar_profile_enable(0) stops recording; pending records are kept
+ * until read. */
+radar_status radar_profile_enable(int32_t on);
+
+/* Waits for the recorded kernels, adds their durations per radar_kernel kind
+ * into ms[0 .. n) and their launch counts into launches[0 .. n) (n >=
+ * RADAR_K_COUNT; both arrays are host memory, zeroed by this call), and
+ * releases the records. */
+radar_status radar_profile_read(double* ms, int64_t* launches, int32_t n);
+
+/* Static text for a status code. */
+const char* radar_status_string(radar_status status);
+
+/* Text of the last HIP error seen by this thread ("" if none). */
+const char* radar_last_error(void);
+
+/* RADAR_ABI_VERSION of the built library. */
+int32_t radar_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RADAR_H */

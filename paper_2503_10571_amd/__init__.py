@@ -1,0 +1,245 @@
+"""Radar decode path on MI355X: Python binding of the C ABI in include/radar.h.
+
+The binding only marshals arguments: every step of the path (index build,
+append, phi(q), segment scores, top-k, union, gather-attention, combine) runs
+in the HIP kernels of libradar.so. torch supplies device memory and the
+stream (the current torch stream of the tensors' device). There is no CPU
+fallback: a missing library raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libradar.so")
+
+RADAR_F32, RADAR_BF16 = 0, 1
+STATUS = {0: "ok", 1: "invalid argument", 2: "position outside the cache capacity",
+          3: "shape not supported by this build", 4: "HIP launch failed",
+          5: "workspace missing or too small"}
+
+
+class RadarError(RuntimeError):
+    def __init__(self, fn, status, detail=""):
+        self.status = status
+        msg = f"{fn}: {STATUS.get(status, status)}"
+        if detail:
+            msg += f" ({detail})"
+        super().__init__(msg)
+
+
+class _Config(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
+                ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("n_features", ctypes.c_int32), ("seg_len", ctypes.c_int32),
+                ("window", ctypes.c_int32), ("capacity", ctypes.c_int64),
+                ("kv_dtype", ctypes.c_int32)]
+
+
+@dataclasses.dataclass(frozen=True)
+class Config:
+    """Shape of one Radar layer (mirrors radar_config)."""
+    batch: int
+    n_q_heads: int
+    n_kv_heads: int
+    head_dim: int
+    n_features: int
+    seg_len: int
+    window: int
+    capacity: int
+    dtype: torch.dtype = torch.bfloat16
+
+    def c_struct(self) -> _Config:
+        dt = {torch.float32: RADAR_F32, torch.bfloat16: RADAR_BF16}[self.dtype]
+        return _Config(self.batch, self.n_q_heads, self.n_kv_heads,
+                       self.head_dim, self.n_features, self.seg_len,
+                       self.window, self.capacity, dt)
+
+    @property
+    def summary_rows(self) -> int:
+        return self.capacity // self.seg_len
+
+
+_lib = None
+_P = ctypes.c_void_p
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libradar.so (raises if it was not built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                f"{LIB_PATH} is missing: build it with "
+                "`python -m paper_2503_10571_amd._build` (hipcc, gfx950)")
+        L = ctypes.CDLL(LIB_PATH)
+        cfgp = ctypes.POINTER(_Config)
+        i64, i32, sz = ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
+        L.radar_build_index.argtypes = [cfgp, _P, _P, i64, _P, _P]
+        L.radar_append.argtypes = [cfgp, _P, _P, _P, _P, _P, i64, _P, _P]
+        L.radar_decode.argtypes = [cfgp, _P, _P, _P, _P, _P, i64, i32, _P, _P,
+                                   _P, _P, sz, _P]
+        L.radar_decode_workspace_bytes.argtypes = [cfgp, i32]
+        L.radar_decode_workspace_bytes.restype = sz
+        L.radar_attend_selected.argtypes = [cfgp, _P, _P, _P, _P, i32, i64, _P,
+                                            _P, sz, _P]
+        L.radar_status_string.argtypes = [ctypes.c_int]
+        L.radar_status_string.restype = ctypes.c_char_p
+        L.radar_last_error.restype = ctypes.c_char_p
+        L.radar_abi_version.restype = ctypes.c_int32
+        L.radar_profile_enable.argtypes = [i32]
+        L.radar_profile_read.argtypes = [ctypes.POINTER(ctypes.c_double),
+                                         ctypes.POINTER(ctypes.c_int64), i32]
+        for fn in ("radar_build_index", "radar_append", "radar_decode",
+                   "radar_attend_selected", "radar_profile_enable",
+                   "radar_profile_read"):
+            getattr(L, fn).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _ptr(x):
+    return None if x is None else ctypes.c_void_p(x.data_ptr())
+
+
+def _stream(x):
+    return ctypes.c_void_p(torch.cuda.current_stream(x.device).cuda_stream)
+
+
+def _check(fn, st):
+    if st != 0:
+        detail = lib().radar_last_error().decode() if st == 4 else ""
+        raise RadarError(fn, st, detail)
+
+
+def _need(x, dtype, name):
+    if not x.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if x.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {x.dtype}")
+    if not x.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def workspace_bytes(cfg: Config, k: int) -> int:
+    return int(lib().radar_decode_workspace_bytes(ctypes.byref(cfg.c_struct()), k))
+
+
+def new_workspace(cfg: Config, k: int, device) -> torch.Tensor:
+    n = workspace_bytes(cfg, k)
+    if n == 0:
+        raise RadarError("radar_decode_workspace_bytes", 1)
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def new_summaries(cfg: Config, device) -> torch.Tensor:
+    return torch.zeros(cfg.batch, cfg.n_kv_heads, max(1, cfg.summary_rows),
+                       cfg.n_features, dtype=torch.float32, device=device)
+
+
+def build_index(cfg: Config, K, omega, t: int, summaries) -> None:
+    """radar_build_index: summaries of the floor(t / c) full segments."""
+    _need(K, cfg.dtype, "K"); _need(omega, torch.float32, "omega")
+    _need(summaries, torch.float32, "summaries")
+    _check("radar_build_index", lib().radar_build_index(
+        ctypes.byref(cfg.c_struct()), _ptr(K), _ptr(omega), t, _ptr(summaries),
+        _stream(K)))
+
+
+def append(cfg: Config, K, V, k_new, v_new, omega, t: int, summaries) -> None:
+    """radar_append: write row t; refresh the summary of a segment it fills."""
+    for x, nm in ((K, "K"), (V, "V"), (k_new, "k_new"), (v_new, "v_new")):
+        _need(x, cfg.dtype, nm)
+    _need(omega, torch.float32, "omega"); _need(summaries, torch.float32, "summaries")
+    _check("radar_append", lib().radar_append(
+        ctypes.byref(cfg.c_struct()), _ptr(K), _ptr(V), _ptr(k_new), _ptr(v_new),
+        _ptr(omega), t, _ptr(summaries), _stream(K)))
+
+
+def decode(cfg: Config, q, K, V, omega, summaries, t: int, k: int, out=None,
+           selected=None, scores=None, workspace=None):
+    """radar_decode: one query per (b, q head). Returns out (and writes the
+    optional selected / scores tensors)."""
+    for x, nm in ((q, "q"), (K, "K"), (V, "V")):
+        _need(x, cfg.dtype, nm)
+    _need(omega, torch.float32, "omega"); _need(summaries, torch.float32, "summaries")
+    if out is None:
+        out = torch.empty_like(q)
+    if workspace is None:
+        workspace = new_workspace(cfg, k, q.device)
+    if selected is not None:
+        _need(selected, torch.int32, "selected")
+    if scores is not None:
+        _need(scores, torch.float32, "scores")
+    _check("radar_decode", lib().radar_decode(
+        ctypes.byref(cfg.c_struct()), _ptr(q), _ptr(K), _ptr(V), _ptr(omega),
+        _ptr(summaries), t, k, _ptr(out), _ptr(selected), _ptr(scores),
+        _ptr(workspace), workspace.numel(), _stream(q)))
+    return out
+
+
+def attend_selected(cfg: Config, q, K, V, selected, t: int, out=None,
+                    workspace=None):
+    """radar_attend_selected: exact attention over given segment ids plus W."""
+    for x, nm in ((q, "q"), (K, "K"), (V, "V")):
+        _need(x, cfg.dtype, nm)
+    _need(selected, torch.int32, "selected")
+    k = selected.shape[-1]
+    if out is None:
+        out = torch.empty_like(q)
+    if workspace is None:
+        workspace = new_workspace(cfg, k, q.device)
+    _check("radar_attend_selected", lib().radar_attend_selected(
+        ctypes.byref(cfg.c_struct()), _ptr(q), _ptr(K), _ptr(V), _ptr(selected),
+        k, t, _ptr(out), _ptr(workspace), workspace.numel(), _stream(q)))
+    return out
+
+
+KERNELS = ("append", "build", "phi_q", "score", "topk", "attend", "combine")
+
+
+def profile_enable(on: bool) -> None:
+    """Bracket every library kernel with a HIP event pair (measurement only)."""
+    _check("radar_profile_enable", lib().radar_profile_enable(1 if on else 0))
+
+
+def profile_read() -> dict:
+    """{kernel: (total ms, launches)} of the kernels recorded since the last
+    read; waits for them to finish."""
+    n = len(KERNELS)
+    ms = (ctypes.c_double * n)()
+    cnt = (ctypes.c_int64 * n)()
+    _check("radar_profile_read", lib().radar_profile_read(ms, cnt, n))
+    return {k: (ms[i], cnt[i]) for i, k in enumerate(KERNELS)}
+
+
+class RadarLayer:
+    """Device state of one Radar layer: K/V cache, summaries, Omega and a
+    decode workspace, driven through the C ABI (append, then decode)."""
+
+    def __init__(self, cfg: Config, omega, K=None, V=None, t: int = 0,
+                 top_k: int = 16, device="cuda"):
+        self.cfg, self.k = cfg, top_k
+        shape = (cfg.batch, cfg.n_kv_heads, cfg.capacity, cfg.head_dim)
+        self.K = K if K is not None else torch.zeros(shape, dtype=cfg.dtype, device=device)
+        self.V = V if V is not None else torch.zeros(shape, dtype=cfg.dtype, device=device)
+        self.omega = omega
+        self.summaries = new_summaries(cfg, self.K.device)
+        self.workspace = new_workspace(cfg, top_k, self.K.device)
+        self.t = t
+        if t > 0:
+            build_index(cfg, self.K, omega, t, self.summaries)
+
+    def append(self, k_new, v_new):
+        append(self.cfg, self.K, self.V, k_new, v_new, self.omega, self.t,
+               self.summaries)
+        self.t += 1
+
+    def decode(self, q, out=None, selected=None, scores=None):
+        return decode(self.cfg, q, self.K, self.V, self.omega, self.summaries,
+                      self.t, self.k, out=out, selected=selected, scores=scores,
+                      workspace=self.workspace)

@@ -1,0 +1,183 @@
+"""Drive the HIP path through the C ABI and compare it with the fp64 oracle.
+
+The HIP side runs through paper_2503_10571_amd (ctypes -> libradar.so); the
+oracle side is oracle.radar_oracle on float64 copies of the same seeded inputs
+(workloads.make_inputs). The two share nothing but those inputs.
+
+Acceptance rules:
+  * selected segments: equal as sets to the oracle's top-k_eff, except that
+    segments whose oracle score lies within 1e-5 (relative) of the oracle's
+    k-th score may be swapped for one another;
+  * outputs: per (b, q head) max_i |o_i - o*_i| / max_i |o*_i| <= 2e-3 (fp32)
+    or 1e-2 (bf16), where o* is the oracle's exact attention over the union
+    the GPU selected plus the window (identical to the oracle's own output
+    whenever the sets agree);
+  * scores of the selected segments: relative error against the oracle's
+    Eq. 6 values, reported and bounded;
+  * summaries: relative error per element <= 1e-4.
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+
+import numpy as np
+import torch
+
+import paper_2503_10571_amd as radar
+import workloads
+from oracle import radar_oracle as orc
+
+TIE_BAND = 1e-5
+OUT_TOL = {"f32": 2e-3, "bf16": 1e-2}
+SCORE_TOL = 2e-5
+SUMM_TOL = 1e-4
+
+
+def config_of(wl: workloads.Workload, capacity: int) -> radar.Config:
+    return radar.Config(wl.batch, wl.n_q_heads, wl.n_kv_heads, wl.head_dim,
+                        wl.n_features, wl.seg_len, wl.window, capacity,
+                        wl.torch_dtype())
+
+
+def f64(x: torch.Tensor) -> np.ndarray:
+    return x.detach().float().cpu().double().numpy()
+
+
+def check_selection(gpu_sel, ora_scores, k_eff, n_cand):
+    """Tie-band set check for one query head. gpu_sel: the k ids (-1 pad)."""
+    sel = [int(s) for s in gpu_sel if s >= 0]
+    assert len(sel) == k_eff, (sel, k_eff)
+    assert len(set(sel)) == k_eff, sel
+    assert all(0 <= s < n_cand for s in sel), sel
+    assert all(s == -1 for s in gpu_sel[k_eff:])
+    if k_eff == 0:
+        return 0
+    order = orc.top_segments(ora_scores, k_eff)
+    s_k = ora_scores[order[-1]]
+    hi, lo = s_k * (1 + TIE_BAND), s_k * (1 - TIE_BAND)
+    must = {int(s) for s in np.nonzero(ora_scores > hi)[0]}
+    assert must <= set(sel), ("missed", sorted(must - set(sel)))
+    bad = [s for s in sel if ora_scores[s] < lo]
+    assert not bad, ("outside band", bad, [ora_scores[s] for s in bad], s_k)
+    return len(set(sel) ^ {int(s) for s in order})
+
+
+def rel_inf(a, b):
+    return float(np.max(np.abs(a - b)) / max(np.max(np.abs(b)), 1e-30))
+
+
+@dataclasses.dataclass
+class Stats:
+    heads: int = 0
+    max_out_err: float = 0.0
+    max_score_err: float = 0.0
+    max_summ_err: float = 0.0
+    band_swaps: int = 0
+
+    def merge_out(self, e):
+        self.max_out_err = max(self.max_out_err, e)
+
+
+class Episode:
+    """One workload run: build the index at t0, then `steps` x (append,
+    decode). Oracle checks on the sampled (batch, kv head) groups."""
+
+    def __init__(self, wl, steps, groups=None, device="cuda"):
+        self.wl = wl
+        self.steps = steps
+        self.inp = workloads.make_inputs(wl, device, steps=steps)
+        self.cfg = config_of(wl, wl.t0 + steps)
+        B, Hkv = wl.batch, wl.n_kv_heads
+        self.groups = groups if groups is not None else \
+            [(b, g) for b in range(B) for g in range(Hkv)]
+        self.omega64 = f64(self.inp.omega)
+        self.keys = {}
+        self.vals = {}
+        self.summ64 = {}
+        for (b, g) in self.groups:
+            kk = f64(self.inp.keys_at(steps, b, g))
+            self.keys[(b, g)] = kk
+            self.vals[(b, g)] = f64(self.inp.values_at(steps, b, g))
+            self.summ64[(b, g)] = orc.segment_summaries(kk, self.omega64,
+                                                        wl.seg_len)
+        self.stats = Stats()
+
+    def run(self, check_steps=None):
+        wl, inp, cfg = self.wl, self.inp, self.cfg
+        dev = inp.K.device
+        K, V = inp.K.clone(), inp.V.clone()
+        summ = radar.new_summaries(cfg, dev)
+        radar.build_index(cfg, K, inp.omega, wl.t0, summ)
+        self.check_summaries(summ, wl.t0)
+        ws = radar.new_workspace(cfg, wl.top_k, dev)
+        sel = torch.empty(wl.batch, wl.n_q_heads, wl.top_k, dtype=torch.int32,
+                          device=dev)
+        sc = torch.empty(wl.batch, wl.n_q_heads, wl.top_k, dtype=torch.float32,
+                         device=dev)
+        out = torch.empty_like(inp.q[0])
+        t = wl.t0
+        for i in range(self.steps):
+            radar.append(cfg, K, V, inp.k_new[i].contiguous(),
+                         inp.v_new[i].contiguous(), inp.omega, t, summ)
+            t += 1
+            q = inp.q[i].contiguous()
+            radar.decode(cfg, q, K, V, inp.omega, summ, t, wl.top_k, out=out,
+                         selected=sel, scores=sc, workspace=ws)
+            if check_steps is None or i in check_steps:
+                torch.cuda.synchronize()
+                self.check_step(i, t, q, out, sel, sc)
+        self.check_summaries(summ, t)
+        self.K, self.V, self.summ = K, V, summ
+        return self.stats
+
+    def check_summaries(self, summ, t):
+        c = self.wl.seg_len
+        n_seg = t // c
+        for (b, g) in self.groups:
+            got = f64(summ[b, g, :n_seg])
+            ref = self.summ64[(b, g)][:n_seg]
+            err = float(np.max(np.abs(got - ref) / np.abs(ref))) if n_seg else 0.0
+            self.stats.max_summ_err = max(self.stats.max_summ_err, err)
+            assert err <= SUMM_TOL, (b, g, err)
+
+    def check_step(self, i, t, q, out, sel, sc):
+        wl = self.wl
+        G, c, d = wl.group, wl.seg_len, wl.head_dim
+        ws, n_cand = orc.window_split(t, c, wl.window)
+        k_eff = min(wl.top_k, n_cand)
+        q64 = f64(q)
+        out64 = f64(out)
+        sel_np = sel.cpu().numpy()
+        sc_np = sc.cpu().numpy()
+        for (b, g) in self.groups:
+            union = set()
+            for h in range(g * G, (g + 1) * G):
+                phi_q = orc.random_features(q64[b, h], self.omega64)
+                ora_sc = orc.segment_scores(phi_q, self.summ64[(b, g)][:n_cand])
+                self.stats.band_swaps += check_selection(sel_np[b, h], ora_sc,
+                                                         k_eff, n_cand)
+                picks = [int(s) for s in sel_np[b, h, :k_eff]]
+                union.update(picks)
+                if k_eff:
+                    ref = ora_sc[picks]
+                    err = float(np.max(np.abs(sc_np[b, h, :k_eff] - ref) / ref))
+                    self.stats.max_score_err = max(self.stats.max_score_err, err)
+                    assert err <= SCORE_TOL, (i, b, h, err)
+                    got_order = sc_np[b, h, :k_eff]
+                    assert np.all(got_order[:-1] >= got_order[1:]), got_order
+            toks = orc.attended_tokens(sorted(union), c, ws, t)
+            for h in range(g * G, (g + 1) * G):
+                ref = orc.attend(q64[b, h], self.keys[(b, g)],
+                                 self.vals[(b, g)], toks)
+                e = rel_inf(out64[b, h], ref)
+                self.stats.merge_out(e)
+                assert e <= OUT_TOL[wl.dtype], (i, b, h, e)
+                self.stats.heads += 1
+
+
+def sample_groups(wl, n, seed=0):
+    rng = np.random.default_rng(seed)
+    allg = [(b, g) for b in range(wl.batch) for g in range(wl.n_kv_heads)]
+    idx = rng.choice(len(allg), size=min(n, len(allg)), replace=False)
+    return [allg[i] for i in sorted(idx)]

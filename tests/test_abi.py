@@ -1,0 +1,131 @@
+"""The C ABI on the CPU: the library loads, exports every function that
+include/radar.h declares, sizes workspaces, and rejects bad arguments with
+the documented status codes before anything reaches the GPU (every call here
+fails validation, so no kernel is launched)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2503_10571_amd as radar
+from paper_2503_10571_amd import _build
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "radar.h")
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(radar.LIB_PATH):
+        _build.build_library()
+    return radar.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(radar_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(L):
+    names = declared_functions()
+    assert {"radar_build_index", "radar_append", "radar_decode",
+            "radar_decode_workspace_bytes", "radar_attend_selected",
+            "radar_status_string", "radar_last_error",
+            "radar_abi_version"} <= set(names)
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_version_and_strings(L):
+    assert L.radar_abi_version() == 1
+    for st in range(6):
+        assert L.radar_status_string(st).decode()
+    assert L.radar_last_error() is not None
+
+
+def _cfg(**kw):
+    base = dict(batch=8, n_q_heads=32, n_kv_heads=32, head_dim=128,
+                n_features=256, seg_len=256, window=256, capacity=131584)
+    base.update(kw)
+    return radar.Config(**base)
+
+
+def test_workspace_bytes(L):
+    import torch
+    cfg = _cfg()
+    n16 = radar.workspace_bytes(cfg, 16)
+    n32 = radar.workspace_bytes(cfg, 32)
+    assert 0 < n16 < n32
+    # phi(q) + scores + union + partials: a few MB at the 128K shape
+    assert n16 < 64 << 20
+    assert radar.workspace_bytes(cfg, 0) == 0
+    assert radar.workspace_bytes(cfg, 257) == 0
+    assert radar.workspace_bytes(_cfg(n_q_heads=24, n_kv_heads=8), 16) == 0  # G=3
+    assert radar.workspace_bytes(_cfg(head_dim=96), 16) == 0
+    assert radar.workspace_bytes(_cfg(n_features=100), 16) == 0
+    assert radar.workspace_bytes(_cfg(dtype=torch.float32), 16) > 0
+
+
+def _P(v):
+    return ctypes.c_void_p(v)
+
+
+def test_validation_before_launch(L):
+    cfg = _cfg().c_struct()
+    good = _P(0x1000)
+    odd = _P(0x1008)
+    null = None
+    by = ctypes.byref
+    # null config / pointers
+    assert L.radar_build_index(None, good, good, 10, good, None) == 1
+    assert L.radar_build_index(by(cfg), null, good, 10, good, None) == 1
+    # misaligned
+    assert L.radar_build_index(by(cfg), odd, good, 10, good, None) == 1
+    # t outside [1, capacity]
+    assert L.radar_build_index(by(cfg), good, good, 0, good, None) == 2
+    assert L.radar_build_index(by(cfg), good, good, 131585, good, None) == 2
+    # append position outside [0, capacity)
+    assert L.radar_append(by(cfg), good, good, good, good, good, 131584, good,
+                          None) == 2
+    assert L.radar_append(by(cfg), good, good, good, good, good, -1, good,
+                          None) == 2
+    ws = L.radar_decode_workspace_bytes(by(cfg), 16)
+    args = [by(cfg), good, good, good, good, good]
+    # k out of range
+    assert L.radar_decode(*args, 1000, 0, good, None, None, good, ws, None) == 3
+    assert L.radar_decode(*args, 1000, 300, good, None, None, good, ws, None) == 3
+    # t out of range
+    assert L.radar_decode(*args, 0, 16, good, None, None, good, ws, None) == 2
+    # workspace missing / too small
+    assert L.radar_decode(*args, 1000, 16, good, None, None, None, ws, None) == 5
+    assert L.radar_decode(*args, 1000, 16, good, None, None, good, ws - 1,
+                          None) == 5
+    # too many candidate segments for the top-k stage
+    big = _cfg(seg_len=16, window=16, capacity=1 << 20).c_struct()
+    wsb = L.radar_decode_workspace_bytes(by(big), 16)
+    assert L.radar_decode(by(big), good, good, good, good, good, 40000, 16,
+                          good, None, None, good, wsb, None) == 3
+    # bad shapes
+    for bad in (_cfg(batch=0), _cfg(n_q_heads=30), _cfg(seg_len=0),
+                _cfg(window=-1), _cfg(capacity=0)):
+        assert L.radar_build_index(by(bad.c_struct()), good, good, 1, good,
+                                   None) == 1
+    for bad in (_cfg(head_dim=256), _cfg(n_features=1024),
+                _cfg(n_q_heads=96, n_kv_heads=32)):
+        assert L.radar_build_index(by(bad.c_struct()), good, good, 1, good,
+                                   None) == 3
+    # attend_selected
+    assert L.radar_attend_selected(by(cfg), good, good, good, null, 4, 100,
+                                   good, good, ws, None) == 1
+    assert L.radar_attend_selected(by(cfg), good, good, good, good, 0, 100,
+                                   good, good, ws, None) == 3
+
+
+def test_product_path_has_no_fallback(monkeypatch, tmp_path):
+    """Without the built library the binding raises instead of computing."""
+    monkeypatch.setattr(radar, "_lib", None)
+    monkeypatch.setattr(radar, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(RuntimeError, match="missing"):
+        radar.lib()

@@ -1,0 +1,235 @@
+"""HIP path vs the fp64 oracle, through the C ABI, on the same seeded inputs.
+
+Every case builds the index at t0 with radar_build_index, then runs
+append + decode steps and checks selections (tie band 1e-5), selected scores,
+outputs (2e-3 fp32 / 1e-2 bf16) and summaries against the oracle. The
+workloads are the five decode configurations of the method's long-context
+setting, checked in full where the oracle is fast enough and on sampled
+(batch, kv head) groups at full size otherwise, plus edge cases: no candidate
+segments, every segment selected, empty window, segment lengths that are not
+multiples of the 64-token tile, grouped-query attention with G = 2, 4, 8,
+d = 64 / 128 in both dtypes, n from 64 to 512.
+"""
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+sys.path.insert(0, os.path.dirname(__file__))
+import _harness as H  # noqa: E402
+
+import paper_2503_10571_amd as radar  # noqa: E402
+import workloads  # noqa: E402
+from workloads import Workload, WORKLOADS  # noqa: E402
+from oracle import radar_oracle as orc  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+
+def _announce(name):
+    print(f"[case] {name}", flush=True)
+
+
+def _run(wl, steps, groups=None, check_steps=None):
+    _announce(f"{wl.name} B{wl.batch} Hq{wl.n_q_heads}/{wl.n_kv_heads} "
+              f"d{wl.head_dim} t0={wl.t0} c={wl.seg_len} k={wl.top_k} "
+              f"n={wl.n_features} w={wl.window} {wl.dtype} steps={steps}")
+    ep = H.Episode(wl, steps, groups=groups)
+    st = ep.run(check_steps=check_steps)
+    print(f"  heads={st.heads} out_err={st.max_out_err:.2e} "
+          f"score_err={st.max_score_err:.2e} summ_err={st.max_summ_err:.2e} "
+          f"band_swaps={st.band_swaps}", flush=True)
+    assert st.heads > 0
+    return ep
+
+
+# --------------------------------------------------------------------------
+# the five workloads
+# --------------------------------------------------------------------------
+def test_tiny_full():
+    """Tiny single-layer decode, fp32, all 32 steps, every head."""
+    _run(WORKLOADS["tiny"], 32)
+
+
+def test_llama2_16k_full_with_close():
+    """Llama-2-7B-shaped layer at 16K, bf16: 130 steps (a segment closes at
+    t = 16512), every head."""
+    wl = WORKLOADS["llama2_16k"]
+    _run(wl, 130, check_steps=set(range(0, 130, 8)) | {126, 127, 128, 129})
+
+
+def test_mha_128k_scaled():
+    wl = WORKLOADS["mha_128k"].scaled(name="mha_128k_s", batch=2, n_q_heads=4,
+                                      n_kv_heads=4, t0=12800)
+    _run(wl, 260, check_steps={0, 1, 2, 254, 255, 256, 259})
+
+
+def test_gqa_64k_scaled():
+    wl = WORKLOADS["gqa_64k"].scaled(name="gqa_64k_s", batch=2, n_q_heads=8,
+                                     n_kv_heads=2, t0=16384)
+    _run(wl, 258, check_steps={0, 1, 255, 256, 257})
+
+
+def test_gqa_512k_scaled():
+    wl = WORKLOADS["gqa_512k"].scaled(name="gqa_512k_s", n_q_heads=8,
+                                      n_kv_heads=2, t0=36200)
+    # c = 724: a segment closes at t = 36924 (step 723)
+    _run(wl, 726, check_steps={0, 1, 400, 722, 723, 724, 725})
+
+
+@pytest.mark.parametrize("name,steps,ngroups", [
+    ("mha_128k", 3, 3), ("gqa_64k", 3, 3), ("gqa_512k", 3, 2)])
+def test_full_size_sampled(name, steps, ngroups):
+    """Full-size workloads, the launch configuration the benchmark times;
+    oracle checks on sampled (batch, kv head) groups."""
+    wl = WORKLOADS[name]
+    _run(wl, steps, groups=H.sample_groups(wl, ngroups, seed=1))
+    torch.cuda.empty_cache()
+
+
+# --------------------------------------------------------------------------
+# edge cases
+# --------------------------------------------------------------------------
+def _edge(name, **kw):
+    base = dict(batch=1, n_q_heads=2, n_kv_heads=2, head_dim=128, t0=300,
+                seg_len=16, top_k=3, n_features=128, window=32, dtype="bf16",
+                steps=1, keys="gauss_scaled", planted=2)
+    base.update(kw)
+    return Workload(name, **base)
+
+
+EDGES = [
+    # t <= w: no candidate segment, the window is everything
+    _edge("window_only", t0=20, window=64, seg_len=16),
+    # k >= n_cand: every candidate selected, exact full attention
+    _edge("all_selected", t0=150, window=16, seg_len=16, top_k=64),
+    # w = 0: Algorithm 1's buffer; t0 multiple of c gives W = {new token}
+    _edge("w0", t0=256, window=0, seg_len=32, top_k=2),
+    # segment lengths that are not multiples of the 64-token tile
+    _edge("c100", t0=1000, window=100, seg_len=100, top_k=3),
+    _edge("c65", t0=700, window=65, seg_len=65, top_k=4, dtype="f32",
+          head_dim=64, n_features=64),
+    _edge("c1", t0=900, window=5, seg_len=1, top_k=7, n_features=64),
+    # grouped-query attention
+    _edge("gqa2", n_q_heads=4, n_kv_heads=2, t0=2000, seg_len=64, window=64,
+          top_k=5, keys="clustered"),
+    _edge("gqa8", n_q_heads=16, n_kv_heads=2, t0=3000, seg_len=128,
+          window=128, top_k=4, keys="clustered"),
+    # head dims / dtypes / feature counts
+    _edge("d64_bf16", head_dim=64, t0=1500, seg_len=64, window=64,
+          n_features=256),
+    _edge("d128_f32", head_dim=128, t0=1500, seg_len=64, window=64,
+          dtype="f32", n_features=512),
+    _edge("n512_b3", batch=3, t0=1200, seg_len=48, window=50, n_features=512,
+          top_k=6, keys="clustered"),
+]
+
+
+@pytest.mark.parametrize("wl", EDGES, ids=[w.name for w in EDGES])
+def test_edge(wl):
+    steps = 70 if wl.seg_len <= 64 else 8
+    _run(wl, steps)
+
+
+# --------------------------------------------------------------------------
+# properties
+# --------------------------------------------------------------------------
+def test_append_equals_rebuild_bitwise():
+    """Summaries grown by appends equal a one-shot rebuild bit for bit (the
+    segment close runs the build kernel's code path)."""
+    wl = _edge("grow", t0=500, seg_len=48, window=48, n_features=256,
+               keys="clustered", batch=2)
+    ep = _run(wl, 100)
+    t = wl.t0 + 100
+    fresh = radar.new_summaries(ep.cfg, ep.K.device)
+    radar.build_index(ep.cfg, ep.K, ep.inp.omega, t, fresh)
+    torch.cuda.synchronize()
+    n_seg = t // wl.seg_len
+    assert torch.equal(fresh[:, :, :n_seg], ep.summ[:, :, :n_seg])
+
+
+def test_attend_selected_matches_oracle_selection():
+    """The gather-attention stage on the oracle's own selection."""
+    wl = _edge("hook", n_q_heads=8, n_kv_heads=2, t0=3000, seg_len=96,
+               window=96, top_k=5, keys="clustered", n_features=256)
+    _announce("attend_selected")
+    inp = workloads.make_inputs(wl, "cuda", steps=1)
+    cfg = H.config_of(wl, wl.t0 + 1)
+    t = wl.t0
+    q = inp.q[0].contiguous()
+    om = H.f64(inp.omega)
+    ws, n_cand = orc.window_split(t, wl.seg_len, wl.window)
+    G = wl.group
+    sel = -np.ones((wl.batch, wl.n_q_heads, wl.top_k), dtype=np.int32)
+    q64 = H.f64(q)
+    summ = {}
+    for b in range(wl.batch):
+        for g in range(wl.n_kv_heads):
+            summ[(b, g)] = orc.segment_summaries(H.f64(inp.K[b, g, :t]), om,
+                                                 wl.seg_len)
+            for h in range(g * G, (g + 1) * G):
+                sc = orc.segment_scores(orc.random_features(q64[b, h], om),
+                                        summ[(b, g)][:n_cand])
+                s = orc.top_segments(sc, wl.top_k)
+                sel[b, h, :len(s)] = s
+    # plant duplicates and out-of-range ids: both must be ignored
+    sel[0, 1, -1] = sel[0, 0, 0]
+    sel[0, 2, -1] = n_cand + 3
+    out = radar.attend_selected(cfg, q, inp.K, inp.V,
+                                torch.as_tensor(sel, device="cuda"), t)
+    torch.cuda.synchronize()
+    got = H.f64(out)
+    for b in range(wl.batch):
+        for g in range(wl.n_kv_heads):
+            ids = sorted({int(s) for s in sel[b, g * G:(g + 1) * G].ravel()
+                          if 0 <= s < n_cand})
+            toks = orc.attended_tokens(ids, wl.seg_len, ws, t)
+            for h in range(g * G, (g + 1) * G):
+                ref = orc.attend(q64[b, h], H.f64(inp.K[b, g, :t]),
+                                 H.f64(inp.V[b, g, :t]), toks)
+                assert H.rel_inf(got[b, h], ref) <= 1e-2
+
+
+def test_decode_deterministic():
+    """Two decodes of the same inputs give identical bits."""
+    wl = _edge("det", n_q_heads=8, n_kv_heads=2, t0=5000, seg_len=128,
+               window=128, top_k=6, keys="clustered", n_features=256)
+    _announce("determinism")
+    inp = workloads.make_inputs(wl, "cuda", steps=1)
+    cfg = H.config_of(wl, wl.t0 + 1)
+    summ = radar.new_summaries(cfg, "cuda")
+    radar.build_index(cfg, inp.K, inp.omega, wl.t0, summ)
+    q = inp.q[0].contiguous()
+    outs, sels = [], []
+    for _ in range(2):
+        sel = torch.full((wl.batch, wl.n_q_heads, wl.top_k), 7,
+                         dtype=torch.int32, device="cuda")
+        outs.append(radar.decode(cfg, q, inp.K, inp.V, inp.omega, summ,
+                                 wl.t0, wl.top_k, selected=sel))
+        sels.append(sel)
+    torch.cuda.synchronize()
+    assert torch.equal(outs[0], outs[1])
+    assert torch.equal(sels[0], sels[1])
+
+
+def test_errors_leave_outputs_untouched():
+    """Rejected calls launch nothing."""
+    wl = _edge("err")
+    cfg = H.config_of(wl, 64)
+    K = torch.zeros(1, 2, 64, 128, dtype=torch.bfloat16, device="cuda")
+    om = torch.zeros(128, 128, device="cuda")
+    summ = torch.full((1, 2, 4, 128), 5.0, device="cuda")
+    with pytest.raises(radar.RadarError) as e:
+        radar.build_index(cfg, K, om, 65, summ)
+    assert e.value.status == 2
+    q = torch.zeros(1, 2, 128, dtype=torch.bfloat16, device="cuda")
+    out = torch.full_like(q, 3.0)
+    with pytest.raises(radar.RadarError) as e:
+        radar.decode(cfg, q, K, K, om, summ, 10, 300, out=out,
+                     workspace=torch.empty(1 << 20, dtype=torch.uint8,
+                                           device="cuda"))
+    assert e.value.status == 3
+    torch.cuda.synchronize()
+    assert bool((summ == 5.0).all()) and bool((out == 3.0).all())
