@@ -133,7 +133,8 @@ size_t radar_decode_workspace_bytes(const radar_config* cfg, int32_t k);
 /* Exact attention over caller-chosen segments (the last step of Algorithm 1
  * with the selection supplied): selected [B][Hq][k] holds segment ids, -1
  * for none; ids outside [0, n_cand) are ignored. Each query head attends the
- * union of its group's ids plus W, exactly as radar_decode does. */
+ * union of its group's ids plus W, exactly as radar_decode does (an empty
+ * union with an empty W, possible only when w = 0, gives a zero output). */
 radar_status radar_attend_selected(const radar_config* cfg, const void* q,
                                    const void* K, const void* V,
                                    const int32_t* selected, int32_t k,
@@ -143,13 +144,13 @@ radar_status radar_attend_selected(const radar_config* cfg, const void* q,
 
 /* Kernel kinds reported by the measurement hook below. */
 typedef enum {
-  RADAR_K_APPEND = 0,   /* k/v row write                                 */
-  RADAR_K_BUILD = 1,    /* segment summaries (build or segment close)    */
-  RADAR_K_PHI_Q = 2,    /* phi(q)                                        */
-  RADAR_K_SCORE = 3,    /* Eq. 6 segment scores                          */
-  RADAR_K_TOPK = 4,     /* top-k and per-kv-head union                   */
-  RADAR_K_ATTEND = 5,   /* gather-attention partials                     */
-  RADAR_K_COMBINE = 6,  /* merge of the partials                         */
+  RADAR_K_APPEND = 0,   /* k/v row write                                   */
+  RADAR_K_BUILD = 1,    /* segment summaries (build or segment close)      */
+  RADAR_K_PHI_Q = 2,    /* phi(q)                                          */
+  RADAR_K_SCORE = 3,    /* Eq. 6 segment scores                            */
+  RADAR_K_TOPK = 4,     /* top-k and per-kv-head union (or given union)    */
+  RADAR_K_ATTEND = 5,   /* gather-attention partials                       */
+  RADAR_K_COMBINE = 6,  /* merge of the partials                           */
   RADAR_K_COUNT = 7
 } radar_kernel;
 

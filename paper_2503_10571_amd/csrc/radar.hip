@@ -1,6 +1,6 @@
 // Radar decode path on MI355X (gfx950, CDNA4): kernels and the C ABI.
 //
-// Kernels (one launch each, all on the caller's stream):
+// Kernels (all on the caller's stream):
 //   k_build       segment summaries, Eq. 4 + Eq. 5: bf16/fp32 matrix-core
 //                 projection of the keys onto Omega, exp2 epilogue, mean over
 //                 the segment's tokens. Also serves the segment close of
@@ -8,13 +8,18 @@
 //   k_append      writes one k/v row per (b, kv head).
 //   k_phi_q       phi(q) of every query head, Eq. 4.
 //   k_score       Eq. 6 scores of every candidate segment: HBM-bound GEMV
-//                 over the fp32 summaries, cross-lane transpose-reduce.
+//                 over the fp32 summaries, DPP transpose-reduce.
 //   k_topk_union  per query head top-k (score desc, index asc) by wavefront
 //                 arg-max rounds; per kv head sorted union of the group.
+//   k_union_given union of caller-given selections (test hook path).
 //   k_attend      exact attention (Eq. 1-2) over the union's segments plus
 //                 the window: coalesced 16-byte gathers of K/V, fp32 online
 //                 softmax, one partial (max, sum, acc[d]) per workgroup.
 //   k_combine     log-sum-exp merge of the partials into the output.
+//
+// Stages hand data to each other only across kernel boundaries: the eight
+// L2 caches of the chip are not coherent with one another, and the fences a
+// same-kernel hand-off would need flush them.
 //
 // All softmax / feature exponentials are base 2 with log2(e) folded into the
 // scale factors: exp(x) = exp2(x * log2(e)).
@@ -27,6 +32,7 @@
 #include <cstdint>
 #include <cstdio>
 #include <cstring>
+#include <type_traits>
 #include <vector>
 
 #include "radar.h"
@@ -39,6 +45,7 @@ constexpr int kTile = 64;          // tokens per wave in k_attend / k_build
 constexpr int kMaxK = 256;         // largest k accepted
 constexpr int kMaxG = 8;           // largest query-head group
 constexpr int kMaxCand = 2048;     // largest number of candidate segments
+constexpr int kMaxWg = 1024;       // largest attention split per (b, kv head)
 
 typedef uint16_t bf16_t;           // storage type of a bfloat16 value
 typedef unsigned long long u64;   // 64-bit type of the wave shuffles
@@ -75,13 +82,13 @@ __device__ __forceinline__ void unpack16<bf16_t>(const uint4& u, float* f) {
   f[6] = bf16_lo(u.w); f[7] = bf16_hi(u.w);
 }
 
-// fp32 -> bf16, round to nearest even (finite inputs; NaN stays NaN)
+// fp32 -> bf16, round to nearest even; infinities stay infinite and NaN
+// becomes a quiet NaN (a select, not a branch)
 __device__ __forceinline__ uint32_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7f800000u) == 0x7f800000u)
-    return (u >> 16) | ((u & 0xffffu) ? 0x40u : 0u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return u >> 16;
+  const uint32_t u = __float_as_uint(f);
+  const uint32_t rounded = (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+  const uint32_t qnan = (u >> 16) | 0x40u;
+  return (u & 0x7fffffffu) > 0x7f800000u ? qnan : rounded;
 }
 __device__ __forceinline__ float round_bf16(float f) {
   return __uint_as_float(f32_to_bf16(f) << 16);
@@ -102,9 +109,73 @@ __device__ __forceinline__ float fast_exp2(float x) {
   return __builtin_amdgcn_exp2f(x);
 }
 
-// One step of a cross-lane transpose-reduce: NV values per lane, lanes that
-// differ in bit MASK exchange half of them, so afterwards v[0 .. NV/2) hold
-// pair sums and the upper/lower half kept is selected by (lane & MASK).
+// Non-temporal 16-byte loads for data read once per launch (K/V tiles, key
+// tiles, summary rows): they stream past the caches and sustain a higher
+// HBM read rate than ordinary loads on MI355X.
+typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4v_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 ld_stream(const void* p) {
+  const u32x4_t t = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+  return make_uint4(t.x, t.y, t.z, t.w);
+}
+__device__ __forceinline__ float4 ld_stream_f4(const float* p) {
+  const f32x4v_t t = __builtin_nontemporal_load(reinterpret_cast<const f32x4v_t*>(p));
+  return make_float4(t.x, t.y, t.z, t.w);
+}
+
+// ---------------------------------------------------------------------------
+// cross-lane exchanges
+// ---------------------------------------------------------------------------
+// DPP controls (GFX9): quad_perm [1,0,3,2] and [2,3,0,1] swap neighbours at
+// distance 1 and 2; row_half_mirror maps lane i of each 8-lane half-row to
+// 7 - i, row_mirror maps lane i of each 16-lane row to 15 - i;
+// row_newbcast:n copies lane n of every row to the whole row.
+constexpr int kDppQuadSwap1 = 0xB1;
+constexpr int kDppQuadSwap2 = 0x4E;
+constexpr int kDppHalfMirror = 0x141;
+constexpr int kDppMirror = 0x140;
+constexpr int kDppRowBcast0 = 0x150;
+
+// compile-time loop: f(std::integral_constant<int, I>) for I = B .. E-1
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(
+      __float_as_int(v), __float_as_int(v), CTRL, 0xf, 0xf, false));
+}
+template <int CTRL>
+__device__ __forceinline__ u64 dpp_u64(u64 v) {
+  const int lo = __builtin_amdgcn_update_dpp((int)(uint32_t)v, (int)(uint32_t)v,
+                                             CTRL, 0xf, 0xf, false);
+  const int hi = __builtin_amdgcn_update_dpp((int)(uint32_t)(v >> 32),
+                                             (int)(uint32_t)(v >> 32), CTRL,
+                                             0xf, 0xf, false);
+  return ((u64)(uint32_t)hi << 32) | (u64)(uint32_t)lo;
+}
+
+// Value of the partner lane in a pairing that differs from this lane in bit
+// MASK. Within a 16-lane row the pairings are DPP moves (mirrors for bits 3
+// and 2, quad swaps for bits 1 and 0); they are only used from the highest
+// bit down, so the lower bits still to be processed never matter.
+template <int MASK>
+__device__ __forceinline__ float partner(float x) {
+  if constexpr (MASK == 1) return dpp_f<kDppQuadSwap1>(x);
+  else if constexpr (MASK == 2) return dpp_f<kDppQuadSwap2>(x);
+  else if constexpr (MASK == 4) return dpp_f<kDppHalfMirror>(x);
+  else if constexpr (MASK == 8) return dpp_f<kDppMirror>(x);
+  else return __shfl_xor(x, MASK);
+}
+
+// One step of a cross-lane transpose-reduce: NV values per lane; paired lanes
+// (different bit MASK) keep complementary halves, chosen by their own bit
+// MASK, and add the partner's copy of the kept half.
 template <int NV, int MASK>
 __device__ __forceinline__ void halve(float* v, int lane) {
   const bool up = (lane & MASK) != 0;
@@ -112,7 +183,7 @@ __device__ __forceinline__ void halve(float* v, int lane) {
   for (int i = 0; i < NV / 2; ++i) {
     const float keep = up ? v[i + NV / 2] : v[i];
     const float send = up ? v[i] : v[i + NV / 2];
-    v[i] = keep + __shfl_xor(send, MASK);
+    v[i] = keep + partner<MASK>(send);
   }
 }
 
@@ -128,15 +199,60 @@ __device__ __forceinline__ void transpose_reduce(float* v, int lane) {
   if constexpr (NV >= 2) halve<2, 1>(v, lane);
 }
 
+// 16-lane row all-reduce (every lane of a row ends with the row's result)
+__device__ __forceinline__ float row_max(float v) {
+  v = fmaxf(v, dpp_f<kDppQuadSwap1>(v));
+  v = fmaxf(v, dpp_f<kDppQuadSwap2>(v));
+  v = fmaxf(v, dpp_f<kDppHalfMirror>(v));
+  return fmaxf(v, dpp_f<kDppMirror>(v));
+}
+__device__ __forceinline__ float row_sum(float v) {
+  v += dpp_f<kDppQuadSwap1>(v);
+  v += dpp_f<kDppQuadSwap2>(v);
+  v += dpp_f<kDppHalfMirror>(v);
+  return v + dpp_f<kDppMirror>(v);
+}
+__device__ __forceinline__ float lane_read(float v, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+// wave-wide results, uniform across the wave (rows combined by readlane)
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int m = 1; m < kWave; m <<= 1) v = fmaxf(v, __shfl_xor(v, m));
-  return v;
+  v = row_max(v);
+  return fmaxf(fmaxf(lane_read(v, 0), lane_read(v, 16)),
+               fmaxf(lane_read(v, 32), lane_read(v, 48)));
 }
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int m = 1; m < kWave; m <<= 1) v += __shfl_xor(v, m);
-  return v;
+  v = row_sum(v);
+  return (lane_read(v, 0) + lane_read(v, 16)) + (lane_read(v, 32) + lane_read(v, 48));
+}
+__device__ __forceinline__ u64 lane_read_u64(u64 v, int l) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), l);
+  return ((u64)hi << 32) | lo;
+}
+__device__ __forceinline__ u64 max_u64(u64 a, u64 b) { return a > b ? a : b; }
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, CTRL, 0xf, 0xf, false);
+}
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+  v = max(v, dpp_u32<kDppQuadSwap1>(v));
+  v = max(v, dpp_u32<kDppQuadSwap2>(v));
+  v = max(v, dpp_u32<kDppHalfMirror>(v));
+  v = max(v, dpp_u32<kDppMirror>(v));
+  const uint32_t a = (uint32_t)__builtin_amdgcn_readlane((int)v, 0);
+  const uint32_t b = (uint32_t)__builtin_amdgcn_readlane((int)v, 16);
+  const uint32_t c = (uint32_t)__builtin_amdgcn_readlane((int)v, 32);
+  const uint32_t d = (uint32_t)__builtin_amdgcn_readlane((int)v, 48);
+  return max(max(a, b), max(c, d));
+}
+__device__ __forceinline__ u64 wave_max_u64(u64 v) {
+  v = max_u64(v, dpp_u64<kDppQuadSwap1>(v));
+  v = max_u64(v, dpp_u64<kDppQuadSwap2>(v));
+  v = max_u64(v, dpp_u64<kDppHalfMirror>(v));
+  v = max_u64(v, dpp_u64<kDppMirror>(v));
+  return max_u64(max_u64(lane_read_u64(v, 0), lane_read_u64(v, 16)),
+                 max_u64(lane_read_u64(v, 32), lane_read_u64(v, 48)));
 }
 
 // ---------------------------------------------------------------------------
@@ -244,12 +360,11 @@ __global__ __launch_bounds__(256) void k_build(
 #pragma unroll
     for (int p = 0; p < CPT; ++p) {
       const int ci = p * 256 + tid;
-      const int row = ci / CPR, ch = ci % CPR;
-      if (row < pre_valid)
-        pre[p] = *reinterpret_cast<const uint4*>(
-            reinterpret_cast<const unsigned char*>(src + (int64_t)row * D) + ch * 16);
-      else
-        pre[p] = make_uint4(0u, 0u, 0u, 0u);
+      // rows past the segment re-read its last row; they are masked out
+      // of the sums (ok[] below)
+      const int row = min(ci / CPR, pre_valid - 1), ch = ci % CPR;
+      pre[p] = ld_stream(reinterpret_cast<const unsigned char*>(src + (int64_t)row * D) +
+                         ch * 16);
     }
   };
   if (item < n_items) fetch(item, 0);
@@ -359,119 +474,65 @@ __global__ __launch_bounds__(64) void k_append(T* __restrict__ K, T* __restrict_
 // ---------------------------------------------------------------------------
 // k_phi_q: phi(q) for every (b, q head), Eq. 4
 // ---------------------------------------------------------------------------
+// One workgroup per query head. 16 lanes share one Omega row (D/16 floats
+// each); a wave covers 4 rows per pass and the workgroup 16. The 16 passes of
+// a 256-feature chunk are transpose-reduced across the 16 lanes, so each lane
+// finishes one feature.
 template <typename T, int D>
 __global__ __launch_bounds__(256) void k_phi_q(const T* __restrict__ q,
                                                const float* __restrict__ omega,
-                                               float* __restrict__ phiq, int n,
-                                               float s1, float s2,
-                                               float inv_sqrt_n) {
-  __shared__ float qf[D];
-  const int64_t bhq = blockIdx.x;
+                                               float* __restrict__ phiq,
+                                               int n, float s1,
+                                               float s2, float inv_sqrt_n) {
+  constexpr int QPL = D / 16;              // q elements per lane
   const int tid = threadIdx.x;
-  if (tid < D) qf[tid] = to_f32<T>(q[bhq * D + tid]);
-  __syncthreads();
+  const int lane = tid & 63, wave = tid >> 6;
+  const int r = lane >> 4, jj = lane & 15;
+  const int64_t bhq = blockIdx.x;
+
+  float qv[QPL];
+#pragma unroll
+  for (int e = 0; e < QPL; ++e) qv[e] = to_f32<T>(q[bhq * D + jj * QPL + e]);
   float nrm = 0.f;
-#pragma unroll 8
-  for (int e = 0; e < D; ++e) nrm = fmaf(qf[e], qf[e], nrm);
-  for (int f = tid; f < n; f += 256) {
-    const float4* orow = reinterpret_cast<const float4*>(omega + (int64_t)f * D);
-    float dot = 0.f;
-#pragma unroll 4
-    for (int e4 = 0; e4 < D / 4; ++e4) {
-      float4 o = orow[e4];
-      if constexpr (sizeof(T) == 2) {
-        o.x = round_bf16(o.x); o.y = round_bf16(o.y);
-        o.z = round_bf16(o.z); o.w = round_bf16(o.w);
-      }
-      dot = fmaf(o.x, qf[4 * e4 + 0], dot);
-      dot = fmaf(o.y, qf[4 * e4 + 1], dot);
-      dot = fmaf(o.z, qf[4 * e4 + 2], dot);
-      dot = fmaf(o.w, qf[4 * e4 + 3], dot);
-    }
-    phiq[bhq * n + f] = fast_exp2(fmaf(dot, s1, -nrm * s2)) * inv_sqrt_n;
-  }
-}
+#pragma unroll
+  for (int e = 0; e < QPL; ++e) nrm = fmaf(qv[e], qv[e], nrm);
+  nrm = row_sum(nrm);
 
-// ---------------------------------------------------------------------------
-// k_score: a[h][s] = phi(q_h) . summ[s], Eq. 6
-// ---------------------------------------------------------------------------
-// Workgroup = 4 waves x 16 rows. Lane l holds features [l*FPL, (l+1)*FPL) of
-// phi(q) for the G heads of the group; each summary row is read as one
-// contiguous n*4-byte wave load, and 16 rows' partial dots are reduced across
-// the wave by a transpose-reduce (17 shuffles per 16 rows).
-template <int N, int G>
-__global__ __launch_bounds__(256) void k_score(const float* __restrict__ phiq,
-                                               const float* __restrict__ summ,
-                                               float* __restrict__ scores,
-                                               int Hq, int Hkv, int n_cand,
-                                               int64_t s_cap, int nc_cap) {
-  constexpr int FPL = N / 64;
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int64_t bh = blockIdx.y;
-  const int64_t b = bh / Hkv, hk = bh % Hkv;
-  const int row0 = blockIdx.x * 64 + wave * 16;
-  if (row0 >= n_cand) return;
-
-  float pq[G][FPL];
+  for (int c0 = 0; c0 < n; c0 += 256) {
+    float part[16];
 #pragma unroll
-  for (int g = 0; g < G; ++g) {
-    const float* src = phiq + ((b * Hq + hk * G + g) * N) + lane * FPL;
+    for (int i = 0; i < 16; ++i) {
+      // rows past n re-read row n - 1; their sums land in lanes that
+      // write nothing
+      const int row = min(c0 + i * 16 + wave * 4 + r, n - 1);
+      float a = 0.f;
+      const float* orow = omega + (int64_t)row * D + jj * QPL;
 #pragma unroll
-    for (int e = 0; e < FPL; ++e) pq[g][e] = src[e];
-  }
-  float part[G][16];
-  const float* base = summ + (bh * s_cap) * N + lane * FPL;
-#pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const int row = row0 + r;
-    float x[FPL];
-    if (row < n_cand) {
-      const float* src = base + (int64_t)row * N;
-      if constexpr (FPL % 4 == 0) {
-#pragma unroll
-        for (int e = 0; e < FPL; e += 4) {
-          const float4 v = *reinterpret_cast<const float4*>(src + e);
-          x[e] = v.x; x[e + 1] = v.y; x[e + 2] = v.z; x[e + 3] = v.w;
+      for (int e4 = 0; e4 < QPL; e4 += 4) {
+        float4 o = *reinterpret_cast<const float4*>(orow + e4);
+        if constexpr (sizeof(T) == 2) {
+          o.x = round_bf16(o.x); o.y = round_bf16(o.y);
+          o.z = round_bf16(o.z); o.w = round_bf16(o.w);
         }
-      } else if constexpr (FPL == 2) {
-        const float2 v = *reinterpret_cast<const float2*>(src);
-        x[0] = v.x; x[1] = v.y;
-      } else {
-        x[0] = src[0];
+        a = fmaf(o.x, qv[e4], a);
+        a = fmaf(o.y, qv[e4 + 1], a);
+        a = fmaf(o.z, qv[e4 + 2], a);
+        a = fmaf(o.w, qv[e4 + 3], a);
       }
-    } else {
-#pragma unroll
-      for (int e = 0; e < FPL; ++e) x[e] = 0.f;
+      part[i] = a;
     }
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-      float acc = 0.f;
-#pragma unroll
-      for (int e = 0; e < FPL; ++e) acc = fmaf(x[e], pq[g][e], acc);
-      part[g][r] = acc;
-    }
-  }
-  const int row = row0 + ((lane >> 2) & 15);
-#pragma unroll
-  for (int g = 0; g < G; ++g) {
-    halve<16, 32>(part[g], lane);
-    halve<8, 16>(part[g], lane);
-    halve<4, 8>(part[g], lane);
-    halve<2, 4>(part[g], lane);
-    float v = part[g][0];
-    v += __shfl_xor(v, 2);
-    v += __shfl_xor(v, 1);
-    if ((lane & 3) == 0 && row < n_cand)
-      scores[(b * Hq + hk * G + g) * (int64_t)nc_cap + row] = v;
+    transpose_reduce<16>(part, lane);
+    const int row = c0 + jj * 16 + wave * 4 + r;
+    if (row < n)
+      phiq[bhq * n + row] = fast_exp2(fmaf(part[0], s1, -nrm * s2)) * inv_sqrt_n;
   }
 }
 
 // ---------------------------------------------------------------------------
-// k_topk_union: per-head top-k and per-kv-head union
+// top-k helpers
 // ---------------------------------------------------------------------------
 // Order key of (score, index): larger key = better; ties in score go to the
-// lower segment index. Keys are unique because indices are.
+// lower segment index. Keys are unique because indices are; 0 = no segment.
 __device__ __forceinline__ u64 order_key(float s, int idx) {
   uint32_t u = __float_as_uint(s);
   u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
@@ -485,13 +546,63 @@ __device__ __forceinline__ float key_score(u64 key) {
   u = (u & 0x80000000u) ? (u & 0x7fffffffu) : ~u;
   return __uint_as_float(u);
 }
-__device__ __forceinline__ u64 wave_max_u64(u64 v) {
+
+// Top-k_eff of one query head by one wave. Lane l holds the keys of segments
+// l, l + 64, ... in registers; each round takes the wave arg-max of the
+// lanes' current bests (DPP row reductions + readlane), and only the lane
+// that owned the winner looks for its next best key below the winner.
+template <int NPL>
+__device__ void head_topk(const float* __restrict__ src, int n_cand, int k,
+                          int k_eff, int* sel_row, int32_t* sel_out,
+                          float* sc_out, int lane) {
+  u64 key[NPL];
+  if (n_cand > 0) {
+    // clamped, unconditional loads: all NPL are in flight together
+    float v[NPL];
 #pragma unroll
-  for (int m = 1; m < kWave; m <<= 1) {
-    const u64 o = __shfl_xor(v, m);
-    v = o > v ? o : v;
+    for (int m = 0; m < NPL; ++m) v[m] = src[min(m * 64 + lane, n_cand - 1)];
+#pragma unroll
+    for (int m = 0; m < NPL; ++m) {
+      const int idx = m * 64 + lane;
+      key[m] = idx < n_cand ? order_key(v[m], idx) : 0ull;
+    }
+  } else {
+#pragma unroll
+    for (int m = 0; m < NPL; ++m) key[m] = 0ull;
   }
-  return v;
+  u64 best = 0;
+#pragma unroll
+  for (int m = 0; m < NPL; ++m) best = max_u64(best, key[m]);
+  for (int r = 0; r < k_eff; ++r) {
+    // wave arg-max: the max of the score halves first (32-bit DPP), then
+    // the lane that holds it; only a tie in score needs the index half.
+    const uint32_t hi = (uint32_t)(best >> 32);
+    const uint32_t whi = wave_max_u32(hi);
+    const u64 tied = __ballot(hi == whi);
+    u64 win;
+    if (__popcll(tied) == 1) {
+      win = lane_read_u64(best, __ffsll((unsigned long long)tied) - 1);
+    } else {
+      const uint32_t lo = hi == whi ? (uint32_t)best : 0u;
+      win = ((u64)whi << 32) | wave_max_u32(lo);
+    }
+    if (lane == 0) {
+      sel_row[r] = key_index(win);
+      if (sel_out) sel_out[r] = key_index(win);
+      if (sc_out) sc_out[r] = key_score(win);
+    }
+    if (best == win) {
+      u64 nb = 0;
+#pragma unroll
+      for (int m = 0; m < NPL; ++m)
+        if (key[m] < win) nb = max_u64(nb, key[m]);
+      best = nb;
+    }
+  }
+  for (int r = k_eff + lane; r < k; r += 64) {
+    if (sel_out) sel_out[r] = -1;
+    if (sc_out) sc_out[r] = __uint_as_float(0x7fc00000u);
+  }
 }
 
 // Union of the group's selections: sel[0 .. M) holds segment ids (-1 = none);
@@ -521,92 +632,153 @@ __device__ void group_union(const int* sel, unsigned char* first, int M,
   if (tid == 0) *ucnt = *cnt_lds;
 }
 
+// ---------------------------------------------------------------------------
+// k_score: a[h][s] = phi(q_h) . summ[s], Eq. 6
+// ---------------------------------------------------------------------------
+// Workgroup = 4 waves x (16 * RB) summary rows of one (b, kv head). Lane l
+// holds features [l*FPL, (l+1)*FPL) of phi(q) for the G heads of the group,
+// so each summary row is one contiguous n*4-byte wave load; all of a wave's
+// rows are loaded before any is reduced. A 16-row batch is transpose-reduced
+// inside each 16-lane row with DPP, then summed over the four rows.
+template <int N, int G>
+__global__ __launch_bounds__(256) void k_score(const float* __restrict__ phiq,
+                                               const float* __restrict__ summ,
+                                               float* __restrict__ scores,
+                                               int Hq, int Hkv, int n_cand,
+                                               int64_t s_cap, int nc_cap) {
+  constexpr int FPL = N / 64;
+  constexpr int RB = N <= 256 ? 2 : 1;     // 16-row batches per wave
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int64_t bh = blockIdx.y;
+  const int64_t b = bh / Hkv, hk = bh % Hkv;
+  const int wrow0 = blockIdx.x * (64 * RB) + wave * (16 * RB);
+  if (wrow0 >= n_cand) return;             // wave-uniform; no barriers below
+
+  float pq[G][FPL];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    const float* src = phiq + ((b * Hq + hk * G + g) * N) + lane * FPL;
+#pragma unroll
+    for (int e = 0; e < FPL; ++e) pq[g][e] = src[e];
+  }
+  const float* base = summ + (bh * s_cap) * N + lane * FPL;
+  float x[RB][16][FPL];
+#pragma unroll
+  for (int bt = 0; bt < RB; ++bt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = min(wrow0 + bt * 16 + r, n_cand - 1);
+      const float* src = base + (int64_t)row * N;
+      if constexpr (FPL % 4 == 0) {
+#pragma unroll
+        for (int e = 0; e < FPL; e += 4) {
+          const float4 v = ld_stream_f4(src + e);
+          x[bt][r][e] = v.x; x[bt][r][e + 1] = v.y;
+          x[bt][r][e + 2] = v.z; x[bt][r][e + 3] = v.w;
+        }
+      } else if constexpr (FPL == 2) {
+        const float2 v = *reinterpret_cast<const float2*>(src);
+        x[bt][r][0] = v.x; x[bt][r][1] = v.y;
+      } else {
+        x[bt][r][0] = src[0];
+      }
+    }
+#pragma unroll
+  for (int bt = 0; bt < RB; ++bt) {
+    const int row = wrow0 + bt * 16 + (lane & 15);
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      float part[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float a = 0.f;
+#pragma unroll
+        for (int e = 0; e < FPL; ++e) a = fmaf(x[bt][r][e], pq[g][e], a);
+        part[r] = a;
+      }
+      transpose_reduce<16>(part, lane);
+      float v = part[0];
+      v += __shfl_xor(v, 16);
+      v += __shfl_xor(v, 32);
+      if (lane < 16 && row < n_cand)
+        scores[(b * Hq + hk * G + g) * (int64_t)nc_cap + row] = v;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// k_topk_union: top-k of every query head, union per kv head
+// ---------------------------------------------------------------------------
+// One workgroup per (b, kv head); wave w takes heads w, w + 4, ... of the
+// group. The heads' sorted selections go to LDS and the union of the group
+// (ascending ids) to the workspace for the attention stage.
 __global__ __launch_bounds__(256) void k_topk_union(
     const float* __restrict__ scores, int Hq, int Hkv, int G, int n_cand,
     int nc_cap, int k, int k_eff, int* __restrict__ uni,
     int* __restrict__ ucnt, int umax, int32_t* __restrict__ selected,
-    float* __restrict__ sel_scores, const int32_t* __restrict__ given,
-    int given_k) {
-  extern __shared__ float sc_lds[];          // [4 waves][npl][64]
+    float* __restrict__ sel_scores) {
   __shared__ int sel_lds[kMaxG * kMaxK];
   __shared__ unsigned char first_lds[kMaxG * kMaxK];
   __shared__ int cnt_lds;
-
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
   const int64_t bh = blockIdx.x;
   const int64_t b = bh / Hkv, hk = bh % Hkv;
-  int M;
+  const int npl = (n_cand + 63) / 64;
+  for (int hl = wave; hl < G; hl += 4) {
+    const int64_t hq = hk * G + hl;
+    const float* src = scores + (b * Hq + hq) * (int64_t)nc_cap;
+    int32_t* so = selected ? selected + (b * Hq + hq) * (int64_t)k : nullptr;
+    float* sco = sel_scores ? sel_scores + (b * Hq + hq) * (int64_t)k : nullptr;
+    int* row = sel_lds + hl * k_eff;
+    if (npl <= 1) head_topk<1>(src, n_cand, k, k_eff, row, so, sco, lane);
+    else if (npl <= 2) head_topk<2>(src, n_cand, k, k_eff, row, so, sco, lane);
+    else if (npl <= 4) head_topk<4>(src, n_cand, k, k_eff, row, so, sco, lane);
+    else if (npl <= 8) head_topk<8>(src, n_cand, k, k_eff, row, so, sco, lane);
+    else if (npl <= 16) head_topk<16>(src, n_cand, k, k_eff, row, so, sco, lane);
+    else head_topk<32>(src, n_cand, k, k_eff, row, so, sco, lane);
+  }
+  __syncthreads();
+  group_union(sel_lds, first_lds, G * k_eff, uni + bh * umax, ucnt + bh, &cnt_lds);
+}
 
-  if (given == nullptr) {
-    const int npl = (n_cand + 63) / 64;
-    float* mine = sc_lds + wave * npl * 64;
-    for (int hl = wave; hl < G; hl += 4) {
-      const int64_t hq = hk * G + hl;
-      const float* src = scores + (b * Hq + hq) * (int64_t)nc_cap;
-      // each lane keeps the scores of segments lane, lane+64, ... in its own
-      // LDS column (only the owning lane ever reads them back)
-      u64 best = 0;
-      for (int m = 0; m < npl; ++m) {
-        const int idx = m * 64 + lane;
-        const float v = idx < n_cand ? src[idx] : 0.f;
-        mine[m * 64 + lane] = v;
-        if (idx < n_cand) {
-          const u64 key = order_key(v, idx);
-          best = key > best ? key : best;
-        }
-      }
-      int32_t* sel_out = selected ? selected + (b * Hq + hq) * (int64_t)k : nullptr;
-      float* sc_out = sel_scores ? sel_scores + (b * Hq + hq) * (int64_t)k : nullptr;
-      for (int r = 0; r < k_eff; ++r) {
-        const u64 win = wave_max_u64(best);
-        const int idx = key_index(win);
-        if (lane == 0) {
-          sel_lds[hl * k_eff + r] = idx;
-          if (sel_out) sel_out[r] = idx;
-          if (sc_out) sc_out[r] = key_score(win);
-        }
-        if ((idx & 63) == lane) {            // owner: next best below `win`
-          best = 0;
-          for (int m = 0; m < npl; ++m) {
-            const int j = m * 64 + lane;
-            if (j < n_cand) {
-              const u64 key = order_key(mine[m * 64 + lane], j);
-              if (key < win && key > best) best = key;
-            }
-          }
-        }
-      }
-      for (int r = k_eff + lane; r < k; r += 64) {
-        if (sel_out) sel_out[r] = -1;
-        if (sc_out) sc_out[r] = __uint_as_float(0x7fc00000u);
-      }
-    }
-    M = G * k_eff;
-  } else {
-    M = G * given_k;
-    for (int i = tid; i < M; i += 256) {
-      const int hl = i / given_k, r = i % given_k;
-      const int id = given[(b * Hq + hk * G + hl) * (int64_t)given_k + r];
-      sel_lds[i] = (id >= 0 && id < n_cand) ? id : -1;
-    }
+// ---------------------------------------------------------------------------
+// k_union_given: union of caller-given selections (attention on a supplied
+// selection, the last step of Algorithm 1 alone)
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_union_given(
+    const int32_t* __restrict__ given, int given_k, int Hq, int Hkv, int G,
+    int n_cand, int* __restrict__ uni, int* __restrict__ ucnt, int umax) {
+  __shared__ int sel_lds[kMaxG * kMaxK];
+  __shared__ unsigned char first_lds[kMaxG * kMaxK];
+  __shared__ int cnt_lds;
+  const int64_t bh = blockIdx.x;
+  const int64_t b = bh / Hkv, hk = bh % Hkv;
+  const int M = G * given_k;
+  for (int i = threadIdx.x; i < M; i += 256) {
+    const int hl = i / given_k, r = i % given_k;
+    const int id = given[(b * Hq + hk * G + hl) * (int64_t)given_k + r];
+    sel_lds[i] = (id >= 0 && id < n_cand) ? id : -1;
   }
   __syncthreads();
   group_union(sel_lds, first_lds, M, uni + bh * umax, ucnt + bh, &cnt_lds);
 }
 
 // ---------------------------------------------------------------------------
-// k_attend: exact attention over union segments + window, one partial per WG
+// k_attend: exact attention over union segments + window, merged in-kernel
 // ---------------------------------------------------------------------------
 // The attended tokens of a (b, kv head) are cut into tiles of <= 64 tokens
 // that never cross a segment or the window boundary: tiles_per_seg tiles per
 // union segment, then ceil(|W| / 64) window tiles. Workgroup j takes tiles
 // 4j .. 4j+3, one per wave. In a wave, lane (r, jj) (r = lane / LPR) reads
 // the 16-byte chunk jj of rows r, r + RPI, ... so every load instruction
-// covers RPI whole rows contiguously; q.k partials are transpose-reduced so
-// that each lane ends with one token's logit, softmax runs across the wave,
-// and p is broadcast back to the lanes that hold the matching V chunks.
+// covers RPI whole rows contiguously (rows past the tile end re-read its
+// last row and are masked). q.k partials are transpose-reduced so that each
+// lane ends with one token's logit, softmax runs across the wave, and p is
+// broadcast back (DPP row broadcast) to the lanes that hold the matching V
+// chunks. The wave results are merged in LDS into one partial (max, sum,
+// acc[d]) per workgroup.
 template <typename T, int D, int G>
 __global__ __launch_bounds__(256) void k_attend(
     const T* __restrict__ q, const T* __restrict__ K, const T* __restrict__ V,
@@ -635,7 +807,8 @@ __global__ __launch_bounds__(256) void k_attend(
   const int seg_tiles = U * tiles_per_seg;
   const int win_tiles = (int)((t - ws + kTile - 1) / kTile);
   const int total = seg_tiles + win_tiles;
-  if (j * 4 >= total) return;
+  const int nwg = (total + 3) / 4;
+  if (j >= nwg) return;
 
   const int ti = j * 4 + wave;
   int64_t start = 0;
@@ -663,75 +836,83 @@ __global__ __launch_bounds__(256) void k_attend(
     for (int e = 0; e < EPL; ++e) qf[g][e] *= qscale;
   }
 
-  const T* kbase = K + (bh * cap + start) * D + jj * EPL;
-  const T* vbase = V + (bh * cap + start) * D + jj * EPL;
-  uint4 kr[ITER], vr[ITER];
-#pragma unroll
-  for (int i = 0; i < ITER; ++i) {
-    const int row = i * RPI + r;
-    kr[i] = row < len ? *reinterpret_cast<const uint4*>(kbase + (int64_t)row * D)
-                      : make_uint4(0u, 0u, 0u, 0u);
-  }
-#pragma unroll
-  for (int i = 0; i < ITER; ++i) {
-    const int row = i * RPI + r;
-    vr[i] = row < len ? *reinterpret_cast<const uint4*>(vbase + (int64_t)row * D)
-                      : make_uint4(0u, 0u, 0u, 0u);
-  }
-
-  // logits: lane (r, jj) ends with the logit of tile row jj * RPI + r
-  float lg[G];
-  {
-    float pl[G][ITER];
-#pragma unroll
-    for (int i = 0; i < ITER; ++i) {
-      float kf[EPL];
-      unpack16<T>(kr[i], kf);
-#pragma unroll
-      for (int g = 0; g < G; ++g) {
-        float a = 0.f;
-#pragma unroll
-        for (int e = 0; e < EPL; ++e) a = fmaf(qf[g][e], kf[e], a);
-        pl[g][i] = a;
-      }
-    }
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-      transpose_reduce<LPR>(pl[g], lane);
-      lg[g] = pl[g][0];
-    }
-  }
-  const bool mine_ok = (jj * RPI + r) < len;
-  float m[G], p[G], l[G];
+  float m[G], l[G], acc[G][EPL];
 #pragma unroll
   for (int g = 0; g < G; ++g) {
-    m[g] = wave_max(mine_ok ? lg[g] : -INFINITY);
-    p[g] = mine_ok ? fast_exp2(lg[g] - m[g]) : 0.f;
-    l[g] = wave_sum(p[g]);
-  }
-
-  float acc[G][EPL];
-#pragma unroll
-  for (int g = 0; g < G; ++g)
+    m[g] = -INFINITY;
+    l[g] = 0.f;
 #pragma unroll
     for (int e = 0; e < EPL; ++e) acc[g][e] = 0.f;
+  }
+
+  if (len > 0) {                           // wave-uniform
+    const T* kbase = K + (bh * cap + start) * D + jj * EPL;
+    const T* vbase = V + (bh * cap + start) * D + jj * EPL;
+    uint4 kr[ITER], vr[ITER];
 #pragma unroll
-  for (int i = 0; i < ITER; ++i) {
-    float vf[EPL];
-    unpack16<T>(vr[i], vf);
+    for (int i = 0; i < ITER; ++i) {
+      const int row = min(i * RPI + r, len - 1);
+      kr[i] = ld_stream(kbase + (int64_t)row * D);
+    }
+#pragma unroll
+    for (int i = 0; i < ITER; ++i) {
+      const int row = min(i * RPI + r, len - 1);
+      vr[i] = ld_stream(vbase + (int64_t)row * D);
+    }
+
+    // logits: lane (r, jj) ends with the logit of tile row jj * RPI + r
+    float lg[G];
+    {
+      float pl[G][ITER];
+#pragma unroll
+      for (int i = 0; i < ITER; ++i) {
+        float kf[EPL];
+        unpack16<T>(kr[i], kf);
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+          float a = 0.f;
+#pragma unroll
+          for (int e = 0; e < EPL; ++e) a = fmaf(qf[g][e], kf[e], a);
+          pl[g][i] = a;
+        }
+      }
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        transpose_reduce<LPR>(pl[g], lane);
+        lg[g] = pl[g][0];
+      }
+    }
+    const bool mine_ok = (jj * RPI + r) < len;
+    float p[G];
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      const float pb = __shfl(p[g], r * LPR + i);
-#pragma unroll
-      for (int e = 0; e < EPL; ++e) acc[g][e] = fmaf(pb, vf[e], acc[g][e]);
+      m[g] = wave_max(mine_ok ? lg[g] : -INFINITY);
+      p[g] = mine_ok ? fast_exp2(lg[g] - m[g]) : 0.f;
+      l[g] = wave_sum(p[g]);
     }
+    static_for<0, ITER>([&](auto ic) {
+      constexpr int i = decltype(ic)::value;
+      float vf[EPL];
+      unpack16<T>(vr[i], vf);
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        // p of row (i, r) lives in lane i of this lane's LPR-lane group
+        float pb;
+        if constexpr (LPR == 16)
+          pb = dpp_f<kDppRowBcast0 + i>(p[g]);
+        else
+          pb = __shfl(p[g], r * LPR + i);
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) acc[g][e] = fmaf(pb, vf[e], acc[g][e]);
+      }
+    });
+#pragma unroll
+    for (int msk = LPR; msk < kWave; msk <<= 1)
+#pragma unroll
+      for (int g = 0; g < G; ++g)
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) acc[g][e] += __shfl_xor(acc[g][e], msk);
   }
-#pragma unroll
-  for (int msk = LPR; msk < kWave; msk <<= 1)
-#pragma unroll
-    for (int g = 0; g < G; ++g)
-#pragma unroll
-      for (int e = 0; e < EPL; ++e) acc[g][e] += __shfl_xor(acc[g][e], msk);
 
   if (lane < LPR) {
 #pragma unroll
@@ -745,7 +926,7 @@ __global__ __launch_bounds__(256) void k_attend(
   }
   __syncthreads();
 
-  float* dst = part + ((bh * maxwg + j) * G) * (int64_t)PSTRIDE;
+  float* pj = part + ((bh * maxwg + j) * G) * (int64_t)PSTRIDE;
   for (int x = tid; x < G * D; x += 256) {
     const int g = x / D, e = x % D;
     float M = wm[0][g];
@@ -758,48 +939,72 @@ __global__ __launch_bounds__(256) void k_attend(
       a = fmaf(wacc[w][g][e], f, a);
       L = fmaf(wl[w][g], f, L);
     }
-    dst[g * PSTRIDE + 4 + e] = a;
-    if (e == 0) { dst[g * PSTRIDE] = M; dst[g * PSTRIDE + 1] = L; }
+    pj[g * PSTRIDE + 4 + e] = a;
+    if (e == 0) { pj[g * PSTRIDE] = M; pj[g * PSTRIDE + 1] = L; }
   }
 }
 
 // ---------------------------------------------------------------------------
-// k_combine: merge the partials of each (b, q head)
+// k_combine: log-sum-exp merge of the partials of each (b, q head)
 // ---------------------------------------------------------------------------
+// 256 threads per query head: the partials' maxima and scale factors are
+// computed in parallel, then 256 / D groups of threads sum disjoint subsets
+// of the partials' accumulators and LDS adds the groups.
 template <typename T, int D>
-__global__ __launch_bounds__(64) void k_combine(const float* __restrict__ part,
-                                                const int* __restrict__ ucnt,
-                                                T* __restrict__ out, int Hq,
-                                                int Hkv, int G,
-                                                int tiles_per_seg,
-                                                int win_tiles, int maxwg) {
+__global__ __launch_bounds__(256) void k_combine(const float* __restrict__ part,
+                                                 const int* __restrict__ ucnt,
+                                                 T* __restrict__ out, int Hq,
+                                                 int Hkv, int G,
+                                                 int tiles_per_seg,
+                                                 int win_tiles, int maxwg) {
   constexpr int PSTRIDE = D + 4;
-  constexpr int DPT = D / 64;
+  constexpr int NGRP = 256 / D;
+  __shared__ float f_lds[kMaxWg];
+  __shared__ float red_lds[8];
+  __shared__ float acc_lds[256];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t bhq = blockIdx.x;
   const int64_t b = bhq / Hq, hq = bhq % Hq;
   const int64_t hk = hq / G;
   const int g = (int)(hq % G);
   const int64_t bh = b * Hkv + hk;
-  const int total = ucnt[bh] * tiles_per_seg + win_tiles;
-  const int nwg = (total + 3) / 4;
-  const float* src = part + ((bh * maxwg) * G + g) * (int64_t)PSTRIDE;
-  const int64_t wstride = (int64_t)G * PSTRIDE;
-  float M = -INFINITY;
-  for (int w = 0; w < nwg; ++w) M = fmaxf(M, src[w * wstride]);
-  float L = 0.f, a[DPT];
-#pragma unroll
-  for (int i = 0; i < DPT; ++i) a[i] = 0.f;
-  for (int w = 0; w < nwg; ++w) {
-    const float* pw = src + w * wstride;
-    const float f = fast_exp2(pw[0] - M);
-    L = fmaf(pw[1], f, L);
-#pragma unroll
-    for (int i = 0; i < DPT; ++i) a[i] = fmaf(pw[4 + threadIdx.x + 64 * i], f, a[i]);
+  const int nwg = (ucnt[bh] * tiles_per_seg + win_tiles + 3) / 4;
+  if (nwg == 0) {                          // nothing attended (given ids only)
+    if (tid < D) out[bhq * D + tid] = from_f32<T>(0.f);
+    return;
   }
-  const float inv = 1.f / L;
+  const float* pb = part + ((bh * maxwg) * G + g) * (int64_t)PSTRIDE;
+  const int64_t wstride = (int64_t)G * PSTRIDE;
+
+  float mx = -INFINITY;
+  for (int w = tid; w < nwg; w += 256) mx = fmaxf(mx, pb[w * wstride]);
+  mx = wave_max(mx);
+  if (lane == 0) red_lds[wave] = mx;
+  __syncthreads();
+  const float M = fmaxf(fmaxf(red_lds[0], red_lds[1]), fmaxf(red_lds[2], red_lds[3]));
+  float ls = 0.f;
+  for (int w = tid; w < nwg; w += 256) {
+    const float f = fast_exp2(pb[w * wstride] - M);
+    f_lds[w] = f;
+    ls = fmaf(pb[w * wstride + 1], f, ls);
+  }
+  ls = wave_sum(ls);
+  if (lane == 0) red_lds[4 + wave] = ls;
+  __syncthreads();
+  const float inv = 1.f / ((red_lds[4] + red_lds[5]) + (red_lds[6] + red_lds[7]));
+  const int e = tid % D, grp = tid / D;
+  float a = 0.f;
+#pragma unroll 4
+  for (int w = grp; w < nwg; w += NGRP)
+    a = fmaf(pb[w * wstride + 4 + e], f_lds[w], a);
+  acc_lds[tid] = a;
+  __syncthreads();
+  if (tid < D) {
+    float sum = 0.f;
 #pragma unroll
-  for (int i = 0; i < DPT; ++i)
-    out[bhq * D + threadIdx.x + 64 * i] = from_f32<T>(a[i] * inv);
+    for (int i = 0; i < NGRP; ++i) sum += acc_lds[i * D + tid];
+    out[bhq * D + tid] = from_f32<T>(sum * inv);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -876,12 +1081,13 @@ WsLayout ws_layout(const Shape& s, int k) {
   const int64_t wmax = std::min<int64_t>(s.cap, (int64_t)s.w + s.c);
   const int64_t wt = ceil_div(wmax, kTile);
   L.maxwg = (int)ceil_div((int64_t)L.umax * L.tiles_per_seg + wt, 4);
+  const size_t bh = (size_t)s.B * s.Hkv;
   size_t off = 0;
-  L.phiq = off;   off += align256((size_t)s.B * s.Hq * s.n * 4);
-  L.scores = off; off += align256((size_t)s.B * s.Hq * std::max<int64_t>(1, s.s_cap) * 4);
-  L.uni = off;    off += align256((size_t)s.B * s.Hkv * L.umax * 4);
-  L.ucnt = off;   off += align256((size_t)s.B * s.Hkv * 4);
-  L.part = off;   off += align256((size_t)s.B * s.Hkv * L.maxwg * s.G * (s.d + 4) * 4);
+  L.phiq = off;        off += align256((size_t)s.B * s.Hq * s.n * 4);
+  L.scores = off;      off += align256((size_t)s.B * s.Hq * std::max<int64_t>(1, s.s_cap) * 4);
+  L.uni = off;         off += align256(bh * L.umax * 4);
+  L.ucnt = off;        off += align256(bh * 4);
+  L.part = off;        off += align256(bh * L.maxwg * s.G * (s.d + 4) * 4);
   L.total = off;
   return L;
 }
@@ -966,20 +1172,28 @@ void launch_phi_q(const Shape& s, const void* q, const float* omega, float* phiq
   const float s1 = kLog2e / std::pow((float)s.d, 0.25f);
   const float s2 = kLog2e / (2.f * std::sqrt((float)s.d));
   launch(RADAR_K_PHI_Q, k_phi_q<T, D>, dim3((unsigned)(s.B * s.Hq)), dim3(256), 0, st,
-                     reinterpret_cast<const T*>(q), omega, phiq, s.n, s1, s2,
-                     1.f / std::sqrt((float)s.n));
+         reinterpret_cast<const T*>(q), omega, phiq, s.n, s1, s2,
+         1.f / std::sqrt((float)s.n));
+}
+
+template <int N, int G>
+void launch_score_ng(const Shape& s, const float* phiq, const float* summ,
+                     float* scores, int n_cand, hipStream_t st) {
+  constexpr int rows_per_wg = 64 * (N <= 256 ? 2 : 1);
+  const dim3 grid((unsigned)ceil_div(n_cand, rows_per_wg), (unsigned)(s.B * s.Hkv));
+  const int nc_cap = (int)std::max<int64_t>(1, s.s_cap);
+  launch(RADAR_K_SCORE, k_score<N, G>, grid, dim3(256), 0, st, phiq, summ, scores,
+         s.Hq, s.Hkv, n_cand, s.s_cap, nc_cap);
 }
 
 template <int N>
 void launch_score_n(const Shape& s, const float* phiq, const float* summ,
                     float* scores, int n_cand, hipStream_t st) {
-  const dim3 grid((unsigned)ceil_div(n_cand, 64), (unsigned)(s.B * s.Hkv));
-  const int nc_cap = (int)std::max<int64_t>(1, s.s_cap);
   switch (s.G) {
-    case 1: launch(RADAR_K_SCORE, k_score<N, 1>, grid, dim3(256), 0, st, phiq, summ, scores, s.Hq, s.Hkv, n_cand, s.s_cap, nc_cap); break;
-    case 2: launch(RADAR_K_SCORE, k_score<N, 2>, grid, dim3(256), 0, st, phiq, summ, scores, s.Hq, s.Hkv, n_cand, s.s_cap, nc_cap); break;
-    case 4: launch(RADAR_K_SCORE, k_score<N, 4>, grid, dim3(256), 0, st, phiq, summ, scores, s.Hq, s.Hkv, n_cand, s.s_cap, nc_cap); break;
-    default: launch(RADAR_K_SCORE, k_score<N, 8>, grid, dim3(256), 0, st, phiq, summ, scores, s.Hq, s.Hkv, n_cand, s.s_cap, nc_cap); break;
+    case 1: launch_score_ng<N, 1>(s, phiq, summ, scores, n_cand, st); break;
+    case 2: launch_score_ng<N, 2>(s, phiq, summ, scores, n_cand, st); break;
+    case 4: launch_score_ng<N, 4>(s, phiq, summ, scores, n_cand, st); break;
+    default: launch_score_ng<N, 8>(s, phiq, summ, scores, n_cand, st); break;
   }
 }
 
@@ -995,66 +1209,52 @@ void launch_score(const Shape& s, const float* phiq, const float* summ,
 
 template <typename T, int D, int G>
 void launch_attend_g(const Shape& s, const void* q, const void* K, const void* V,
-                     const int* uni, const int* ucnt, float* part,
-                     const WsLayout& L, int grid_x, int64_t ws, int64_t t,
-                     hipStream_t st) {
+                     unsigned char* w, const WsLayout& L, int grid_x, int64_t ws,
+                     int64_t t, hipStream_t st) {
   const float qscale = kLog2e / std::sqrt((float)s.d);
-  launch(RADAR_K_ATTEND, k_attend<T, D, G>, dim3((unsigned)grid_x, (unsigned)(s.B * s.Hkv)),
-                     dim3(256), 0, st, reinterpret_cast<const T*>(q),
-                     reinterpret_cast<const T*>(K), reinterpret_cast<const T*>(V),
-                     uni, ucnt, part, s.Hq, s.Hkv, s.cap, s.c, L.tiles_per_seg, ws,
-                     t, L.umax, L.maxwg, qscale);
+  launch(RADAR_K_ATTEND, k_attend<T, D, G>,
+         dim3((unsigned)grid_x, (unsigned)(s.B * s.Hkv)), dim3(256), 0, st,
+         reinterpret_cast<const T*>(q), reinterpret_cast<const T*>(K),
+         reinterpret_cast<const T*>(V), reinterpret_cast<const int*>(w + L.uni),
+         reinterpret_cast<const int*>(w + L.ucnt), reinterpret_cast<float*>(w + L.part),
+         s.Hq, s.Hkv, s.cap, s.c, L.tiles_per_seg, ws, t, L.umax, L.maxwg, qscale);
 }
 
 template <typename T, int D>
 void launch_attend_d(const Shape& s, const void* q, const void* K, const void* V,
-                     const int* uni, const int* ucnt, float* part,
-                     const WsLayout& L, int grid_x, int64_t ws, int64_t t,
-                     hipStream_t st) {
+                     unsigned char* w, const WsLayout& L, int grid_x, int64_t ws,
+                     int64_t t, void* out, hipStream_t st) {
   switch (s.G) {
-    case 1: launch_attend_g<T, D, 1>(s, q, K, V, uni, ucnt, part, L, grid_x, ws, t, st); break;
-    case 2: launch_attend_g<T, D, 2>(s, q, K, V, uni, ucnt, part, L, grid_x, ws, t, st); break;
-    case 4: launch_attend_g<T, D, 4>(s, q, K, V, uni, ucnt, part, L, grid_x, ws, t, st); break;
-    default: launch_attend_g<T, D, 8>(s, q, K, V, uni, ucnt, part, L, grid_x, ws, t, st); break;
+    case 1: launch_attend_g<T, D, 1>(s, q, K, V, w, L, grid_x, ws, t, st); break;
+    case 2: launch_attend_g<T, D, 2>(s, q, K, V, w, L, grid_x, ws, t, st); break;
+    case 4: launch_attend_g<T, D, 4>(s, q, K, V, w, L, grid_x, ws, t, st); break;
+    default: launch_attend_g<T, D, 8>(s, q, K, V, w, L, grid_x, ws, t, st); break;
   }
-}
-
-template <typename T, int D>
-void launch_combine_d(const Shape& s, const float* part, const int* ucnt, void* out,
-                      const WsLayout& L, int win_tiles, hipStream_t st) {
-  launch(RADAR_K_COMBINE, k_combine<T, D>, dim3((unsigned)(s.B * s.Hq)), dim3(64), 0, st,
-                     part, ucnt, reinterpret_cast<T*>(out), s.Hq, s.Hkv, s.G,
-                     L.tiles_per_seg, win_tiles, L.maxwg);
-}
-
-// exact attention over the union written to the workspace, then combine
-radar_status attend_and_combine(const Shape& s, const void* q, const void* K,
-                                const void* V, int u_bound, int64_t ws, int64_t t,
-                                void* out, unsigned char* w, const WsLayout& L,
-                                hipStream_t st) {
-  const int* uni = reinterpret_cast<const int*>(w + L.uni);
-  const int* ucnt = reinterpret_cast<const int*>(w + L.ucnt);
-  float* part = reinterpret_cast<float*>(w + L.part);
   const int win_tiles = (int)ceil_div(t - ws, kTile);
-  const int grid_x = (int)ceil_div((int64_t)u_bound * L.tiles_per_seg + win_tiles, 4);
+  launch(RADAR_K_COMBINE, k_combine<T, D>, dim3((unsigned)(s.B * s.Hq)), dim3(256), 0,
+         st, reinterpret_cast<const float*>(w + L.part),
+         reinterpret_cast<const int*>(w + L.ucnt), reinterpret_cast<T*>(out), s.Hq,
+         s.Hkv, s.G, L.tiles_per_seg, win_tiles, L.maxwg);
+}
+
+// exact attention over the union in the workspace, then the merge
+radar_status launch_attend(const Shape& s, const void* q, const void* K,
+                           const void* V, int grid_x, int64_t ws, int64_t t,
+                           void* out, unsigned char* w, const WsLayout& L,
+                           hipStream_t st) {
   if (s.dt == RADAR_BF16) {
-    if (s.d == 64) {
-      launch_attend_d<bf16_t, 64>(s, q, K, V, uni, ucnt, part, L, grid_x, ws, t, st);
-      launch_combine_d<bf16_t, 64>(s, part, ucnt, out, L, win_tiles, st);
-    } else {
-      launch_attend_d<bf16_t, 128>(s, q, K, V, uni, ucnt, part, L, grid_x, ws, t, st);
-      launch_combine_d<bf16_t, 128>(s, part, ucnt, out, L, win_tiles, st);
-    }
+    if (s.d == 64) launch_attend_d<bf16_t, 64>(s, q, K, V, w, L, grid_x, ws, t, out, st);
+    else launch_attend_d<bf16_t, 128>(s, q, K, V, w, L, grid_x, ws, t, out, st);
   } else {
-    if (s.d == 64) {
-      launch_attend_d<float, 64>(s, q, K, V, uni, ucnt, part, L, grid_x, ws, t, st);
-      launch_combine_d<float, 64>(s, part, ucnt, out, L, win_tiles, st);
-    } else {
-      launch_attend_d<float, 128>(s, q, K, V, uni, ucnt, part, L, grid_x, ws, t, st);
-      launch_combine_d<float, 128>(s, part, ucnt, out, L, win_tiles, st);
-    }
+    if (s.d == 64) launch_attend_d<float, 64>(s, q, K, V, w, L, grid_x, ws, t, out, st);
+    else launch_attend_d<float, 128>(s, q, K, V, w, L, grid_x, ws, t, out, st);
   }
   return launch_status();
+}
+
+int attend_grid(const WsLayout& L, int u_bound, int64_t ws, int64_t t) {
+  const int64_t win_tiles = ceil_div(t - ws, kTile);
+  return (int)ceil_div((int64_t)u_bound * L.tiles_per_seg + win_tiles, 4);
 }
 
 void window_split(const Shape& s, int64_t t, int64_t* ws, int* n_cand) {
@@ -1195,13 +1395,13 @@ radar_status radar_decode(const radar_config* cfg, const void* q, const void* K,
   if (n_cand > kMaxCand) return RADAR_EUNSUPPORTED;
   const int k_eff = std::min(k, n_cand);
 
+  const int u_bound = std::min(s.G * k_eff, n_cand);
+  const int grid_x = attend_grid(L, u_bound, ws, t);
+  if (grid_x > kMaxWg) return RADAR_EUNSUPPORTED;
+
   unsigned char* w = reinterpret_cast<unsigned char*>(workspace);
   float* phiq = reinterpret_cast<float*>(w + L.phiq);
   float* sc = reinterpret_cast<float*>(w + L.scores);
-  int* uni = reinterpret_cast<int*>(w + L.uni);
-  int* ucnt = reinterpret_cast<int*>(w + L.ucnt);
-  const int nc_cap = (int)std::max<int64_t>(1, s.s_cap);
-
   if (n_cand > 0) {
     if (s.dt == RADAR_BF16) {
       if (s.d == 64) launch_phi_q<bf16_t, 64>(s, q, omega, phiq, stream);
@@ -1212,15 +1412,13 @@ radar_status radar_decode(const radar_config* cfg, const void* q, const void* K,
     }
     launch_score(s, phiq, summaries, sc, n_cand, stream);
   }
-  const int npl = std::max(1, (n_cand + 63) / 64);
-  launch(RADAR_K_TOPK, k_topk_union, dim3((unsigned)(s.B * s.Hkv)), dim3(256),
-                     (size_t)4 * npl * 64 * sizeof(float), stream, sc, s.Hq, s.Hkv,
-                     s.G, n_cand, nc_cap, k, k_eff, uni, ucnt, L.umax, selected,
-                     scores, nullptr, 0);
+  launch(RADAR_K_TOPK, k_topk_union, dim3((unsigned)(s.B * s.Hkv)), dim3(256), 0, stream,
+         sc, s.Hq, s.Hkv, s.G, n_cand, (int)std::max<int64_t>(1, s.s_cap), k, k_eff,
+         reinterpret_cast<int*>(w + L.uni), reinterpret_cast<int*>(w + L.ucnt), L.umax,
+         selected, scores);
   r = launch_status();
   if (r != RADAR_OK) return r;
-  const int u_bound = std::min(s.G * k_eff, n_cand);
-  return attend_and_combine(s, q, K, V, u_bound, ws, t, out, w, L, stream);
+  return launch_attend(s, q, K, V, grid_x, ws, t, out, w, L, stream);
 }
 
 radar_status radar_attend_selected(const radar_config* cfg, const void* q,
@@ -1243,16 +1441,17 @@ radar_status radar_attend_selected(const radar_config* cfg, const void* q,
   int64_t ws;
   int n_cand;
   window_split(s, t, &ws, &n_cand);
+  const int u_bound = std::min(s.G * k, n_cand);
+  const int grid_x = attend_grid(L, u_bound, ws, t);
+  if (grid_x > kMaxWg) return RADAR_EUNSUPPORTED;
   unsigned char* w = reinterpret_cast<unsigned char*>(workspace);
-  int* uni = reinterpret_cast<int*>(w + L.uni);
-  int* ucnt = reinterpret_cast<int*>(w + L.ucnt);
-  launch(RADAR_K_TOPK, k_topk_union, dim3((unsigned)(s.B * s.Hkv)), dim3(256), 0, stream,
-                     nullptr, s.Hq, s.Hkv, s.G, n_cand, 1, k, 0, uni, ucnt, L.umax,
-                     nullptr, nullptr, selected, k);
+  launch(RADAR_K_TOPK, k_union_given, dim3((unsigned)(s.B * s.Hkv)), dim3(256), 0,
+         stream, selected, k, s.Hq, s.Hkv, s.G, n_cand,
+         reinterpret_cast<int*>(w + L.uni), reinterpret_cast<int*>(w + L.ucnt),
+         L.umax);
   r = launch_status();
   if (r != RADAR_OK) return r;
-  const int u_bound = std::min(s.G * k, n_cand);
-  return attend_and_combine(s, q, K, V, u_bound, ws, t, out, w, L, stream);
+  return launch_attend(s, q, K, V, grid_x, ws, t, out, w, L, stream);
 }
 
 }  // extern "C"
