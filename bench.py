@@ -97,7 +97,8 @@ def union_sizes(sel, G):
 
 def step_bytes(wl, t, U, s_kv):
     """Algorithmic HBM bytes of one step whose decode runs at length t (the
-    append wrote row t - 1). U: union size per (b, kv head)."""
+    append wrote row t - 1). U: union size per (b, kv head).
+    Returns (whole step, decode call, K/V gather)."""
     c, d, n = wl.seg_len, wl.head_dim, wl.n_features
     ws, n_cand = window_split(t, c, wl.window)
     W = t - ws
@@ -108,7 +109,8 @@ def step_bytes(wl, t, U, s_kv):
     om = n * d * 4
     app = BH * 2 * d * s_kv
     close = BH * (c * d * s_kv + n * 4) if t % c == 0 else 0
-    return summ + kv + qo + om + app + close, kv
+    decode = summ + kv + qo + om
+    return decode + app + close, decode, kv
 
 
 def blas_threads():
@@ -198,6 +200,8 @@ def main():
                     help="also run a plain 1 GiB read+write elementwise "
                          "kernel (counter calibration for HBM traffic)")
     ap.add_argument("--build-reps", type=int, default=3)
+    ap.add_argument("--path", default="auto", choices=["auto", "split", "fused"],
+                    help="decode path (auto: the library's choice)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the decode path has no multi-GPU "
@@ -207,6 +211,8 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(2)
 
+    radar.set_decode_path({"auto": radar.PATH_AUTO, "split": radar.PATH_SPLIT,
+                           "fused": radar.PATH_FUSED}[args.path])
     wl = workloads.WORKLOADS[args.workload]
     W, Ksteps = args.warmup, args.steps
     total = W + Ksteps
@@ -264,17 +270,25 @@ def main():
 
     # ---- algorithmic bytes ------------------------------------------------
     sel_np = sel_log.cpu().numpy()
-    tot_bytes, kv_bytes = 0, 0
+    tot_bytes, dec_bytes, kv_bytes = 0, 0, 0
     for j in range(Ksteps):
         t = wl.t0 + W + j + 1
         U = union_sizes(sel_np[j], wl.group)
-        b_all, b_kv = step_bytes(wl, t, U, s_kv)
+        b_all, b_dec, b_kv = step_bytes(wl, t, U, s_kv)
         tot_bytes += b_all
+        dec_bytes += b_dec
         kv_bytes += b_kv
     step_gbps = tot_bytes / (ms * 1e-3) / 1e9
-    att_ms, att_n = prof["attend"]
-    att_avg_ms = att_ms / max(att_n, 1)
-    att_gbps = (kv_bytes / Ksteps) / (att_avg_ms * 1e-3) / 1e9
+    path = radar.decode_path(cfg, wl.t0 + W + 1, wl.top_k)
+    # dominant kernel: the fused decode (all decode bytes), or the split
+    # path's gather-attention kernel (the K/V bytes)
+    if path == radar.PATH_FUSED:
+        dom, dom_name, dom_bytes = "fused", "k_decode_fused", dec_bytes
+    else:
+        dom, dom_name, dom_bytes = "attend", "k_attend", kv_bytes
+    dom_ms, dom_n = prof[dom]
+    dom_avg_ms = dom_ms / max(dom_n, 1)
+    dom_gbps = (dom_bytes / Ksteps) / (dom_avg_ms * 1e-3) / 1e9
     tokens_s = wl.batch * Ksteps / (ms * 1e-3)
 
     kern = {k: {"avg_us": round(v[0] / max(v[1], 1) * 1e3, 2), "launches": v[1]}
@@ -324,20 +338,22 @@ def main():
             "batch": wl.batch, "context": wl.t0, "seg_len": wl.seg_len,
             "top_k": wl.top_k, "n_features": wl.n_features,
             "window": wl.window,
+            "decode_path": {radar.PATH_SPLIT: "split",
+                            radar.PATH_FUSED: "fused"}.get(path, "?"),
         },
         "hbm_GBps": round(step_gbps, 1),
         "hbm_frac": round(step_gbps / HBM_PEAK_GBPS, 4),
         "bytes_per_step": int(tot_bytes // Ksteps),
         "roofline": {
-            "kernel": "k_attend",
+            "kernel": dom_name,
             "bound": "hbm",
-            "achieved": round(att_gbps, 1),
+            "achieved": round(dom_gbps, 1),
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
-            "frac": round(att_gbps / HBM_PEAK_GBPS, 4),
+            "frac": round(dom_gbps / HBM_PEAK_GBPS, 4),
             "traffic": None,
-            "bytes_per_launch": int(kv_bytes // Ksteps),
-            "avg_us": round(att_avg_ms * 1e3, 2),
+            "bytes_per_launch": int(dom_bytes // Ksteps),
+            "avg_us": round(dom_avg_ms * 1e3, 2),
         },
         "kernels_us": {k: v["avg_us"] for k, v in kern.items()},
         "index_build": {

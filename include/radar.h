@@ -142,6 +142,27 @@ radar_status radar_attend_selected(const radar_config* cfg, const void* q,
                                    size_t workspace_bytes,
                                    hipStream_t stream);
 
+/* Decode paths. The split path runs phi(q), scores, top-k, attention and
+ * merge as separate kernels spread over the whole chip; the fused path runs
+ * the whole step of one (b, kv head) in one workgroup, which suits shapes
+ * with at least as many (b, kv head) pairs as compute units. Both compute the
+ * same method; their fp32 summation orders differ. */
+typedef enum {
+  RADAR_PATH_AUTO = 0,   /* fused when B * Hkv >= #CUs and the shape fits   */
+  RADAR_PATH_SPLIT = 1,
+  RADAR_PATH_FUSED = 2   /* used when the shape fits (G <= 4, at most 1024
+                            candidate segments, not fp32 with d = 128),
+                            else split                                      */
+} radar_path;
+
+/* Choose the decode path for later calls from this host thread (default
+ * RADAR_PATH_AUTO). For tests and tuning; results stay within tolerance. */
+radar_status radar_set_decode_path(int32_t path);
+
+/* The path radar_decode would take for this shape, t and k on this thread
+ * (RADAR_PATH_SPLIT or RADAR_PATH_FUSED; -1 if the arguments are invalid). */
+int32_t radar_decode_path(const radar_config* cfg, int64_t t, int32_t k);
+
 /* Kernel kinds reported by the measurement hook below. */
 typedef enum {
   RADAR_K_APPEND = 0,   /* k/v row write                                   */
@@ -151,7 +172,8 @@ typedef enum {
   RADAR_K_TOPK = 4,     /* top-k and per-kv-head union (or given union)    */
   RADAR_K_ATTEND = 5,   /* gather-attention partials                       */
   RADAR_K_COMBINE = 6,  /* merge of the partials                           */
-  RADAR_K_COUNT = 7
+  RADAR_K_FUSED = 7,    /* the whole decode step, fused path               */
+  RADAR_K_COUNT = 8
 } radar_kernel;
 
 /* Measurement hook (not part of the method). While enabled on the calling

@@ -92,6 +92,10 @@ def lib() -> ctypes.CDLL:
         L.radar_last_error.restype = ctypes.c_char_p
         L.radar_abi_version.restype = ctypes.c_int32
         L.radar_profile_enable.argtypes = [i32]
+        L.radar_set_decode_path.argtypes = [i32]
+        L.radar_set_decode_path.restype = ctypes.c_int
+        L.radar_decode_path.argtypes = [cfgp, i64, i32]
+        L.radar_decode_path.restype = i32
         L.radar_profile_read.argtypes = [ctypes.POINTER(ctypes.c_double),
                                          ctypes.POINTER(ctypes.c_int64), i32]
         for fn in ("radar_build_index", "radar_append", "radar_decode",
@@ -199,7 +203,21 @@ def attend_selected(cfg: Config, q, K, V, selected, t: int, out=None,
     return out
 
 
-KERNELS = ("append", "build", "phi_q", "score", "topk", "attend", "combine")
+KERNELS = ("append", "build", "phi_q", "score", "topk", "attend", "combine",
+           "fused")
+
+
+PATH_AUTO, PATH_SPLIT, PATH_FUSED = 0, 1, 2
+
+
+def set_decode_path(path: int) -> None:
+    """Force the split or fused decode path on this thread (0 = automatic)."""
+    _check("radar_set_decode_path", lib().radar_set_decode_path(path))
+
+
+def decode_path(cfg: Config, t: int, k: int) -> int:
+    """The path radar_decode takes for this shape, t and k."""
+    return int(lib().radar_decode_path(ctypes.byref(cfg.c_struct()), t, k))
 
 
 def profile_enable(on: bool) -> None:

@@ -766,19 +766,134 @@ __global__ __launch_bounds__(256) void k_union_given(
 }
 
 // ---------------------------------------------------------------------------
-// k_attend: exact attention over union segments + window, merged in-kernel
+// exact attention over <= 64-token tiles (shared by k_attend and k_decode_fused)
 // ---------------------------------------------------------------------------
 // The attended tokens of a (b, kv head) are cut into tiles of <= 64 tokens
-// that never cross a segment or the window boundary: tiles_per_seg tiles per
-// union segment, then ceil(|W| / 64) window tiles. Workgroup j takes tiles
-// 4j .. 4j+3, one per wave. In a wave, lane (r, jj) (r = lane / LPR) reads
-// the 16-byte chunk jj of rows r, r + RPI, ... so every load instruction
-// covers RPI whole rows contiguously (rows past the tile end re-read its
-// last row and are masked). q.k partials are transpose-reduced so that each
-// lane ends with one token's logit, softmax runs across the wave, and p is
-// broadcast back (DPP row broadcast) to the lanes that hold the matching V
-// chunks. The wave results are merged in LDS into one partial (max, sum,
-// acc[d]) per workgroup.
+// that never cross a segment or the window boundary. A wave processes one
+// tile at a time: lane (r, jj) (r = lane / LPR) reads the 16-byte chunk jj of
+// rows r, r + RPI, ... so every load instruction covers RPI whole rows
+// contiguously (rows past the tile end re-read its last row and are masked).
+// q.k partials are transpose-reduced so that each lane ends with one token's
+// logit, softmax runs across the wave, and p is broadcast back (DPP row
+// broadcast) to the lanes that hold the matching V chunks. The state carries
+// across tiles as an online softmax: running max m and sum l (log2 units,
+// wave-uniform) and unreduced per-lane accumulators.
+template <typename T, int D, int G>
+struct TileAttn {
+  static constexpr int EPL = Elem<T>::kPer16;   // elements per 16-byte chunk
+  static constexpr int LPR = D / EPL;           // lanes per row
+  static constexpr int RPI = kWave / LPR;       // rows per load instruction
+  static constexpr int ITER = kTile / RPI;      // load instructions per tile
+  static_assert(ITER == LPR, "tile shape");
+
+  float qf[G][EPL];
+  float m[G], l[G], acc[G][EPL];
+
+  // q0: the group's first query head; qscale folds log2(e) / sqrt(d)
+  __device__ __forceinline__ void init(const T* __restrict__ q0, float qscale,
+                                       int lane) {
+    const int jj = lane % LPR;
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const uint4 u = *reinterpret_cast<const uint4*>(q0 + g * D + jj * EPL);
+      unpack16<T>(u, qf[g]);
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) qf[g][e] *= qscale;
+      m[g] = -INFINITY;
+      l[g] = 0.f;
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) acc[g][e] = 0.f;
+    }
+  }
+
+  // rows [row0, row0 + len) of K and V (row0 counts rows from the base
+  // pointers); 1 <= len <= 64; wave-uniform call
+  __device__ __forceinline__ void tile(const T* __restrict__ K,
+                                       const T* __restrict__ V, int64_t row0,
+                                       int len, int lane) {
+    const int r = lane / LPR;
+    const int jj = lane % LPR;
+    const T* kbase = K + row0 * D + jj * EPL;
+    const T* vbase = V + row0 * D + jj * EPL;
+    uint4 kr[ITER], vr[ITER];
+#pragma unroll
+    for (int i = 0; i < ITER; ++i)
+      kr[i] = ld_stream(kbase + (int64_t)min(i * RPI + r, len - 1) * D);
+#pragma unroll
+    for (int i = 0; i < ITER; ++i)
+      vr[i] = ld_stream(vbase + (int64_t)min(i * RPI + r, len - 1) * D);
+
+    // logits: lane (r, jj) ends with the logit of tile row jj * RPI + r
+    float lg[G];
+    {
+      float pl[G][ITER];
+#pragma unroll
+      for (int i = 0; i < ITER; ++i) {
+        float kf[EPL];
+        unpack16<T>(kr[i], kf);
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+          float a = 0.f;
+#pragma unroll
+          for (int e = 0; e < EPL; ++e) a = fmaf(qf[g][e], kf[e], a);
+          pl[g][i] = a;
+        }
+      }
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        transpose_reduce<LPR>(pl[g], lane);
+        lg[g] = pl[g][0];
+      }
+    }
+    const bool mine_ok = (jj * RPI + r) < len;
+    float p[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const float mt = wave_max(mine_ok ? lg[g] : -INFINITY);
+      const float mn = fmaxf(m[g], mt);
+      const float scale = fast_exp2(m[g] - mn);   // 0 on the first tile
+      p[g] = mine_ok ? fast_exp2(lg[g] - mn) : 0.f;
+      l[g] = fmaf(l[g], scale, wave_sum(p[g]));
+      m[g] = mn;
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) acc[g][e] *= scale;
+    }
+    static_for<0, ITER>([&](auto ic) {
+      constexpr int i = decltype(ic)::value;
+      float vf[EPL];
+      unpack16<T>(vr[i], vf);
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        // p of row (i, r) lives in lane i of this lane's LPR-lane group
+        float pb;
+        if constexpr (LPR == 16)
+          pb = dpp_f<kDppRowBcast0 + i>(p[g]);
+        else
+          pb = __shfl(p[g], r * LPR + i);
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) acc[g][e] = fmaf(pb, vf[e], acc[g][e]);
+      }
+    });
+  }
+
+  // sum the accumulators over the RPI row groups: lanes r = 0 (lane < LPR)
+  // then hold dims jj*EPL .. jj*EPL + EPL - 1 of the wave's total
+  __device__ __forceinline__ void reduce_rows() {
+#pragma unroll
+    for (int msk = LPR; msk < kWave; msk <<= 1)
+#pragma unroll
+      for (int g = 0; g < G; ++g)
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) acc[g][e] += __shfl_xor(acc[g][e], msk);
+  }
+};
+
+// ---------------------------------------------------------------------------
+// k_attend: split attention, one partial (max, sum, acc[d]) per workgroup
+// ---------------------------------------------------------------------------
+// Tiles of a (b, kv head): tiles_per_seg per union segment, then ceil(|W| /
+// 64) window tiles. Workgroup j takes tiles 4j .. 4j+3, one per wave, and
+// merges its four waves in LDS.
 template <typename T, int D, int G>
 __global__ __launch_bounds__(256) void k_attend(
     const T* __restrict__ q, const T* __restrict__ K, const T* __restrict__ V,
@@ -786,11 +901,8 @@ __global__ __launch_bounds__(256) void k_attend(
     float* __restrict__ part, int Hq, int Hkv, int64_t cap, int c,
     int tiles_per_seg, int64_t ws, int64_t t, int umax, int maxwg,
     float qscale) {
-  constexpr int EPL = Elem<T>::kPer16;     // elements per 16-byte chunk
-  constexpr int LPR = D / EPL;             // lanes per row
-  constexpr int RPI = kWave / LPR;         // rows per load instruction
-  constexpr int ITER = kTile / RPI;        // load instructions per tile
-  static_assert(ITER == LPR, "tile shape");
+  using TA = TileAttn<T, D, G>;
+  constexpr int EPL = TA::EPL, LPR = TA::LPR;
   constexpr int PSTRIDE = D + 4;
 
   __shared__ float wm[4][G], wl[4][G];
@@ -823,106 +935,21 @@ __global__ __launch_bounds__(256) void k_attend(
     len = (int)min((int64_t)kTile, t - start);
   }
 
-  const int r = lane / LPR;
+  TA ta;
+  ta.init(q + (b * Hq + hk * G) * D, qscale, lane);
+  if (len > 0) ta.tile(K, V, bh * cap + start, len, lane);   // wave-uniform
+  ta.reduce_rows();
+
   const int jj = lane % LPR;
-
-  float qf[G][EPL];
-#pragma unroll
-  for (int g = 0; g < G; ++g) {
-    const uint4 u = *reinterpret_cast<const uint4*>(
-        q + ((b * Hq + hk * G + g) * D + jj * EPL));
-    unpack16<T>(u, qf[g]);
-#pragma unroll
-    for (int e = 0; e < EPL; ++e) qf[g][e] *= qscale;
-  }
-
-  float m[G], l[G], acc[G][EPL];
-#pragma unroll
-  for (int g = 0; g < G; ++g) {
-    m[g] = -INFINITY;
-    l[g] = 0.f;
-#pragma unroll
-    for (int e = 0; e < EPL; ++e) acc[g][e] = 0.f;
-  }
-
-  if (len > 0) {                           // wave-uniform
-    const T* kbase = K + (bh * cap + start) * D + jj * EPL;
-    const T* vbase = V + (bh * cap + start) * D + jj * EPL;
-    uint4 kr[ITER], vr[ITER];
-#pragma unroll
-    for (int i = 0; i < ITER; ++i) {
-      const int row = min(i * RPI + r, len - 1);
-      kr[i] = ld_stream(kbase + (int64_t)row * D);
-    }
-#pragma unroll
-    for (int i = 0; i < ITER; ++i) {
-      const int row = min(i * RPI + r, len - 1);
-      vr[i] = ld_stream(vbase + (int64_t)row * D);
-    }
-
-    // logits: lane (r, jj) ends with the logit of tile row jj * RPI + r
-    float lg[G];
-    {
-      float pl[G][ITER];
-#pragma unroll
-      for (int i = 0; i < ITER; ++i) {
-        float kf[EPL];
-        unpack16<T>(kr[i], kf);
-#pragma unroll
-        for (int g = 0; g < G; ++g) {
-          float a = 0.f;
-#pragma unroll
-          for (int e = 0; e < EPL; ++e) a = fmaf(qf[g][e], kf[e], a);
-          pl[g][i] = a;
-        }
-      }
-#pragma unroll
-      for (int g = 0; g < G; ++g) {
-        transpose_reduce<LPR>(pl[g], lane);
-        lg[g] = pl[g][0];
-      }
-    }
-    const bool mine_ok = (jj * RPI + r) < len;
-    float p[G];
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-      m[g] = wave_max(mine_ok ? lg[g] : -INFINITY);
-      p[g] = mine_ok ? fast_exp2(lg[g] - m[g]) : 0.f;
-      l[g] = wave_sum(p[g]);
-    }
-    static_for<0, ITER>([&](auto ic) {
-      constexpr int i = decltype(ic)::value;
-      float vf[EPL];
-      unpack16<T>(vr[i], vf);
-#pragma unroll
-      for (int g = 0; g < G; ++g) {
-        // p of row (i, r) lives in lane i of this lane's LPR-lane group
-        float pb;
-        if constexpr (LPR == 16)
-          pb = dpp_f<kDppRowBcast0 + i>(p[g]);
-        else
-          pb = __shfl(p[g], r * LPR + i);
-#pragma unroll
-        for (int e = 0; e < EPL; ++e) acc[g][e] = fmaf(pb, vf[e], acc[g][e]);
-      }
-    });
-#pragma unroll
-    for (int msk = LPR; msk < kWave; msk <<= 1)
-#pragma unroll
-      for (int g = 0; g < G; ++g)
-#pragma unroll
-        for (int e = 0; e < EPL; ++e) acc[g][e] += __shfl_xor(acc[g][e], msk);
-  }
-
   if (lane < LPR) {
 #pragma unroll
     for (int g = 0; g < G; ++g)
 #pragma unroll
-      for (int e = 0; e < EPL; ++e) wacc[wave][g][jj * EPL + e] = acc[g][e];
+      for (int e = 0; e < EPL; ++e) wacc[wave][g][jj * EPL + e] = ta.acc[g][e];
   }
   if (lane == 0) {
 #pragma unroll
-    for (int g = 0; g < G; ++g) { wm[wave][g] = m[g]; wl[wave][g] = l[g]; }
+    for (int g = 0; g < G; ++g) { wm[wave][g] = ta.m[g]; wl[wave][g] = ta.l[g]; }
   }
   __syncthreads();
 
@@ -941,6 +968,236 @@ __global__ __launch_bounds__(256) void k_attend(
     }
     pj[g * PSTRIDE + 4 + e] = a;
     if (e == 0) { pj[g * PSTRIDE] = M; pj[g * PSTRIDE + 1] = L; }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// k_decode_fused: the whole decode step of one (b, kv head) in one workgroup
+// ---------------------------------------------------------------------------
+// Used when there are at least as many (b, kv head) pairs as compute units:
+// then one 512-thread workgroup per pair keeps every CU streaming, and no
+// stage hands data to another workgroup (the per-XCD L2s are not coherent,
+// so a cross-workgroup hand-off would need a kernel boundary or a cache
+// flush). Phases:
+//   1. phi(q) of the group's G heads into LDS (16 lanes per Omega row);
+//   2. Eq. 6 scores of all candidates into LDS (32 summary rows per wave
+//      per pass, streaming loads);
+//   3. waves < G take the top-k of one head each, while the other waves
+//      already attend the window tiles (the window never depends on the
+//      selection);
+//   4. the group's union in LDS;
+//   5. every wave attends segment tiles (tile i to wave i mod 8);
+//   6. the waves' online-softmax states merge in LDS into the output.
+constexpr int kFusedWaves = 8;
+constexpr int kFusedMaxG = 4;
+constexpr int kFusedMaxCand = 1024;
+
+template <typename T, int D, int G, int N>
+__global__ __launch_bounds__(512) void k_decode_fused(
+    const T* __restrict__ q, const T* __restrict__ K, const T* __restrict__ V,
+    const float* __restrict__ omega, const float* __restrict__ summ,
+    T* __restrict__ out, int32_t* __restrict__ selected,
+    float* __restrict__ sel_scores, int Hq, int Hkv, int64_t cap,
+    int64_t s_cap, int c, int tiles_per_seg, int64_t ws, int64_t t,
+    int n_cand, int k, int k_eff, float s1, float s2, float inv_sqrt_n,
+    float qscale) {
+  constexpr int NW = kFusedWaves;
+  constexpr int QPL = D / 16;              // q elements per lane (phase 1)
+  constexpr int FPL = N / 64;              // features per lane (phase 2)
+  using TA = TileAttn<T, D, G>;
+  constexpr int EPL = TA::EPL, LPR = TA::LPR;
+  constexpr int SEL_FLOATS = G * N + G * kFusedMaxCand;
+  constexpr int MRG_FLOATS = NW * G * D;
+  constexpr int AREA = SEL_FLOATS > MRG_FLOATS ? SEL_FLOATS : MRG_FLOATS;
+  static_assert(G <= kFusedMaxG, "group");
+  static_assert(N % (4 * NW) == 0, "features");
+
+  // phi(q) and the scores live only until the top-k; the merge reuses them
+  __shared__ __attribute__((aligned(16))) float area[AREA];
+  __shared__ int sel_lds[G * kMaxK];
+  __shared__ unsigned char first_lds[G * kMaxK];
+  __shared__ int uni_lds[G * kMaxK];
+  __shared__ float wm[NW][G], wl[NW][G];
+  __shared__ int cnt_lds, ucnt_lds;
+  float* phq = area;                       // [G][N]
+  float* sc = area + G * N;                // [G][kFusedMaxCand]
+  float* wacc = area;                      // [NW][G][D]
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int64_t bh = blockIdx.x;
+  const int64_t b = bh / Hkv, hk = bh % Hkv;
+  const T* q0 = q + (b * Hq + hk * G) * D;
+
+  if (n_cand > 0) {                        // uniform
+    // ---- 1. phi(q) -----------------------------------------------------
+    {
+      const int r = lane >> 4, jj = lane & 15;
+      float qv[G][QPL], nrm[G];
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        float sq = 0.f;
+#pragma unroll
+        for (int e = 0; e < QPL; ++e) {
+          qv[g][e] = to_f32<T>(q0[g * D + jj * QPL + e]);
+          sq = fmaf(qv[g][e], qv[g][e], sq);
+        }
+        nrm[g] = row_sum(sq);
+      }
+#pragma unroll
+      for (int row0 = 0; row0 < N; row0 += 4 * NW) {
+        const int row = row0 + wave * 4 + r;
+        const float* orow = omega + (int64_t)row * D + jj * QPL;
+        float a[G];
+#pragma unroll
+        for (int g = 0; g < G; ++g) a[g] = 0.f;
+#pragma unroll
+        for (int e4 = 0; e4 < QPL; e4 += 4) {
+          float4 o = *reinterpret_cast<const float4*>(orow + e4);
+          if constexpr (sizeof(T) == 2) {
+            o.x = round_bf16(o.x); o.y = round_bf16(o.y);
+            o.z = round_bf16(o.z); o.w = round_bf16(o.w);
+          }
+#pragma unroll
+          for (int g = 0; g < G; ++g) {
+            a[g] = fmaf(o.x, qv[g][e4], a[g]);
+            a[g] = fmaf(o.y, qv[g][e4 + 1], a[g]);
+            a[g] = fmaf(o.z, qv[g][e4 + 2], a[g]);
+            a[g] = fmaf(o.w, qv[g][e4 + 3], a[g]);
+          }
+        }
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+          const float dot = row_sum(a[g]);
+          if (jj == 0)
+            phq[g * N + row] = fast_exp2(fmaf(dot, s1, -nrm[g] * s2)) * inv_sqrt_n;
+        }
+      }
+    }
+    __syncthreads();
+
+    // ---- 2. scores ------------------------------------------------------
+    {
+      float pq[G][FPL];
+#pragma unroll
+      for (int g = 0; g < G; ++g)
+#pragma unroll
+        for (int e = 0; e < FPL; ++e) pq[g][e] = phq[g * N + lane * FPL + e];
+      constexpr int RB = FPL <= 4 ? 2 : 1;   // 16-row batches per pass
+      const float* base = summ + (bh * s_cap) * N + lane * FPL;
+      for (int rb = wave * 16 * RB; rb < n_cand; rb += NW * 16 * RB) {
+        float x[RB][16][FPL];
+#pragma unroll
+        for (int bt = 0; bt < RB; ++bt)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            const int row = min(rb + bt * 16 + i, n_cand - 1);
+            const float* src = base + (int64_t)row * N;
+            if constexpr (FPL % 4 == 0) {
+#pragma unroll
+              for (int e = 0; e < FPL; e += 4) {
+                const float4 v = ld_stream_f4(src + e);
+                x[bt][i][e] = v.x; x[bt][i][e + 1] = v.y;
+                x[bt][i][e + 2] = v.z; x[bt][i][e + 3] = v.w;
+              }
+            } else if constexpr (FPL == 2) {
+              const float2 v = *reinterpret_cast<const float2*>(src);
+              x[bt][i][0] = v.x; x[bt][i][1] = v.y;
+            } else {
+              x[bt][i][0] = src[0];
+            }
+          }
+#pragma unroll
+        for (int bt = 0; bt < RB; ++bt) {
+          const int row = rb + bt * 16 + (lane & 15);
+#pragma unroll
+          for (int g = 0; g < G; ++g) {
+            float part[16];
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+              float a = 0.f;
+#pragma unroll
+              for (int e = 0; e < FPL; ++e) a = fmaf(x[bt][i][e], pq[g][e], a);
+              part[i] = a;
+            }
+            transpose_reduce<16>(part, lane);
+            float v = part[0];
+            v += __shfl_xor(v, 16);
+            v += __shfl_xor(v, 32);
+            if (lane < 16 && row < n_cand) sc[g * kFusedMaxCand + row] = v;
+          }
+        }
+      }
+    }
+    __syncthreads();
+  }
+
+  // ---- 3. top-k (waves < G) | window tiles (the other waves) -------------
+  TA ta;
+  ta.init(q0, qscale, lane);
+  const int win_tiles = (int)((t - ws + kTile - 1) / kTile);
+  if (wave < G) {
+    const int64_t hq = hk * G + wave;
+    int32_t* so = selected ? selected + (b * Hq + hq) * (int64_t)k : nullptr;
+    float* sco = sel_scores ? sel_scores + (b * Hq + hq) * (int64_t)k : nullptr;
+    const float* src = sc + wave * kFusedMaxCand;
+    int* row = sel_lds + wave * k_eff;
+    const int npl = (n_cand + 63) / 64;
+    if (npl <= 1) head_topk<1>(src, n_cand, k, k_eff, row, so, sco, lane);
+    else if (npl <= 2) head_topk<2>(src, n_cand, k, k_eff, row, so, sco, lane);
+    else if (npl <= 4) head_topk<4>(src, n_cand, k, k_eff, row, so, sco, lane);
+    else if (npl <= 8) head_topk<8>(src, n_cand, k, k_eff, row, so, sco, lane);
+    else head_topk<16>(src, n_cand, k, k_eff, row, so, sco, lane);
+  } else {
+    for (int i = wave - G; i < win_tiles; i += NW - G) {
+      const int64_t start = ws + (int64_t)i * kTile;
+      ta.tile(K, V, bh * cap + start, (int)min((int64_t)kTile, t - start), lane);
+    }
+  }
+  __syncthreads();
+
+  // ---- 4. union -----------------------------------------------------------
+  group_union(sel_lds, first_lds, G * k_eff, uni_lds, &ucnt_lds, &cnt_lds);
+  __syncthreads();
+  const int seg_tiles = ucnt_lds * tiles_per_seg;
+
+  // ---- 5. segment tiles ---------------------------------------------------
+  for (int i = wave; i < seg_tiles; i += NW) {
+    const int s = uni_lds[i / tiles_per_seg];
+    const int off = (i % tiles_per_seg) * kTile;
+    ta.tile(K, V, bh * cap + (int64_t)s * c + off, min(kTile, c - off), lane);
+  }
+
+  // ---- 6. merge -----------------------------------------------------------
+  ta.reduce_rows();
+  __syncthreads();                         // phq / sc are dead from here on
+  const int jj = lane % LPR;
+  if (lane < LPR) {
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+      for (int e = 0; e < EPL; ++e)
+        wacc[(wave * G + g) * D + jj * EPL + e] = ta.acc[g][e];
+  }
+  if (lane == 0) {
+#pragma unroll
+    for (int g = 0; g < G; ++g) { wm[wave][g] = ta.m[g]; wl[wave][g] = ta.l[g]; }
+  }
+  __syncthreads();
+  for (int x = tid; x < G * D; x += NW * 64) {
+    const int g = x / D, e = x % D;
+    float M = wm[0][g];
+#pragma unroll
+    for (int w = 1; w < NW; ++w) M = fmaxf(M, wm[w][g]);
+    float a = 0.f, L = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      const float f = wm[w][g] == -INFINITY ? 0.f : fast_exp2(wm[w][g] - M);
+      a = fmaf(wacc[(w * G + g) * D + e], f, a);
+      L = fmaf(wl[w][g], f, L);
+    }
+    out[(b * Hq + hk * G + g) * D + e] = from_f32<T>(a / L);
   }
 }
 
@@ -1257,6 +1514,81 @@ int attend_grid(const WsLayout& L, int u_bound, int64_t ws, int64_t t) {
   return (int)ceil_div((int64_t)u_bound * L.tiles_per_seg + win_tiles, 4);
 }
 
+// ---- fused path -------------------------------------------------------------
+thread_local int g_path_override = RADAR_PATH_AUTO;
+
+template <typename T, int D, int G, int N>
+radar_status launch_fused_n(const Shape& s, const void* q, const void* K,
+                            const void* V, const float* omega,
+                            const float* summ, int64_t ws, int64_t t,
+                            int n_cand, int k, int k_eff, void* out,
+                            int32_t* selected, float* sel_scores,
+                            hipStream_t st) {
+  const float s1 = kLog2e / std::pow((float)s.d, 0.25f);
+  const float s2 = kLog2e / (2.f * std::sqrt((float)s.d));
+  launch(RADAR_K_FUSED, k_decode_fused<T, D, G, N>, dim3((unsigned)(s.B * s.Hkv)),
+         dim3(kFusedWaves * 64), 0, st, reinterpret_cast<const T*>(q),
+         reinterpret_cast<const T*>(K), reinterpret_cast<const T*>(V), omega, summ,
+         reinterpret_cast<T*>(out), selected, sel_scores, s.Hq, s.Hkv, s.cap,
+         s.s_cap, s.c, (int)ceil_div(s.c, kTile), ws, t, n_cand, k, k_eff, s1, s2,
+         1.f / std::sqrt((float)s.n), kLog2e / std::sqrt((float)s.d));
+  return launch_status();
+}
+
+template <typename T, int D, int G>
+radar_status launch_fused_g(const Shape& s, const void* q, const void* K,
+                            const void* V, const float* omega,
+                            const float* summ, int64_t ws, int64_t t,
+                            int n_cand, int k, int k_eff, void* out,
+                            int32_t* selected, float* sel_scores,
+                            hipStream_t st) {
+  switch (s.n) {
+    case 64: return launch_fused_n<T, D, G, 64>(s, q, K, V, omega, summ, ws, t, n_cand, k, k_eff, out, selected, sel_scores, st);
+    case 128: return launch_fused_n<T, D, G, 128>(s, q, K, V, omega, summ, ws, t, n_cand, k, k_eff, out, selected, sel_scores, st);
+    case 256: return launch_fused_n<T, D, G, 256>(s, q, K, V, omega, summ, ws, t, n_cand, k, k_eff, out, selected, sel_scores, st);
+    default: return launch_fused_n<T, D, G, 512>(s, q, K, V, omega, summ, ws, t, n_cand, k, k_eff, out, selected, sel_scores, st);
+  }
+}
+
+template <typename T, int D>
+radar_status launch_fused_d(const Shape& s, const void* q, const void* K,
+                            const void* V, const float* omega,
+                            const float* summ, int64_t ws, int64_t t,
+                            int n_cand, int k, int k_eff, void* out,
+                            int32_t* selected, float* sel_scores,
+                            hipStream_t st) {
+  switch (s.G) {
+    case 1: return launch_fused_g<T, D, 1>(s, q, K, V, omega, summ, ws, t, n_cand, k, k_eff, out, selected, sel_scores, st);
+    case 2: return launch_fused_g<T, D, 2>(s, q, K, V, omega, summ, ws, t, n_cand, k, k_eff, out, selected, sel_scores, st);
+    default: return launch_fused_g<T, D, 4>(s, q, K, V, omega, summ, ws, t, n_cand, k, k_eff, out, selected, sel_scores, st);
+  }
+}
+
+radar_status launch_fused(const Shape& s, const void* q, const void* K, const void* V,
+                          const float* omega, const float* summ, int64_t ws,
+                          int64_t t, int n_cand, int k, int k_eff, void* out,
+                          int32_t* selected, float* sel_scores, hipStream_t st) {
+  if (s.dt == RADAR_BF16)
+    return s.d == 64 ? launch_fused_d<bf16_t, 64>(s, q, K, V, omega, summ, ws, t, n_cand, k, k_eff, out, selected, sel_scores, st)
+                     : launch_fused_d<bf16_t, 128>(s, q, K, V, omega, summ, ws, t, n_cand, k, k_eff, out, selected, sel_scores, st);
+  // fp32 caches with d = 128 keep the split path: their tiles need more
+  // registers than the fused kernel has to spare
+  if (s.d == 64)
+    return launch_fused_d<float, 64>(s, q, K, V, omega, summ, ws, t, n_cand, k, k_eff, out, selected, sel_scores, st);
+  return RADAR_EUNSUPPORTED;
+}
+
+// Which decode path a call takes: the fused one-workgroup-per-(b, kv head)
+// kernel when there are enough pairs to occupy every CU (or when forced),
+// and the shape fits its LDS plan; the split multi-kernel path otherwise.
+int choose_path(const Shape& s, int n_cand) {
+  const bool fits = s.G <= kFusedMaxG && n_cand <= kFusedMaxCand &&
+                    !(s.dt == RADAR_F32 && s.d == 128);
+  if (!fits || g_path_override == RADAR_PATH_SPLIT) return RADAR_PATH_SPLIT;
+  if (g_path_override == RADAR_PATH_FUSED) return RADAR_PATH_FUSED;
+  return (int64_t)s.B * s.Hkv >= num_cu() ? RADAR_PATH_FUSED : RADAR_PATH_SPLIT;
+}
+
 void window_split(const Shape& s, int64_t t, int64_t* ws, int* n_cand) {
   const int64_t past = std::max<int64_t>(0, t - s.w);
   *ws = (int64_t)s.c * (past / s.c);
@@ -1271,6 +1603,23 @@ void window_split(const Shape& s, int64_t t, int64_t* ws, int* n_cand) {
 extern "C" {
 
 int32_t radar_abi_version(void) { return RADAR_ABI_VERSION; }
+
+radar_status radar_set_decode_path(int32_t path) {
+  if (path != RADAR_PATH_AUTO && path != RADAR_PATH_SPLIT && path != RADAR_PATH_FUSED)
+    return RADAR_EINVAL;
+  g_path_override = path;
+  return RADAR_OK;
+}
+
+int32_t radar_decode_path(const radar_config* cfg, int64_t t, int32_t k) {
+  Shape s;
+  if (check_cfg(cfg, &s) != RADAR_OK || k < 1 || k > kMaxK || t < 1 || t > s.cap)
+    return -1;
+  int64_t ws;
+  int n_cand;
+  window_split(s, t, &ws, &n_cand);
+  return choose_path(s, n_cand);
+}
 
 radar_status radar_profile_enable(int32_t on) {
   g_prof.on = on != 0;
@@ -1394,6 +1743,10 @@ radar_status radar_decode(const radar_config* cfg, const void* q, const void* K,
   window_split(s, t, &ws, &n_cand);
   if (n_cand > kMaxCand) return RADAR_EUNSUPPORTED;
   const int k_eff = std::min(k, n_cand);
+
+  if (choose_path(s, n_cand) == RADAR_PATH_FUSED)
+    return launch_fused(s, q, K, V, omega, summaries, ws, t, n_cand, k, k_eff, out,
+                        selected, scores, stream);
 
   const int u_bound = std::min(s.G * k_eff, n_cand);
   const int grid_x = attend_grid(L, u_bound, ws, t);

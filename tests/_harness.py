@@ -83,9 +83,11 @@ class Episode:
     """One workload run: build the index at t0, then `steps` x (append,
     decode). Oracle checks on the sampled (batch, kv head) groups."""
 
-    def __init__(self, wl, steps, groups=None, device="cuda"):
+    def __init__(self, wl, steps, groups=None, device="cuda",
+                 path=radar.PATH_AUTO):
         self.wl = wl
         self.steps = steps
+        self.path = path
         self.inp = workloads.make_inputs(wl, device, steps=steps)
         self.cfg = config_of(wl, wl.t0 + steps)
         B, Hkv = wl.batch, wl.n_kv_heads
@@ -104,6 +106,13 @@ class Episode:
         self.stats = Stats()
 
     def run(self, check_steps=None):
+        radar.set_decode_path(self.path)
+        try:
+            return self._run(check_steps)
+        finally:
+            radar.set_decode_path(radar.PATH_AUTO)
+
+    def _run(self, check_steps):
         wl, inp, cfg = self.wl, self.inp, self.cfg
         dev = inp.K.device
         K, V = inp.K.clone(), inp.V.clone()

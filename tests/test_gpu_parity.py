@@ -32,11 +32,16 @@ def _announce(name):
     print(f"[case] {name}", flush=True)
 
 
-def _run(wl, steps, groups=None, check_steps=None):
+PATHS = pytest.mark.parametrize("path", [radar.PATH_SPLIT, radar.PATH_FUSED],
+                                ids=["split", "fused"])
+
+
+def _run(wl, steps, groups=None, check_steps=None, path=radar.PATH_AUTO):
     _announce(f"{wl.name} B{wl.batch} Hq{wl.n_q_heads}/{wl.n_kv_heads} "
               f"d{wl.head_dim} t0={wl.t0} c={wl.seg_len} k={wl.top_k} "
-              f"n={wl.n_features} w={wl.window} {wl.dtype} steps={steps}")
-    ep = H.Episode(wl, steps, groups=groups)
+              f"n={wl.n_features} w={wl.window} {wl.dtype} steps={steps} "
+              f"path={path}")
+    ep = H.Episode(wl, steps, groups=groups, path=path)
     st = ep.run(check_steps=check_steps)
     print(f"  heads={st.heads} out_err={st.max_out_err:.2e} "
           f"score_err={st.max_score_err:.2e} summ_err={st.max_summ_err:.2e} "
@@ -48,45 +53,75 @@ def _run(wl, steps, groups=None, check_steps=None):
 # --------------------------------------------------------------------------
 # the five workloads
 # --------------------------------------------------------------------------
-def test_tiny_full():
+@PATHS
+def test_tiny_full(path):
     """Tiny single-layer decode, fp32, all 32 steps, every head."""
-    _run(WORKLOADS["tiny"], 32)
+    _run(WORKLOADS["tiny"], 32, path=path)
 
 
-def test_llama2_16k_full_with_close():
+@PATHS
+def test_llama2_16k_full_with_close(path):
     """Llama-2-7B-shaped layer at 16K, bf16: 130 steps (a segment closes at
     t = 16512), every head."""
     wl = WORKLOADS["llama2_16k"]
-    _run(wl, 130, check_steps=set(range(0, 130, 8)) | {126, 127, 128, 129})
+    _run(wl, 130, check_steps=set(range(0, 130, 8)) | {126, 127, 128, 129},
+         path=path)
 
 
-def test_mha_128k_scaled():
+@PATHS
+def test_mha_128k_scaled(path):
     wl = WORKLOADS["mha_128k"].scaled(name="mha_128k_s", batch=2, n_q_heads=4,
                                       n_kv_heads=4, t0=12800)
-    _run(wl, 260, check_steps={0, 1, 2, 254, 255, 256, 259})
+    _run(wl, 260, check_steps={0, 1, 2, 254, 255, 256, 259}, path=path)
 
 
-def test_gqa_64k_scaled():
+@PATHS
+def test_gqa_64k_scaled(path):
     wl = WORKLOADS["gqa_64k"].scaled(name="gqa_64k_s", batch=2, n_q_heads=8,
                                      n_kv_heads=2, t0=16384)
-    _run(wl, 258, check_steps={0, 1, 255, 256, 257})
+    _run(wl, 258, check_steps={0, 1, 255, 256, 257}, path=path)
 
 
-def test_gqa_512k_scaled():
+@PATHS
+def test_gqa_512k_scaled(path):
     wl = WORKLOADS["gqa_512k"].scaled(name="gqa_512k_s", n_q_heads=8,
                                       n_kv_heads=2, t0=36200)
     # c = 724: a segment closes at t = 36924 (step 723)
-    _run(wl, 726, check_steps={0, 1, 400, 722, 723, 724, 725})
+    _run(wl, 726, check_steps={0, 1, 400, 722, 723, 724, 725}, path=path)
 
 
+@PATHS
 @pytest.mark.parametrize("name,steps,ngroups", [
     ("mha_128k", 3, 3), ("gqa_64k", 3, 3), ("gqa_512k", 3, 2)])
-def test_full_size_sampled(name, steps, ngroups):
-    """Full-size workloads, the launch configuration the benchmark times;
-    oracle checks on sampled (batch, kv head) groups."""
+def test_full_size_sampled(name, steps, ngroups, path):
+    """Full-size workloads (the automatic path of the 128K MHA workload is
+    the one the benchmark times); oracle checks on sampled (batch, kv head)
+    groups."""
     wl = WORKLOADS[name]
-    _run(wl, steps, groups=H.sample_groups(wl, ngroups, seed=1))
+    _run(wl, steps, groups=H.sample_groups(wl, ngroups, seed=1), path=path)
     torch.cuda.empty_cache()
+
+
+def test_path_choice():
+    """The fused path serves shapes with at least one (b, kv head) pair per
+    CU; fewer pairs, G > 4 or more than 1024 candidates take the split path."""
+    def cfg(wl):
+        return H.config_of(wl, wl.t0 + 1)
+    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
+    mha = WORKLOADS["mha_128k"]
+    assert mha.batch * mha.n_kv_heads >= n_cu
+    assert radar.decode_path(cfg(mha), mha.t0 + 1, mha.top_k) == radar.PATH_FUSED
+    g5 = WORKLOADS["gqa_512k"]
+    assert radar.decode_path(cfg(g5), g5.t0 + 1, g5.top_k) == radar.PATH_SPLIT
+    g8 = mha.scaled(n_q_heads=32, n_kv_heads=4, batch=128)
+    assert radar.decode_path(cfg(g8), g8.t0 + 1, 16) == radar.PATH_SPLIT
+    radar.set_decode_path(radar.PATH_FUSED)
+    try:
+        assert radar.decode_path(cfg(g5), g5.t0 + 1, g5.top_k) == radar.PATH_FUSED
+        many = mha.scaled(seg_len=64, window=64)           # 2047 candidates
+        assert radar.decode_path(cfg(many), many.t0 + 1, 16) == radar.PATH_SPLIT
+    finally:
+        radar.set_decode_path(radar.PATH_AUTO)
 
 
 # --------------------------------------------------------------------------
@@ -127,10 +162,11 @@ EDGES = [
 ]
 
 
+@PATHS
 @pytest.mark.parametrize("wl", EDGES, ids=[w.name for w in EDGES])
-def test_edge(wl):
+def test_edge(wl, path):
     steps = 70 if wl.seg_len <= 64 else 8
-    _run(wl, steps)
+    _run(wl, steps, path=path)
 
 
 # --------------------------------------------------------------------------
