@@ -113,6 +113,23 @@ def step_bytes(wl, t, U, s_kv):
     return decode + app + close, decode, kv
 
 
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
+    record (FETCH_SIZE and WRITE_SIZE KiB per dispatch, each divided by the
+    scale a 1 GiB copy kernel shows), or None when there is no record or the
+    kernel source has changed since it was taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    src = os.path.join(ROOT, rec["source"])
+    if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["source_sha256"]:
+        return None
+    return int(rec["fetch_size_kib"] * 1024 / rec["fetch_scale"] +
+               rec["write_size_kib"] * 1024 / rec["write_scale"])
+
+
 def blas_threads():
     try:
         from threadpoolctl import threadpool_info
@@ -351,7 +368,7 @@ def main():
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": round(dom_gbps / HBM_PEAK_GBPS, 4),
-            "traffic": None,
+            "traffic": measured_traffic(dom_name, wl.name),
             "bytes_per_launch": int(dom_bytes // Ksteps),
             "avg_us": round(dom_avg_ms * 1e3, 2),
         },
