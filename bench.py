@@ -207,7 +207,8 @@ def cpu_baseline(wl, inp, first_step, n_steps, n_heads, min_s=10.0,
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=512)
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed steps (default: the workload's step count)")
     ap.add_argument("--warmup", type=int, default=16)
     ap.add_argument("--workload", default="mha_128k",
                     choices=sorted(workloads.WORKLOADS))
@@ -231,7 +232,8 @@ def main():
     radar.set_decode_path({"auto": radar.PATH_AUTO, "split": radar.PATH_SPLIT,
                            "fused": radar.PATH_FUSED}[args.path])
     wl = workloads.WORKLOADS[args.workload]
-    W, Ksteps = args.warmup, args.steps
+    W = args.warmup
+    Ksteps = args.steps if args.steps is not None else wl.steps
     total = W + Ksteps
     log(f"[bench] generating {wl.name} inputs ({total} steps)")
     inp = workloads.make_inputs(wl, "cuda", steps=total)

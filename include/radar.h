@@ -148,7 +148,9 @@ radar_status radar_attend_selected(const radar_config* cfg, const void* q,
  * with at least as many (b, kv head) pairs as compute units. Both compute the
  * same method; their fp32 summation orders differ. */
 typedef enum {
-  RADAR_PATH_AUTO = 0,   /* fused when B * Hkv >= #CUs and the shape fits   */
+  RADAR_PATH_AUTO = 0,   /* fused when the shape fits and either B * Hkv >=
+                            #CUs or one pair's step reads <= 256 KB; split
+                            otherwise                                       */
   RADAR_PATH_SPLIT = 1,
   RADAR_PATH_FUSED = 2   /* used when the shape fits (G <= 4, at most 1024
                             candidate segments, not fp32 with d = 128),

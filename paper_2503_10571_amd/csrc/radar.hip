@@ -547,56 +547,114 @@ __device__ __forceinline__ float key_score(u64 key) {
   return __uint_as_float(u);
 }
 
-// Top-k_eff of one query head by one wave. Lane l holds the keys of segments
-// l, l + 64, ... in registers; each round takes the wave arg-max of the
-// lanes' current bests (DPP row reductions + readlane), and only the lane
-// that owned the winner looks for its next best key below the winner.
+// Top-k_eff of one query head by one wave, k-independent: radix selection of
+// the k_eff-th largest 32-bit score key in four 8-bit passes (a 256-bin LDS
+// histogram of the keys that still match the prefix found so far, a suffix
+// count over the bins by DPP row scans and readlanes, and a ballot for the
+// bin holding the k_eff-th key), then a ballot rank among keys equal to that
+// threshold (lower segment index first), compaction of the k_eff selected
+// keys into LDS and a rank sort by (score desc, index asc).
+// hist: 256 words and list: k words of LDS owned by this wave.
+__device__ __forceinline__ int row_incl_scan(int v, int lane) {
+  // inclusive prefix sum over the 64 lanes
+  int x = v;
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false);   // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false);   // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false);   // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false);   // row_shr:8
+  const int r0 = __builtin_amdgcn_readlane(x, 15);
+  const int r1 = __builtin_amdgcn_readlane(x, 31);
+  const int r2 = __builtin_amdgcn_readlane(x, 47);
+  const int row = lane >> 4;
+  return x + (row > 0 ? r0 : 0) + (row > 1 ? r1 : 0) + (row > 2 ? r2 : 0);
+}
+
 template <int NPL>
 __device__ void head_topk(const float* __restrict__ src, int n_cand, int k,
                           int k_eff, int* sel_row, int32_t* sel_out,
-                          float* sc_out, int lane) {
-  u64 key[NPL];
+                          float* sc_out, int lane, unsigned* hist, u64* list) {
+  uint32_t u[NPL];                         // ordered score keys, 0 = absent
   if (n_cand > 0) {
-    // clamped, unconditional loads: all NPL are in flight together
     float v[NPL];
 #pragma unroll
     for (int m = 0; m < NPL; ++m) v[m] = src[min(m * 64 + lane, n_cand - 1)];
 #pragma unroll
-    for (int m = 0; m < NPL; ++m) {
-      const int idx = m * 64 + lane;
-      key[m] = idx < n_cand ? order_key(v[m], idx) : 0ull;
-    }
+    for (int m = 0; m < NPL; ++m)
+      u[m] = (m * 64 + lane < n_cand) ? (uint32_t)(order_key(v[m], 0) >> 32) : 0u;
   } else {
 #pragma unroll
-    for (int m = 0; m < NPL; ++m) key[m] = 0ull;
+    for (int m = 0; m < NPL; ++m) u[m] = 0u;
   }
-  u64 best = 0;
+  if (k_eff > 0) {
+    uint32_t prefix = 0u, mask = 0u;
+    int need = k_eff;                      // keys still to take at or below prefix
+#pragma unroll 1
+    for (int shift = 24; shift >= 0; shift -= 8) {
 #pragma unroll
-  for (int m = 0; m < NPL; ++m) best = max_u64(best, key[m]);
-  for (int r = 0; r < k_eff; ++r) {
-    // wave arg-max: the max of the score halves first (32-bit DPP), then
-    // the lane that holds it; only a tie in score needs the index half.
-    const uint32_t hi = (uint32_t)(best >> 32);
-    const uint32_t whi = wave_max_u32(hi);
-    const u64 tied = __ballot(hi == whi);
-    u64 win;
-    if (__popcll(tied) == 1) {
-      win = lane_read_u64(best, __ffsll((unsigned long long)tied) - 1);
-    } else {
-      const uint32_t lo = hi == whi ? (uint32_t)best : 0u;
-      win = ((u64)whi << 32) | wave_max_u32(lo);
-    }
-    if (lane == 0) {
-      sel_row[r] = key_index(win);
-      if (sel_out) sel_out[r] = key_index(win);
-      if (sc_out) sc_out[r] = key_score(win);
-    }
-    if (best == win) {
-      u64 nb = 0;
+      for (int i = 0; i < 4; ++i) hist[lane * 4 + i] = 0u;
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 #pragma unroll
       for (int m = 0; m < NPL; ++m)
-        if (key[m] < win) nb = max_u64(nb, key[m]);
-      best = nb;
+        if (u[m] != 0u && (u[m] & mask) == prefix)
+          atomicAdd(&hist[(u[m] >> shift) & 255u], 1u);
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      // lane l owns bins 255 - 4l - j (j = 0..3): lane order runs from the
+      // largest digit down, so a prefix over lanes counts larger digits
+      int c[4], tot = 0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) { c[j] = (int)hist[255 - lane * 4 - j]; tot += c[j]; }
+      const int above = row_incl_scan(tot, lane) - tot;   // keys in larger digits
+      int cum = above, pick = -1, before = 0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if (pick < 0 && cum < need && need <= cum + c[j]) { pick = j; before = cum; }
+        cum += c[j];
+      }
+      const u64 who = __ballot(pick >= 0);
+      const int wl = __ffsll((unsigned long long)who) - 1;
+      const int pj = __builtin_amdgcn_readlane(pick, wl);
+      const int pb = __builtin_amdgcn_readlane(before, wl);
+      const uint32_t digit = 255u - (uint32_t)(wl * 4 + pj);
+      prefix |= digit << shift;
+      mask |= 255u << shift;
+      need -= pb;
+    }
+    // prefix is the k_eff-th largest key; take every larger key and the
+    // `need` lowest-index keys equal to it
+    int eq_before = 0;
+    int n_sel = 0;
+    const u64 lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+#pragma unroll
+    for (int m = 0; m < NPL; ++m) {
+      const bool eq = u[m] == prefix && u[m] != 0u;
+      const u64 be = __ballot(eq);
+      const bool take = (u[m] > prefix) ||
+                        (eq && eq_before + __popcll(be & lt_mask) < need);
+      eq_before += __popcll(be);
+      const u64 bt = __ballot(take);
+      if (take) {
+        const int pos = n_sel + __popcll(bt & lt_mask);
+        const int idx = m * 64 + lane;
+        list[pos] = ((u64)u[m] << 32) | (u64)(0xffffffffu - (uint32_t)idx);
+      }
+      n_sel += __popcll(bt);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    // rank sort of the k_eff selected keys (larger key first)
+    for (int i = lane; i < k_eff; i += 64) {
+      const u64 key = list[i];
+      int rank = 0;
+      for (int j = 0; j < k_eff; ++j) rank += list[j] > key ? 1 : 0;
+      const int idx = key_index(key);
+      sel_row[rank] = idx;
+      if (sel_out) sel_out[rank] = idx;
+      if (sc_out) sc_out[rank] = key_score(key);
     }
   }
   for (int r = k_eff + lane; r < k; r += 64) {
@@ -605,31 +663,41 @@ __device__ void head_topk(const float* __restrict__ src, int n_cand, int k,
   }
 }
 
-// Union of the group's selections: sel[0 .. M) holds segment ids (-1 = none);
-// writes the distinct ids in ascending order to uni and their count to *ucnt.
-__device__ void group_union(const int* sel, unsigned char* first, int M,
-                            int* uni, int* ucnt, int* cnt_lds) {
+// Union of the group's selections: sel[0 .. M) holds segment ids (-1 = none,
+// every other id < kMaxCand). The ids are set in an LDS bitmap, the first
+// wave turns the words' popcounts into prefix offsets, and each lane lists
+// its word's set bits: the distinct ids in ascending order go to uni and
+// their count to *ucnt. bits: kMaxCand / 32 words of LDS.
+constexpr int kBitmapWords = kMaxCand / 32;
+static_assert(kBitmapWords == kWave, "one bitmap word per lane");
+__device__ void group_union(const int* sel, unsigned* bits, int M, int* uni,
+                            int* ucnt) {
   const int tid = threadIdx.x;
-  if (tid == 0) *cnt_lds = 0;
+  for (int i = tid; i < kBitmapWords; i += blockDim.x) bits[i] = 0u;
+  __syncthreads();
   for (int i = tid; i < M; i += blockDim.x) {
     const int id = sel[i];
-    bool f = id >= 0;
-    for (int j = 0; j < i && f; ++j) f = sel[j] != id;
-    first[i] = f;
+    if (id >= 0) atomicOr(&bits[id >> 5], 1u << (id & 31));
   }
   __syncthreads();
-  int mine = 0;
-  for (int i = tid; i < M; i += blockDim.x) {
-    if (!first[i]) continue;
-    const int id = sel[i];
-    int rank = 0;
-    for (int j = 0; j < M; ++j) rank += (first[j] && sel[j] < id) ? 1 : 0;
-    uni[rank] = id;
-    ++mine;
+  if (tid < kWave) {
+    uint32_t word = bits[tid];
+    const int pc = __popc(word);
+    // exclusive prefix sum of the popcounts over the 64 lanes
+    int incl = pc;
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+      const int o = __shfl_up(incl, d);
+      if (tid >= d) incl += o;
+    }
+    int pos = incl - pc;
+    while (word) {
+      const int bit = __ffs(word) - 1;
+      uni[pos++] = tid * 32 + bit;
+      word &= word - 1u;
+    }
+    if (tid == kWave - 1) *ucnt = incl;
   }
-  if (mine) atomicAdd(cnt_lds, mine);
-  __syncthreads();
-  if (tid == 0) *ucnt = *cnt_lds;
 }
 
 // ---------------------------------------------------------------------------
@@ -719,28 +787,31 @@ __global__ __launch_bounds__(256) void k_topk_union(
     int* __restrict__ ucnt, int umax, int32_t* __restrict__ selected,
     float* __restrict__ sel_scores) {
   __shared__ int sel_lds[kMaxG * kMaxK];
-  __shared__ unsigned char first_lds[kMaxG * kMaxK];
-  __shared__ int cnt_lds;
+  __shared__ unsigned bits_lds[kBitmapWords];
+  __shared__ unsigned hist_lds[4][256];
+  __shared__ u64 list_lds[4][kMaxK];
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int64_t bh = blockIdx.x;
   const int64_t b = bh / Hkv, hk = bh % Hkv;
   const int npl = (n_cand + 63) / 64;
+  unsigned* hist = hist_lds[wave];
+  u64* list = list_lds[wave];
   for (int hl = wave; hl < G; hl += 4) {
     const int64_t hq = hk * G + hl;
     const float* src = scores + (b * Hq + hq) * (int64_t)nc_cap;
     int32_t* so = selected ? selected + (b * Hq + hq) * (int64_t)k : nullptr;
     float* sco = sel_scores ? sel_scores + (b * Hq + hq) * (int64_t)k : nullptr;
     int* row = sel_lds + hl * k_eff;
-    if (npl <= 1) head_topk<1>(src, n_cand, k, k_eff, row, so, sco, lane);
-    else if (npl <= 2) head_topk<2>(src, n_cand, k, k_eff, row, so, sco, lane);
-    else if (npl <= 4) head_topk<4>(src, n_cand, k, k_eff, row, so, sco, lane);
-    else if (npl <= 8) head_topk<8>(src, n_cand, k, k_eff, row, so, sco, lane);
-    else if (npl <= 16) head_topk<16>(src, n_cand, k, k_eff, row, so, sco, lane);
-    else head_topk<32>(src, n_cand, k, k_eff, row, so, sco, lane);
+    if (npl <= 1) head_topk<1>(src, n_cand, k, k_eff, row, so, sco, lane, hist, list);
+    else if (npl <= 2) head_topk<2>(src, n_cand, k, k_eff, row, so, sco, lane, hist, list);
+    else if (npl <= 4) head_topk<4>(src, n_cand, k, k_eff, row, so, sco, lane, hist, list);
+    else if (npl <= 8) head_topk<8>(src, n_cand, k, k_eff, row, so, sco, lane, hist, list);
+    else if (npl <= 16) head_topk<16>(src, n_cand, k, k_eff, row, so, sco, lane, hist, list);
+    else head_topk<32>(src, n_cand, k, k_eff, row, so, sco, lane, hist, list);
   }
   __syncthreads();
-  group_union(sel_lds, first_lds, G * k_eff, uni + bh * umax, ucnt + bh, &cnt_lds);
+  group_union(sel_lds, bits_lds, G * k_eff, uni + bh * umax, ucnt + bh);
 }
 
 // ---------------------------------------------------------------------------
@@ -751,8 +822,7 @@ __global__ __launch_bounds__(256) void k_union_given(
     const int32_t* __restrict__ given, int given_k, int Hq, int Hkv, int G,
     int n_cand, int* __restrict__ uni, int* __restrict__ ucnt, int umax) {
   __shared__ int sel_lds[kMaxG * kMaxK];
-  __shared__ unsigned char first_lds[kMaxG * kMaxK];
-  __shared__ int cnt_lds;
+  __shared__ unsigned bits_lds[kBitmapWords];
   const int64_t bh = blockIdx.x;
   const int64_t b = bh / Hkv, hk = bh % Hkv;
   const int M = G * given_k;
@@ -762,7 +832,7 @@ __global__ __launch_bounds__(256) void k_union_given(
     sel_lds[i] = (id >= 0 && id < n_cand) ? id : -1;
   }
   __syncthreads();
-  group_union(sel_lds, first_lds, M, uni + bh * umax, ucnt + bh, &cnt_lds);
+  group_union(sel_lds, bits_lds, M, uni + bh * umax, ucnt + bh);
 }
 
 // ---------------------------------------------------------------------------
@@ -892,14 +962,15 @@ struct TileAttn {
 // k_attend: split attention, one partial (max, sum, acc[d]) per workgroup
 // ---------------------------------------------------------------------------
 // Tiles of a (b, kv head): tiles_per_seg per union segment, then ceil(|W| /
-// 64) window tiles. Workgroup j takes tiles 4j .. 4j+3, one per wave, and
-// merges its four waves in LDS.
+// 64) window tiles. Workgroup j takes tiles [4 tpw j, 4 tpw (j + 1)); wave w
+// takes every fourth of them from 4 tpw j + w, with an online softmax across
+// its tiles, and the workgroup merges its four waves in LDS.
 template <typename T, int D, int G>
 __global__ __launch_bounds__(256) void k_attend(
     const T* __restrict__ q, const T* __restrict__ K, const T* __restrict__ V,
     const int* __restrict__ uni, const int* __restrict__ ucnt,
     float* __restrict__ part, int Hq, int Hkv, int64_t cap, int c,
-    int tiles_per_seg, int64_t ws, int64_t t, int umax, int maxwg,
+    int tiles_per_seg, int64_t ws, int64_t t, int umax, int maxwg, int tpw,
     float qscale) {
   using TA = TileAttn<T, D, G>;
   constexpr int EPL = TA::EPL, LPR = TA::LPR;
@@ -919,25 +990,26 @@ __global__ __launch_bounds__(256) void k_attend(
   const int seg_tiles = U * tiles_per_seg;
   const int win_tiles = (int)((t - ws + kTile - 1) / kTile);
   const int total = seg_tiles + win_tiles;
-  const int nwg = (total + 3) / 4;
+  const int nwg = (total + 4 * tpw - 1) / (4 * tpw);
   if (j >= nwg) return;
-
-  const int ti = j * 4 + wave;
-  int64_t start = 0;
-  int len = 0;
-  if (ti < seg_tiles) {
-    const int s = uni[bh * umax + ti / tiles_per_seg];
-    const int off = (ti % tiles_per_seg) * kTile;
-    start = (int64_t)s * c + off;
-    len = min(kTile, c - off);
-  } else if (ti < total) {
-    start = ws + (int64_t)(ti - seg_tiles) * kTile;
-    len = (int)min((int64_t)kTile, t - start);
-  }
 
   TA ta;
   ta.init(q + (b * Hq + hk * G) * D, qscale, lane);
-  if (len > 0) ta.tile(K, V, bh * cap + start, len, lane);   // wave-uniform
+  const int t_end = min(total, (j + 1) * 4 * tpw);
+  for (int ti = j * 4 * tpw + wave; ti < t_end; ti += 4) {   // wave-uniform
+    int64_t start;
+    int len;
+    if (ti < seg_tiles) {
+      const int s = uni[bh * umax + ti / tiles_per_seg];
+      const int off = (ti % tiles_per_seg) * kTile;
+      start = (int64_t)s * c + off;
+      len = min(kTile, c - off);
+    } else {
+      start = ws + (int64_t)(ti - seg_tiles) * kTile;
+      len = (int)min((int64_t)kTile, t - start);
+    }
+    ta.tile(K, V, bh * cap + start, len, lane);
+  }
   ta.reduce_rows();
 
   const int jj = lane % LPR;
@@ -1015,10 +1087,12 @@ __global__ __launch_bounds__(512) void k_decode_fused(
   // phi(q) and the scores live only until the top-k; the merge reuses them
   __shared__ __attribute__((aligned(16))) float area[AREA];
   __shared__ int sel_lds[G * kMaxK];
-  __shared__ unsigned char first_lds[G * kMaxK];
+  __shared__ unsigned bits_lds[kBitmapWords];
   __shared__ int uni_lds[G * kMaxK];
+  __shared__ unsigned hist_lds[G][256];
+  __shared__ u64 list_lds[G][kMaxK];
   __shared__ float wm[NW][G], wl[NW][G];
-  __shared__ int cnt_lds, ucnt_lds;
+  __shared__ int ucnt_lds;
   float* phq = area;                       // [G][N]
   float* sc = area + G * N;                // [G][kFusedMaxCand]
   float* wacc = area;                      // [NW][G][D]
@@ -1143,12 +1217,14 @@ __global__ __launch_bounds__(512) void k_decode_fused(
     float* sco = sel_scores ? sel_scores + (b * Hq + hq) * (int64_t)k : nullptr;
     const float* src = sc + wave * kFusedMaxCand;
     int* row = sel_lds + wave * k_eff;
+    unsigned* hist = hist_lds[wave];
+    u64* list = list_lds[wave];
     const int npl = (n_cand + 63) / 64;
-    if (npl <= 1) head_topk<1>(src, n_cand, k, k_eff, row, so, sco, lane);
-    else if (npl <= 2) head_topk<2>(src, n_cand, k, k_eff, row, so, sco, lane);
-    else if (npl <= 4) head_topk<4>(src, n_cand, k, k_eff, row, so, sco, lane);
-    else if (npl <= 8) head_topk<8>(src, n_cand, k, k_eff, row, so, sco, lane);
-    else head_topk<16>(src, n_cand, k, k_eff, row, so, sco, lane);
+    if (npl <= 1) head_topk<1>(src, n_cand, k, k_eff, row, so, sco, lane, hist, list);
+    else if (npl <= 2) head_topk<2>(src, n_cand, k, k_eff, row, so, sco, lane, hist, list);
+    else if (npl <= 4) head_topk<4>(src, n_cand, k, k_eff, row, so, sco, lane, hist, list);
+    else if (npl <= 8) head_topk<8>(src, n_cand, k, k_eff, row, so, sco, lane, hist, list);
+    else head_topk<16>(src, n_cand, k, k_eff, row, so, sco, lane, hist, list);
   } else {
     for (int i = wave - G; i < win_tiles; i += NW - G) {
       const int64_t start = ws + (int64_t)i * kTile;
@@ -1158,7 +1234,7 @@ __global__ __launch_bounds__(512) void k_decode_fused(
   __syncthreads();
 
   // ---- 4. union -----------------------------------------------------------
-  group_union(sel_lds, first_lds, G * k_eff, uni_lds, &ucnt_lds, &cnt_lds);
+  group_union(sel_lds, bits_lds, G * k_eff, uni_lds, &ucnt_lds);
   __syncthreads();
   const int seg_tiles = ucnt_lds * tiles_per_seg;
 
@@ -1204,28 +1280,30 @@ __global__ __launch_bounds__(512) void k_decode_fused(
 // ---------------------------------------------------------------------------
 // k_combine: log-sum-exp merge of the partials of each (b, q head)
 // ---------------------------------------------------------------------------
-// 256 threads per query head: the partials' maxima and scale factors are
-// computed in parallel, then 256 / D groups of threads sum disjoint subsets
+// 1024 threads per query head: the partials' maxima and scale factors are
+// computed in parallel, then 1024 / D groups of threads sum disjoint subsets
 // of the partials' accumulators and LDS adds the groups.
+constexpr int kCombineThreads = 1024;
+
 template <typename T, int D>
-__global__ __launch_bounds__(256) void k_combine(const float* __restrict__ part,
-                                                 const int* __restrict__ ucnt,
-                                                 T* __restrict__ out, int Hq,
-                                                 int Hkv, int G,
-                                                 int tiles_per_seg,
-                                                 int win_tiles, int maxwg) {
+__global__ __launch_bounds__(kCombineThreads) void k_combine(
+    const float* __restrict__ part, const int* __restrict__ ucnt,
+    T* __restrict__ out, int Hq, int Hkv, int G, int tiles_per_seg,
+    int win_tiles, int maxwg, int tpw) {
   constexpr int PSTRIDE = D + 4;
-  constexpr int NGRP = 256 / D;
+  constexpr int NT = kCombineThreads;
+  constexpr int NWAVE = NT / kWave;
+  constexpr int NGRP = NT / D;
   __shared__ float f_lds[kMaxWg];
-  __shared__ float red_lds[8];
-  __shared__ float acc_lds[256];
+  __shared__ float red_lds[2 * NWAVE];
+  __shared__ float acc_lds[NT];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t bhq = blockIdx.x;
   const int64_t b = bhq / Hq, hq = bhq % Hq;
   const int64_t hk = hq / G;
   const int g = (int)(hq % G);
   const int64_t bh = b * Hkv + hk;
-  const int nwg = (ucnt[bh] * tiles_per_seg + win_tiles + 3) / 4;
+  const int nwg = (ucnt[bh] * tiles_per_seg + win_tiles + 4 * tpw - 1) / (4 * tpw);
   if (nwg == 0) {                          // nothing attended (given ids only)
     if (tid < D) out[bhq * D + tid] = from_f32<T>(0.f);
     return;
@@ -1234,21 +1312,25 @@ __global__ __launch_bounds__(256) void k_combine(const float* __restrict__ part,
   const int64_t wstride = (int64_t)G * PSTRIDE;
 
   float mx = -INFINITY;
-  for (int w = tid; w < nwg; w += 256) mx = fmaxf(mx, pb[w * wstride]);
+  for (int w = tid; w < nwg; w += NT) mx = fmaxf(mx, pb[w * wstride]);
   mx = wave_max(mx);
   if (lane == 0) red_lds[wave] = mx;
   __syncthreads();
-  const float M = fmaxf(fmaxf(red_lds[0], red_lds[1]), fmaxf(red_lds[2], red_lds[3]));
+  float M = red_lds[0];
+#pragma unroll
+  for (int i = 1; i < NWAVE; ++i) M = fmaxf(M, red_lds[i]);
   float ls = 0.f;
-  for (int w = tid; w < nwg; w += 256) {
+  for (int w = tid; w < nwg; w += NT) {
     const float f = fast_exp2(pb[w * wstride] - M);
     f_lds[w] = f;
     ls = fmaf(pb[w * wstride + 1], f, ls);
   }
   ls = wave_sum(ls);
-  if (lane == 0) red_lds[4 + wave] = ls;
+  if (lane == 0) red_lds[NWAVE + wave] = ls;
   __syncthreads();
-  const float inv = 1.f / ((red_lds[4] + red_lds[5]) + (red_lds[6] + red_lds[7]));
+  float L = 0.f;
+#pragma unroll
+  for (int i = 0; i < NWAVE; ++i) L += red_lds[NWAVE + i];
   const int e = tid % D, grp = tid / D;
   float a = 0.f;
 #pragma unroll 4
@@ -1260,7 +1342,7 @@ __global__ __launch_bounds__(256) void k_combine(const float* __restrict__ part,
     float sum = 0.f;
 #pragma unroll
     for (int i = 0; i < NGRP; ++i) sum += acc_lds[i * D + tid];
-    out[bhq * D + tid] = from_f32<T>(sum * inv);
+    out[bhq * D + tid] = from_f32<T>(sum / L);
   }
 }
 
@@ -1466,52 +1548,66 @@ void launch_score(const Shape& s, const float* phiq, const float* summ,
 
 template <typename T, int D, int G>
 void launch_attend_g(const Shape& s, const void* q, const void* K, const void* V,
-                     unsigned char* w, const WsLayout& L, int grid_x, int64_t ws,
-                     int64_t t, hipStream_t st) {
+                     unsigned char* w, const WsLayout& L, int grid_x, int tpw,
+                     int64_t ws, int64_t t, hipStream_t st) {
   const float qscale = kLog2e / std::sqrt((float)s.d);
   launch(RADAR_K_ATTEND, k_attend<T, D, G>,
          dim3((unsigned)grid_x, (unsigned)(s.B * s.Hkv)), dim3(256), 0, st,
          reinterpret_cast<const T*>(q), reinterpret_cast<const T*>(K),
          reinterpret_cast<const T*>(V), reinterpret_cast<const int*>(w + L.uni),
          reinterpret_cast<const int*>(w + L.ucnt), reinterpret_cast<float*>(w + L.part),
-         s.Hq, s.Hkv, s.cap, s.c, L.tiles_per_seg, ws, t, L.umax, L.maxwg, qscale);
+         s.Hq, s.Hkv, s.cap, s.c, L.tiles_per_seg, ws, t, L.umax, L.maxwg, tpw,
+         qscale);
 }
 
 template <typename T, int D>
 void launch_attend_d(const Shape& s, const void* q, const void* K, const void* V,
-                     unsigned char* w, const WsLayout& L, int grid_x, int64_t ws,
-                     int64_t t, void* out, hipStream_t st) {
+                     unsigned char* w, const WsLayout& L, int grid_x, int tpw,
+                     int64_t ws, int64_t t, void* out, hipStream_t st) {
   switch (s.G) {
-    case 1: launch_attend_g<T, D, 1>(s, q, K, V, w, L, grid_x, ws, t, st); break;
-    case 2: launch_attend_g<T, D, 2>(s, q, K, V, w, L, grid_x, ws, t, st); break;
-    case 4: launch_attend_g<T, D, 4>(s, q, K, V, w, L, grid_x, ws, t, st); break;
-    default: launch_attend_g<T, D, 8>(s, q, K, V, w, L, grid_x, ws, t, st); break;
+    case 1: launch_attend_g<T, D, 1>(s, q, K, V, w, L, grid_x, tpw, ws, t, st); break;
+    case 2: launch_attend_g<T, D, 2>(s, q, K, V, w, L, grid_x, tpw, ws, t, st); break;
+    case 4: launch_attend_g<T, D, 4>(s, q, K, V, w, L, grid_x, tpw, ws, t, st); break;
+    default: launch_attend_g<T, D, 8>(s, q, K, V, w, L, grid_x, tpw, ws, t, st); break;
   }
   const int win_tiles = (int)ceil_div(t - ws, kTile);
-  launch(RADAR_K_COMBINE, k_combine<T, D>, dim3((unsigned)(s.B * s.Hq)), dim3(256), 0,
+  launch(RADAR_K_COMBINE, k_combine<T, D>, dim3((unsigned)(s.B * s.Hq)),
+         dim3(kCombineThreads), 0,
          st, reinterpret_cast<const float*>(w + L.part),
          reinterpret_cast<const int*>(w + L.ucnt), reinterpret_cast<T*>(out), s.Hq,
-         s.Hkv, s.G, L.tiles_per_seg, win_tiles, L.maxwg);
+         s.Hkv, s.G, L.tiles_per_seg, win_tiles, L.maxwg, tpw);
+}
+
+// Split of the attention work: tiles per wave (tpw) so that the grid still
+// holds about eight workgroups per CU (a grid only just above the resident
+// count leaves a long tail), but no more (fewer, larger workgroups mean fewer
+// partials to merge); and the grid width per (b, kv head) for the largest
+// union.
+struct AttendGrid {
+  int grid_x, tpw;
+};
+
+AttendGrid attend_grid(const Shape& s, const WsLayout& L, int u_bound, int64_t ws,
+                       int64_t t) {
+  const int64_t per_bh = (int64_t)u_bound * L.tiles_per_seg + ceil_div(t - ws, kTile);
+  const int64_t tiles = per_bh * s.B * s.Hkv;
+  const int64_t tpw = std::min<int64_t>(8, std::max<int64_t>(1, tiles / (4 * 8 * num_cu())));
+  return {(int)ceil_div(per_bh, 4 * tpw), (int)tpw};
 }
 
 // exact attention over the union in the workspace, then the merge
 radar_status launch_attend(const Shape& s, const void* q, const void* K,
-                           const void* V, int grid_x, int64_t ws, int64_t t,
+                           const void* V, const AttendGrid& ag, int64_t ws, int64_t t,
                            void* out, unsigned char* w, const WsLayout& L,
                            hipStream_t st) {
   if (s.dt == RADAR_BF16) {
-    if (s.d == 64) launch_attend_d<bf16_t, 64>(s, q, K, V, w, L, grid_x, ws, t, out, st);
-    else launch_attend_d<bf16_t, 128>(s, q, K, V, w, L, grid_x, ws, t, out, st);
+    if (s.d == 64) launch_attend_d<bf16_t, 64>(s, q, K, V, w, L, ag.grid_x, ag.tpw, ws, t, out, st);
+    else launch_attend_d<bf16_t, 128>(s, q, K, V, w, L, ag.grid_x, ag.tpw, ws, t, out, st);
   } else {
-    if (s.d == 64) launch_attend_d<float, 64>(s, q, K, V, w, L, grid_x, ws, t, out, st);
-    else launch_attend_d<float, 128>(s, q, K, V, w, L, grid_x, ws, t, out, st);
+    if (s.d == 64) launch_attend_d<float, 64>(s, q, K, V, w, L, ag.grid_x, ag.tpw, ws, t, out, st);
+    else launch_attend_d<float, 128>(s, q, K, V, w, L, ag.grid_x, ag.tpw, ws, t, out, st);
   }
   return launch_status();
-}
-
-int attend_grid(const WsLayout& L, int u_bound, int64_t ws, int64_t t) {
-  const int64_t win_tiles = ceil_div(t - ws, kTile);
-  return (int)ceil_div((int64_t)u_bound * L.tiles_per_seg + win_tiles, 4);
 }
 
 // ---- fused path -------------------------------------------------------------
@@ -1581,12 +1677,27 @@ radar_status launch_fused(const Shape& s, const void* q, const void* K, const vo
 // Which decode path a call takes: the fused one-workgroup-per-(b, kv head)
 // kernel when there are enough pairs to occupy every CU (or when forced),
 // and the shape fits its LDS plan; the split multi-kernel path otherwise.
-int choose_path(const Shape& s, int n_cand) {
+// A pair's HBM bytes in one decode step (summary rows plus the K/V of the
+// largest union and the window), the quantity one fused workgroup streams.
+int64_t pair_bytes(const Shape& s, int64_t t, int k) {
+  const int64_t past = std::max<int64_t>(0, t - s.w);
+  const int64_t ws = (int64_t)s.c * (past / s.c), n_cand = ws / s.c;
+  const int64_t u = std::min<int64_t>((int64_t)s.G * std::min<int64_t>(k, n_cand), n_cand);
+  const int64_t skv = s.dt == RADAR_BF16 ? 2 : 4;
+  return n_cand * s.n * 4 + (u * s.c + (t - ws)) * 2 * s.d * skv;
+}
+
+// Which decode path a call takes. Fused when the shape fits its LDS plan and
+// either there are enough (b, kv head) pairs to occupy every CU, or each
+// pair's step is small enough (<= 256 KB) that one workgroup streams it in a
+// few microseconds, less than the split path's extra launches cost.
+int choose_path(const Shape& s, int64_t t, int n_cand, int k) {
   const bool fits = s.G <= kFusedMaxG && n_cand <= kFusedMaxCand &&
                     !(s.dt == RADAR_F32 && s.d == 128);
   if (!fits || g_path_override == RADAR_PATH_SPLIT) return RADAR_PATH_SPLIT;
   if (g_path_override == RADAR_PATH_FUSED) return RADAR_PATH_FUSED;
-  return (int64_t)s.B * s.Hkv >= num_cu() ? RADAR_PATH_FUSED : RADAR_PATH_SPLIT;
+  if ((int64_t)s.B * s.Hkv >= num_cu()) return RADAR_PATH_FUSED;
+  return pair_bytes(s, t, k) <= (256 << 10) ? RADAR_PATH_FUSED : RADAR_PATH_SPLIT;
 }
 
 void window_split(const Shape& s, int64_t t, int64_t* ws, int* n_cand) {
@@ -1618,7 +1729,7 @@ int32_t radar_decode_path(const radar_config* cfg, int64_t t, int32_t k) {
   int64_t ws;
   int n_cand;
   window_split(s, t, &ws, &n_cand);
-  return choose_path(s, n_cand);
+  return choose_path(s, t, n_cand, k);
 }
 
 radar_status radar_profile_enable(int32_t on) {
@@ -1744,13 +1855,13 @@ radar_status radar_decode(const radar_config* cfg, const void* q, const void* K,
   if (n_cand > kMaxCand) return RADAR_EUNSUPPORTED;
   const int k_eff = std::min(k, n_cand);
 
-  if (choose_path(s, n_cand) == RADAR_PATH_FUSED)
+  if (choose_path(s, t, n_cand, k) == RADAR_PATH_FUSED)
     return launch_fused(s, q, K, V, omega, summaries, ws, t, n_cand, k, k_eff, out,
                         selected, scores, stream);
 
   const int u_bound = std::min(s.G * k_eff, n_cand);
-  const int grid_x = attend_grid(L, u_bound, ws, t);
-  if (grid_x > kMaxWg) return RADAR_EUNSUPPORTED;
+  const AttendGrid ag = attend_grid(s, L, u_bound, ws, t);
+  if (ag.grid_x > kMaxWg) return RADAR_EUNSUPPORTED;
 
   unsigned char* w = reinterpret_cast<unsigned char*>(workspace);
   float* phiq = reinterpret_cast<float*>(w + L.phiq);
@@ -1771,7 +1882,7 @@ radar_status radar_decode(const radar_config* cfg, const void* q, const void* K,
          selected, scores);
   r = launch_status();
   if (r != RADAR_OK) return r;
-  return launch_attend(s, q, K, V, grid_x, ws, t, out, w, L, stream);
+  return launch_attend(s, q, K, V, ag, ws, t, out, w, L, stream);
 }
 
 radar_status radar_attend_selected(const radar_config* cfg, const void* q,
@@ -1794,9 +1905,10 @@ radar_status radar_attend_selected(const radar_config* cfg, const void* q,
   int64_t ws;
   int n_cand;
   window_split(s, t, &ws, &n_cand);
+  if (n_cand > kMaxCand) return RADAR_EUNSUPPORTED;
   const int u_bound = std::min(s.G * k, n_cand);
-  const int grid_x = attend_grid(L, u_bound, ws, t);
-  if (grid_x > kMaxWg) return RADAR_EUNSUPPORTED;
+  const AttendGrid ag = attend_grid(s, L, u_bound, ws, t);
+  if (ag.grid_x > kMaxWg) return RADAR_EUNSUPPORTED;
   unsigned char* w = reinterpret_cast<unsigned char*>(workspace);
   launch(RADAR_K_TOPK, k_union_given, dim3((unsigned)(s.B * s.Hkv)), dim3(256), 0,
          stream, selected, k, s.Hq, s.Hkv, s.G, n_cand,
@@ -1804,7 +1916,7 @@ radar_status radar_attend_selected(const radar_config* cfg, const void* q,
          L.umax);
   r = launch_status();
   if (r != RADAR_OK) return r;
-  return launch_attend(s, q, K, V, grid_x, ws, t, out, w, L, stream);
+  return launch_attend(s, q, K, V, ag, ws, t, out, w, L, stream);
 }
 
 }  // extern "C"

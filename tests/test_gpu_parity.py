@@ -104,7 +104,8 @@ def test_full_size_sampled(name, steps, ngroups, path):
 
 def test_path_choice():
     """The fused path serves shapes with at least one (b, kv head) pair per
-    CU; fewer pairs, G > 4 or more than 1024 candidates take the split path."""
+    CU, or small steps; G > 4 or more than 1024 candidates take the split
+    path."""
     def cfg(wl):
         return H.config_of(wl, wl.t0 + 1)
     n_cu = torch.cuda.get_device_properties(0).multi_processor_count
@@ -113,6 +114,9 @@ def test_path_choice():
     assert radar.decode_path(cfg(mha), mha.t0 + 1, mha.top_k) == radar.PATH_FUSED
     g5 = WORKLOADS["gqa_512k"]
     assert radar.decode_path(cfg(g5), g5.t0 + 1, g5.top_k) == radar.PATH_SPLIT
+    # a small step per pair (launch-bound): fused even with few pairs
+    tiny = WORKLOADS["tiny"]
+    assert radar.decode_path(cfg(tiny), tiny.t0 + 1, tiny.top_k) == radar.PATH_FUSED
     g8 = mha.scaled(n_q_heads=32, n_kv_heads=4, batch=128)
     assert radar.decode_path(cfg(g8), g8.t0 + 1, 16) == radar.PATH_SPLIT
     radar.set_decode_path(radar.PATH_FUSED)
@@ -269,3 +273,55 @@ def test_errors_leave_outputs_untouched():
     assert e.value.status == 3
     torch.cuda.synchronize()
     assert bool((summ == 5.0).all()) and bool((out == 3.0).all())
+
+
+@PATHS
+@pytest.mark.parametrize("k", [3, 6, 13])
+def test_exact_ties_take_lower_index(path, k):
+    """Identical segments have bit-identical summaries and scores; the
+    selection must then be the oracle's order exactly: score descending,
+    lower segment index first among equal scores."""
+    _announce(f"exact ties k={k} path={path}")
+    rng = np.random.default_rng(123 + k)
+    d, c, n, n_types, reps = 64, 16, 128, 4, 8
+    B, NH = 1, 2
+    types = rng.standard_normal((NH, n_types, c, d)) * 0.4
+    order = rng.permutation(n_types * reps) % n_types      # segment -> type
+    t0 = n_types * reps * c + 5                              # + a ragged tail
+    K = np.zeros((B, NH, t0 + 1, d))
+    for h in range(NH):
+        for s_, ty in enumerate(order):
+            K[0, h, s_ * c:(s_ + 1) * c] = types[h, ty]
+        K[0, h, n_types * reps * c:] = rng.standard_normal((t0 + 1 - n_types * reps * c, d)) * 0.4
+    V = rng.standard_normal((B, NH, t0 + 1, d))
+    q = rng.standard_normal((B, NH, d)) * 0.5
+    om = rng.standard_normal((n, d))
+    wl = Workload("ties", B, NH, NH, d, t0, c, k, n, 5, "f32", 1, "gauss", 1)
+    cfg = H.config_of(wl, t0 + 1)
+    Kt = torch.tensor(K, dtype=torch.float32, device="cuda")
+    Vt = torch.tensor(V, dtype=torch.float32, device="cuda")
+    qt = torch.tensor(q, dtype=torch.float32, device="cuda")
+    omt = torch.tensor(om, dtype=torch.float32, device="cuda")
+    summ = radar.new_summaries(cfg, "cuda")
+    t = t0
+    radar.build_index(cfg, Kt, omt, t, summ)
+    sel = torch.empty(B, NH, k, dtype=torch.int32, device="cuda")
+    radar.set_decode_path(path)
+    try:
+        radar.decode(cfg, qt, Kt, Vt, omt, summ, t, k, selected=sel)
+    finally:
+        radar.set_decode_path(radar.PATH_AUTO)
+    torch.cuda.synchronize()
+    # the GPU's own summaries of identical segments must be identical
+    sm = summ.cpu().numpy()
+    for h in range(NH):
+        for ty in range(n_types):
+            segs = np.nonzero(order == ty)[0]
+            for s_ in segs[1:]:
+                assert np.array_equal(sm[0, h, s_], sm[0, h, segs[0]])
+    ws, n_cand = orc.window_split(t, c, wl.window)
+    for h in range(NH):
+        summ64 = orc.segment_summaries(K[0, h, :t], om, c)
+        sc = orc.segment_scores(orc.random_features(q[0, h], om), summ64[:n_cand])
+        ref = orc.top_segments(sc, k)
+        assert sel[0, h].cpu().numpy().tolist() == ref.tolist()
