@@ -14,6 +14,9 @@ HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
     # packed fp32 ops are kept out of the device code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA results land in ordinary VGPRs, so the exp2 epilogue of the index
+    # build reads them without an accumulator-register copy per element
+    "-mllvm", "-amdgpu-mfma-vgpr-form=1",
 ]
 
 

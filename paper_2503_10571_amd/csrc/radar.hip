@@ -51,6 +51,7 @@ typedef uint16_t bf16_t;           // storage type of a bfloat16 value
 typedef unsigned long long u64;   // 64-bit type of the wave shuffles
 typedef __attribute__((__vector_size__(8 * sizeof(short)))) short bf16x8_t;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4_t;
+typedef __bf16 bf16x2v_t __attribute__((ext_vector_type(2)));
 
 // ---------------------------------------------------------------------------
 // element helpers
@@ -261,8 +262,9 @@ __device__ __forceinline__ u64 wave_max_u64(u64 v) {
 // Work item = one (b, kv head, segment) and one slice of 64*FT features.
 // Wave w of the workgroup owns features [w*16*FT, (w+1)*16*FT) of the slice
 // and keeps that slice of Omega (rounded to the MFMA input type) resident in
-// registers as MFMA B operands for the whole kernel. Keys stream through LDS
-// in tiles of 64 tokens (register-prefetched one tile ahead); every wave
+// registers as MFMA B operands for the whole kernel. Keys stream through two
+// LDS buffers in tiles of 64 tokens (register-prefetched one tile ahead, one
+// barrier per tile); every wave
 // multiplies each 16-token sub-tile with its Omega slice on the matrix cores,
 // applies exp2(acc * s1 - |k|^2 * s2) and adds the result into per-lane
 // column sums. At the segment's end the sums are reduced across the four
@@ -305,8 +307,8 @@ __global__ __launch_bounds__(256) void k_build(
   constexpr int CPT = BT::kChunksPerThread;
   static_assert(CPT >= 1 && (256 % CPR) == 0, "tile shape");
 
-  __shared__ __attribute__((aligned(16))) unsigned char tile_lds[kTile * BT::kPitch];
-  __shared__ float nrm_lds[kTile];
+  __shared__ __attribute__((aligned(16))) unsigned char tile_lds[2][kTile * BT::kPitch];
+  __shared__ float nrm_lds[2][kTile];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -342,63 +344,75 @@ __global__ __launch_bounds__(256) void k_build(
 #pragma unroll
   for (int f = 0; f < FT; ++f) psum[f] = 0.f;
 
-  // address of tile `tl` of item `it`
-  auto tile_src = [&](int64_t it, int tl, int& valid) -> const T* {
-    const int64_t bh = it / seg_count;
-    const int64_t s = seg_first + (it % seg_count);
-    const int64_t row0 = s * (int64_t)c + (int64_t)tl * kTile;
-    valid = min(kTile, c - tl * kTile);
-    return K + bh * kv_head_stride_rows * D + row0 * D;
+  // Base row pointer of an item (one (b, kv head, segment)); computed once
+  // per segment, in 32-bit arithmetic (item counts stay below 2^31).
+  auto item_base = [&](int64_t it) -> const T* {
+    const uint32_t u = (uint32_t)it, sc = (uint32_t)seg_count;
+    const uint32_t bh = u / sc, s = (uint32_t)seg_first + u % sc;
+    return K + ((int64_t)bh * kv_head_stride_rows + (int64_t)s * c) * D;
   };
 
   uint4 pre[CPT];
   int pre_valid = 0;
-  int64_t item = blockIdx.x;
-  int tl = 0;
-  auto fetch = [&](int64_t it, int t_) {
-    const T* src = tile_src(it, t_, pre_valid);
+  // tile tl of the item whose rows start at `base`
+  auto fetch = [&](const T* base, int tl_) {
+    pre_valid = min(kTile, c - tl_ * kTile);
+    const T* src = base + (int64_t)tl_ * kTile * D;
 #pragma unroll
     for (int p = 0; p < CPT; ++p) {
       const int ci = p * 256 + tid;
       // rows past the segment re-read its last row; they are masked out
-      // of the sums (ok[] below)
+      // of the sums below
       const int row = min(ci / CPR, pre_valid - 1), ch = ci % CPR;
       pre[p] = ld_stream(reinterpret_cast<const unsigned char*>(src + (int64_t)row * D) +
                          ch * 16);
     }
   };
-  if (item < n_items) fetch(item, 0);
-
-  while (item < n_items) {
-    const int valid = pre_valid;
-    __syncthreads();                       // previous tile fully consumed
+  // registers -> LDS buffer `buf`, with |k|^2 * s2 per row: the CPR chunks
+  // of a row sit in CPR consecutive lanes, summed by DPP row reductions
+  auto stage = [&](int buf) {
+    unsigned char* tb = tile_lds[buf];
 #pragma unroll
     for (int p = 0; p < CPT; ++p) {
       const int ci = p * 256 + tid;
       const int row = ci / CPR, ch = ci % CPR;
-      *reinterpret_cast<uint4*>(tile_lds + row * BT::kPitch + ch * 16) = pre[p];
-      float e[16 / sizeof(T)];
-      unpack16<T>(pre[p], e);
+      *reinterpret_cast<uint4*>(tb + row * BT::kPitch + ch * 16) = pre[p];
       float sq = 0.f;
+      if constexpr (sizeof(T) == 2) {
+        // bf16 pairs: one dot2 per 32-bit word (exact products, fp32 sum)
+        const uint32_t w[4] = {pre[p].x, pre[p].y, pre[p].z, pre[p].w};
 #pragma unroll
-      for (int i = 0; i < (int)(16 / sizeof(T)); ++i) sq = fmaf(e[i], e[i], sq);
+        for (int i = 0; i < 4; ++i) {
+          const bf16x2v_t v = __builtin_bit_cast(bf16x2v_t, w[i]);
+          sq = __builtin_amdgcn_fdot2_f32_bf16(v, v, sq, false);
+        }
+      } else {
+        float e[4];
+        unpack16<T>(pre[p], e);
 #pragma unroll
-      for (int m = 1; m < CPR; m <<= 1) sq += __shfl_xor(sq, m);
-      if (ch == 0) nrm_lds[row] = sq * s2;
+        for (int i = 0; i < 4; ++i) sq = fmaf(e[i], e[i], sq);
+      }
+      if constexpr (CPR == 8) {
+        sq += dpp_f<kDppQuadSwap1>(sq);
+        sq += dpp_f<kDppQuadSwap2>(sq);
+        sq += dpp_f<kDppHalfMirror>(sq);
+      } else {
+        sq = row_sum(sq);
+        if constexpr (CPR == 32) sq += __shfl_xor(sq, 16);
+      }
+      if (ch == 0) nrm_lds[buf][row] = sq * s2;
     }
-    __syncthreads();
+  };
 
-    // prefetch the next tile while this one is multiplied
-    int64_t nitem = item;
-    int ntl = tl + 1;
-    if (ntl == ntiles) { nitem += gridDim.x; ntl = 0; }
-    if (nitem < n_items) fetch(nitem, ntl);
-
+  // 16-token sub-tiles of the tile in `buf`; FULL: no rows to mask
+  auto compute = [&](int buf, int valid, auto full_tag) {
+    constexpr bool FULL = decltype(full_tag)::value;
+    const unsigned char* tb = tile_lds[buf];
 #pragma unroll
     for (int st = 0; st < kTile / 16; ++st) {
-      if (st * 16 >= valid) break;
+      if (!FULL && st * 16 >= valid) break;
       typename MC::frag_t afrag[KB];
-      const unsigned char* arow = tile_lds + (st * 16 + col) * BT::kPitch;
+      const unsigned char* arow = tb + (st * 16 + col) * BT::kPitch;
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb) {
         if constexpr (sizeof(T) == 2)
@@ -407,35 +421,65 @@ __global__ __launch_bounds__(256) void k_build(
           afrag[kb] = *reinterpret_cast<const float*>(arow + (kb * 4 + grp) * 4);
       }
       float nb[4];
-      bool ok[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int r = st * 16 + grp * 4 + j;
-        nb[j] = nrm_lds[r];
-        ok[j] = r < valid;
-      }
+      for (int j = 0; j < 4; ++j) nb[j] = nrm_lds[buf][st * 16 + grp * 4 + j];
+      // head-dim block outer, feature tile inner: FT independent
+      // accumulation chains keep the matrix pipe busy
+      f32x4_t acc[FT];
 #pragma unroll
-      for (int f = 0; f < FT; ++f) {
-        f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+      for (int f = 0; f < FT; ++f) acc[f] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int kb = 0; kb < KB; ++kb) {
+      for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+        for (int f = 0; f < FT; ++f) {
           if constexpr (sizeof(T) == 2)
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(afrag[kb], bfrag[f][kb], acc, 0, 0, 0);
+            acc[f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(afrag[kb], bfrag[f][kb], acc[f], 0, 0, 0);
           else
-            acc = __builtin_amdgcn_mfma_f32_16x16x4f32(afrag[kb], bfrag[f][kb], acc, 0, 0, 0);
+            acc[f] = __builtin_amdgcn_mfma_f32_16x16x4f32(afrag[kb], bfrag[f][kb], acc[f], 0, 0, 0);
         }
+#pragma unroll
+      for (int f = 0; f < FT; ++f)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const float v = fast_exp2(fmaf(acc[j], s1, -nb[j]));
-          psum[f] += ok[j] ? v : 0.f;
+          const float v = fast_exp2(fmaf(acc[f][j], s1, -nb[j]));
+          if (FULL) psum[f] += v;
+          else psum[f] += (st * 16 + grp * 4 + j < valid) ? v : 0.f;
         }
-      }
     }
+  };
+
+  // Pipeline, one barrier per tile: tile i is multiplied from one LDS buffer
+  // while tile i+1 is in flight to registers; after the multiply the
+  // registers go to the other buffer.
+  int64_t item = blockIdx.x;
+  int tl = 0, buf = 0;
+  const T* base = nullptr;
+  if (item < n_items) {
+    base = item_base(item);
+    fetch(base, 0);
+    stage(0);
+  }
+  int valid = pre_valid;
+  __syncthreads();
+  while (item < n_items) {
+    int64_t nitem = item;
+    int ntl = tl + 1;
+    const T* nbase = base;
+    if (ntl == ntiles) {
+      nitem += gridDim.x;
+      ntl = 0;
+      if (nitem < n_items) nbase = item_base(nitem);
+    }
+    const bool more = nitem < n_items;
+    if (more) fetch(nbase, ntl);
+
+    if (valid == kTile) compute(buf, valid, std::true_type{});
+    else compute(buf, valid, std::false_type{});
 
     if (tl == ntiles - 1) {                // segment complete
-      const int64_t bh = item / seg_count;
-      const int64_t s = seg_first + (item % seg_count);
-      float* dst = summ + (bh * s_cap + s) * n + fbase;
+      const uint32_t u = (uint32_t)item, sc = (uint32_t)seg_count;
+      const int64_t bh = u / sc, sg = seg_first + u % sc;
+      float* dst = summ + (bh * s_cap + sg) * n + fbase;
 #pragma unroll
       for (int f = 0; f < FT; ++f) {
         float v = psum[f];
@@ -445,8 +489,13 @@ __global__ __launch_bounds__(256) void k_build(
         psum[f] = 0.f;
       }
     }
+    if (more) stage(buf ^ 1);
+    __syncthreads();
+    buf ^= 1;
+    valid = pre_valid;
     item = nitem;
     tl = ntl;
+    base = nbase;
   }
 }
 
@@ -1459,6 +1508,7 @@ radar_status launch_build_t(const Shape& s, const void* K, const float* omega,
   const int slices = s.n / (64 * FT);
   const int64_t items = (int64_t)s.B * s.Hkv * seg_count;
   if (items == 0) return RADAR_OK;
+  if (items >= ((int64_t)1 << 31)) return RADAR_EUNSUPPORTED;   // 32-bit item ids
   auto kern = k_build<T, D, FT>;
   int per_cu = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, 256, 0) != hipSuccess || per_cu < 1)
