@@ -18,6 +18,7 @@ from __future__ import annotations
 
 import argparse
 import ctypes
+import dataclasses
 import json
 import math
 import os
@@ -53,8 +54,10 @@ class Stepper:
     """Direct C-ABI calls with pre-marshalled arguments (the per-step host
     cost stays small next to the GPU time)."""
 
-    def __init__(self, cfg, inp, K, V, summ, ws, out, k):
+    def __init__(self, cfg, inp, K, V, summ, ws, out, k, sqrt_schedule=False):
         self.L = radar.lib()
+        self.sqrt = sqrt_schedule
+        self.restructures = 0
         self.cfg_c = cfg.c_struct()
         self.cfgp = ctypes.byref(self.cfg_c)
         self.inp = inp
@@ -77,6 +80,18 @@ class Stepper:
                                  self.vn[i], self.om, t, self.summ, self.stream)
         if st:
             raise radar.RadarError("radar_append", st)
+        if self.sqrt:
+            # Algorithm 1: c = floor(sqrt(t + 1)), W = [c^2, t + 1); rebuild
+            # the summaries when t + 1 is a perfect square
+            c = math.isqrt(t + 1)
+            if c != self.cfg_c.seg_len:
+                self.cfg_c.seg_len = c
+                st = self.L.radar_build_index(self.cfgp, self.K, self.om, t + 1,
+                                              self.summ, self.stream)
+                if st:
+                    raise radar.RadarError("radar_build_index", st)
+                self.restructures += 1
+            self.cfg_c.window = t + 1 - c * c
         st = self.L.radar_decode(self.cfgp, self.q[i], self.K, self.V, self.om,
                                  self.summ, t + 1, self.k, self.out, sel, None,
                                  self.ws, self.ws_n, self.stream)
@@ -95,12 +110,16 @@ def union_sizes(sel, G):
     return out
 
 
-def step_bytes(wl, t, U, s_kv):
+def step_bytes(wl, t, U, s_kv, sqrt_schedule=False):
     """Algorithmic HBM bytes of one step whose decode runs at length t (the
     append wrote row t - 1). U: union size per (b, kv head).
     Returns (whole step, decode call, K/V gather)."""
-    c, d, n = wl.seg_len, wl.head_dim, wl.n_features
-    ws, n_cand = window_split(t, c, wl.window)
+    d, n = wl.head_dim, wl.n_features
+    if sqrt_schedule:
+        c, w = radar.schedule_sqrt(t)
+    else:
+        c, w = wl.seg_len, wl.window
+    ws, n_cand = window_split(t, c, w)
     W = t - ws
     BH = wl.batch * wl.n_kv_heads
     summ = BH * n_cand * n * 4
@@ -109,6 +128,8 @@ def step_bytes(wl, t, U, s_kv):
     om = n * d * 4
     app = BH * 2 * d * s_kv
     close = BH * (c * d * s_kv + n * 4) if t % c == 0 else 0
+    if sqrt_schedule and w == 0:       # restructure: all t keys re-summarised
+        close += BH * (t * d * s_kv + (t // c) * n * 4)
     decode = summ + kv + qo + om
     return decode + app + close, decode, kv
 
@@ -143,12 +164,14 @@ def blas_threads():
 
 
 def cpu_baseline(wl, inp, first_step, n_steps, n_heads, min_s=10.0,
-                 max_s=25.0):
+                 max_s=25.0, sqrt_schedule=False):
     """The fp64 oracle (as it stands) on `n_heads` sampled (b, q head) pairs
     over the timed steps: per step a segment-close refresh when one is due,
     then phi(q), scores, top-k and exact attention. The pass over the steps
     repeats until at least `min_s` seconds of work (at most `max_s`). Scaled
-    to the workload's tokens/s (all heads)."""
+    to the workload's tokens/s (all heads). With the sqrt schedule the
+    segment length follows Algorithm 1 and a perfect square rebuilds the
+    summaries inside the timed step."""
     from oracle import radar_oracle as orc
     G, c = wl.group, wl.seg_len
     rng = np.random.default_rng(5)
@@ -163,7 +186,8 @@ def cpu_baseline(wl, inp, first_step, n_steps, n_heads, min_s=10.0,
         keys = inp.keys_at(last, b, g).double().cpu().numpy()
         vals = inp.values_at(last, b, g).double().cpu().numpy()
         t_start = wl.t0 + first_step
-        summ = orc.segment_summaries(keys[:t_start], om, c)   # index (untimed)
+        c0 = orc.sqrt_schedule(t_start)[0] if sqrt_schedule else c
+        summ = orc.segment_summaries(keys[:t_start], om, c0)  # index (untimed)
         state.append([b, h, keys, vals, summ])
     qs = inp.q[first_step:last].double().cpu().numpy()
     start_summ = [st[4] for st in state]
@@ -174,16 +198,23 @@ def cpu_baseline(wl, inp, first_step, n_steps, n_heads, min_s=10.0,
             st[4] = s0
         for i in range(n_steps):
             t = wl.t0 + first_step + i + 1
+            if sqrt_schedule:
+                cs, w = orc.sqrt_schedule(t)
+            else:
+                cs, w = c, wl.window
             for st in state:
                 b, h, keys, vals, summ = st
-                if t % c == 0:              # the appended row closed a segment
+                if sqrt_schedule and w == 0:   # restructure at a square
+                    st[4] = summ = orc.segment_summaries(keys[:t], om, cs)
+                elif not sqrt_schedule and t % c == 0:
+                    # the appended row closed a segment
                     new = orc.segment_summaries(keys[:t], om, c,
                                                 first=t // c - 1)
                     st[4] = summ = np.concatenate([summ, new], 0)
-                ws, n_cand = orc.window_split(t, c, wl.window)
+                ws, n_cand = orc.window_split(t, cs, w)
                 phi_q = orc.random_features(qs[i, b, h], om)
                 _, sel = orc.decode_head(phi_q, summ, n_cand, wl.top_k)
-                toks = orc.attended_tokens(sel, c, ws, t)
+                toks = orc.attended_tokens(sel, cs, ws, t)
                 orc.attend(qs[i, b, h], keys, vals, toks)
                 done += 1
             if time.perf_counter() - t_begin > max_s:
@@ -220,6 +251,10 @@ def main():
     ap.add_argument("--build-reps", type=int, default=3)
     ap.add_argument("--path", default="auto", choices=["auto", "split", "fused"],
                     help="decode path (auto: the library's choice)")
+    ap.add_argument("--schedule", default="fixed", choices=["fixed", "sqrt"],
+                    help="fixed: the workload's segment length and window; "
+                         "sqrt: Algorithm 1's restructuring (c = sqrt(t) at "
+                         "perfect squares, W = [c^2, t)), rebuilds timed")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the decode path has no multi-GPU "
@@ -237,13 +272,24 @@ def main():
     total = W + Ksteps
     log(f"[bench] generating {wl.name} inputs ({total} steps)")
     inp = workloads.make_inputs(wl, "cuda", steps=total)
+    if args.schedule == "sqrt":
+        c0, w0 = radar.schedule_sqrt(wl.t0)
+        wl = wl.scaled(seg_len=c0, window=w0)
     cfg = radar.Config(wl.batch, wl.n_q_heads, wl.n_kv_heads, wl.head_dim,
                        wl.n_features, wl.seg_len, wl.window, wl.t0 + total,
                        wl.torch_dtype())
     s_kv = 2 if wl.dtype == "bf16" else 4
     K, V = inp.K, inp.V
     summ = radar.new_summaries(cfg, K.device)
-    ws = radar.new_workspace(cfg, wl.top_k, K.device)
+    if args.schedule == "sqrt":
+        # the largest scratch any step of the run needs (window up to 2c)
+        need = max(radar.workspace_bytes(
+            dataclasses.replace(cfg, seg_len=radar.schedule_sqrt(t)[0],
+                                window=radar.schedule_sqrt(t)[1]), wl.top_k)
+            for t in range(wl.t0, wl.t0 + total + 1))
+        ws = torch.empty(need, dtype=torch.uint8, device=K.device)
+    else:
+        ws = radar.new_workspace(cfg, wl.top_k, K.device)
     out = torch.empty_like(inp.q[0])
     torch.cuda.synchronize()
 
@@ -263,13 +309,17 @@ def main():
     build_tflops = build_flop / (build_ms * 1e-3) / 1e12
 
     # ---- decode steps ----------------------------------------------------
-    stp = Stepper(cfg, inp, K, V, summ, ws, out, wl.top_k)
+    stp = Stepper(cfg, inp, K, V, summ, ws, out, wl.top_k,
+                  sqrt_schedule=args.schedule == "sqrt")
     sel_log = torch.empty(Ksteps, wl.batch, wl.n_q_heads, wl.top_k,
                           dtype=torch.int32, device=K.device)
     log(f"[bench] warmup {W} steps")
     for i in range(W):
         stp.step(i)
     torch.cuda.synchronize()
+    t_timed = wl.t0 + W
+    seg_timed, win_timed = stp.cfg_c.seg_len, stp.cfg_c.window
+    restr_before = stp.restructures
     log(f"[bench] timing {Ksteps} steps")
     e0.record()
     for j in range(Ksteps):
@@ -279,6 +329,13 @@ def main():
     ms = e0.elapsed_time(e1)
     ms_step = ms / Ksteps
 
+    restructures = stp.restructures - restr_before
+    if args.schedule == "sqrt":
+        # restore the schedule state of the timed pass's start
+        stp.cfg_c.seg_len, stp.cfg_c.window = seg_timed, win_timed
+        radar.build_index(dataclasses.replace(cfg, seg_len=seg_timed,
+                                              window=win_timed),
+                          K, inp.omega, t_timed, summ)
     # the same steps again with every kernel bracketed by HIP events
     radar.profile_enable(True)
     for j in range(Ksteps):
@@ -293,12 +350,15 @@ def main():
     for j in range(Ksteps):
         t = wl.t0 + W + j + 1
         U = union_sizes(sel_np[j], wl.group)
-        b_all, b_dec, b_kv = step_bytes(wl, t, U, s_kv)
+        b_all, b_dec, b_kv = step_bytes(wl, t, U, s_kv,
+                                        sqrt_schedule=args.schedule == "sqrt")
         tot_bytes += b_all
         dec_bytes += b_dec
         kv_bytes += b_kv
     step_gbps = tot_bytes / (ms * 1e-3) / 1e9
-    path = radar.decode_path(cfg, wl.t0 + W + 1, wl.top_k)
+    path = radar.decode_path(dataclasses.replace(cfg, seg_len=seg_timed,
+                                                 window=win_timed),
+                             wl.t0 + W + 1, wl.top_k)
     # dominant kernel: the fused decode (all decode bytes), or the split
     # path's gather-attention kernel (the K/V bytes)
     if path == radar.PATH_FUSED:
@@ -317,7 +377,8 @@ def main():
     cpu = None
     if args.cpu_baseline:
         log("[bench] cpu baseline (fp64 oracle)")
-        cpu = cpu_baseline(wl, inp, W, Ksteps, n_heads=args.cpu_heads)
+        cpu = cpu_baseline(wl, inp, W, Ksteps, n_heads=args.cpu_heads,
+                           sqrt_schedule=args.schedule == "sqrt")
 
     copy_gbps = None
     if args.calibrate_copy:
@@ -359,6 +420,8 @@ def main():
             "window": wl.window,
             "decode_path": {radar.PATH_SPLIT: "split",
                             radar.PATH_FUSED: "fused"}.get(path, "?"),
+            "schedule": args.schedule,
+            "restructures": restructures,
         },
         "hbm_GBps": round(step_gbps, 1),
         "hbm_frac": round(step_gbps / HBM_PEAK_GBPS, 4),

@@ -142,6 +142,18 @@ radar_status radar_attend_selected(const radar_config* cfg, const void* q,
                                    size_t workspace_bytes,
                                    hipStream_t stream);
 
+/* Algorithm 1's dynamic restructuring (Section 2.2, Appendix A): the
+ * segment length becomes sqrt(t) whenever t is a perfect square, the c
+ * segments of c tokens then cover [0, c^2), and later tokens wait in the
+ * buffer W until the next perfect square. For context length t >= 1 this
+ * writes c = floor(sqrt(t)) to *seg_len and t - c^2 to *window: a config
+ * with these two fields makes radar_decode attend exactly Algorithm 1's
+ * candidates (the c restructured segments) and buffer W = [c^2, t). At a
+ * perfect square the caller rebuilds the summaries with radar_build_index
+ * under the new seg_len (summaries then need capacity / c rows for the
+ * smallest c used). Host-only; launches nothing. */
+radar_status radar_schedule_sqrt(int64_t t, int32_t* seg_len, int32_t* window);
+
 /* Decode paths. The split path runs phi(q), scores, top-k, attention and
  * merge as separate kernels spread over the whole chip; the fused path runs
  * the whole step of one (b, kv head) in one workgroup, which suits shapes

@@ -30,7 +30,7 @@ import numpy as np
 __all__ = [
     "random_features", "segment_summaries", "window_split", "segment_scores",
     "top_segments", "attended_tokens", "attend", "decode_head", "decode",
-    "full_attention",
+    "full_attention", "sqrt_schedule",
 ]
 
 
@@ -183,3 +183,22 @@ def decode(q, K, V, omega, summaries, t, k, c, w):
                 out[b, h] = attend(q[b, h], K[b, g], V[b, g], toks)
     return dict(out=out, selected=selected, sel_scores=sel_scores,
                 scores=scores, union=union, ws=ws, n_cand=n_cand, k_eff=k_eff)
+
+
+def sqrt_schedule(t):
+    """Algorithm 1's dynamic restructuring (Section 2.2, Appendix A): the
+    segment length is reset to sqrt(t) whenever t is a perfect square, the c
+    segments of c tokens then cover [0, c^2), and every later token waits in
+    the buffer W until the next perfect square. At context length t >= 1
+    this gives c = floor(sqrt(t)) and W = [c^2, t).
+
+    Returns (c, w) such that window_split(t, c, w) reproduces that state:
+    w = t - c^2, so ws = c * floor(c^2 / c) = c^2 and the candidates are
+    the c restructured segments."""
+    assert t >= 1
+    c = int(np.floor(np.sqrt(t)))
+    while c * c > t:
+        c -= 1
+    while (c + 1) * (c + 1) <= t:
+        c += 1
+    return c, t - c * c

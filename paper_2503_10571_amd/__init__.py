@@ -92,6 +92,9 @@ def lib() -> ctypes.CDLL:
         L.radar_last_error.restype = ctypes.c_char_p
         L.radar_abi_version.restype = ctypes.c_int32
         L.radar_profile_enable.argtypes = [i32]
+        L.radar_schedule_sqrt.argtypes = [i64, ctypes.POINTER(i32),
+                                          ctypes.POINTER(i32)]
+        L.radar_schedule_sqrt.restype = ctypes.c_int
         L.radar_set_decode_path.argtypes = [i32]
         L.radar_set_decode_path.restype = ctypes.c_int
         L.radar_decode_path.argtypes = [cfgp, i64, i32]
@@ -207,6 +210,15 @@ KERNELS = ("append", "build", "phi_q", "score", "topk", "attend", "combine",
            "fused")
 
 
+def schedule_sqrt(t: int):
+    """Algorithm 1's restructuring schedule at context length t: (segment
+    length c = floor(sqrt(t)), window t - c^2)."""
+    c, w = ctypes.c_int32(), ctypes.c_int32()
+    _check("radar_schedule_sqrt", lib().radar_schedule_sqrt(t, ctypes.byref(c),
+                                                            ctypes.byref(w)))
+    return c.value, w.value
+
+
 PATH_AUTO, PATH_SPLIT, PATH_FUSED = 0, 1, 2
 
 
@@ -237,27 +249,58 @@ def profile_read() -> dict:
 
 class RadarLayer:
     """Device state of one Radar layer: K/V cache, summaries, Omega and a
-    decode workspace, driven through the C ABI (append, then decode)."""
+    decode workspace, driven through the C ABI (append, then decode).
+
+    schedule="fixed" keeps cfg.seg_len and cfg.window. schedule="sqrt"
+    follows Algorithm 1's restructuring: at every perfect-square context
+    length the summaries are rebuilt with c = sqrt(t), and each decode
+    attends the c restructured segments' top-k plus the buffer [c^2, t)."""
 
     def __init__(self, cfg: Config, omega, K=None, V=None, t: int = 0,
-                 top_k: int = 16, device="cuda"):
-        self.cfg, self.k = cfg, top_k
+                 top_k: int = 16, device="cuda", schedule: str = "fixed"):
+        if schedule not in ("fixed", "sqrt"):
+            raise ValueError(schedule)
+        self.cfg, self.k, self.schedule = cfg, top_k, schedule
         shape = (cfg.batch, cfg.n_kv_heads, cfg.capacity, cfg.head_dim)
         self.K = K if K is not None else torch.zeros(shape, dtype=cfg.dtype, device=device)
         self.V = V if V is not None else torch.zeros(shape, dtype=cfg.dtype, device=device)
         self.omega = omega
-        self.summaries = new_summaries(cfg, self.K.device)
-        self.workspace = new_workspace(cfg, top_k, self.K.device)
         self.t = t
+        if schedule == "sqrt":
+            c0 = schedule_sqrt(max(t, 1))[0]
+            rows = cfg.capacity // c0              # the smallest c comes first
+            self.summaries = torch.zeros(cfg.batch, cfg.n_kv_heads, rows,
+                                         cfg.n_features, dtype=torch.float32,
+                                         device=self.K.device)
+            self.cfg = self._cfg_at(max(t, 1))
+        else:
+            self.summaries = new_summaries(cfg, self.K.device)
+        self.workspace = new_workspace(self.cfg, top_k, self.K.device)
+        self.restructures = 0
         if t > 0:
-            build_index(cfg, self.K, omega, t, self.summaries)
+            build_index(self.cfg, self.K, omega, t, self.summaries)
+
+    def _cfg_at(self, t):
+        c, w = schedule_sqrt(t)
+        return dataclasses.replace(self.cfg, seg_len=c, window=w)
 
     def append(self, k_new, v_new):
         append(self.cfg, self.K, self.V, k_new, v_new, self.omega, self.t,
                self.summaries)
         self.t += 1
+        if self.schedule == "sqrt":
+            c_old = self.cfg.seg_len
+            self.cfg = self._cfg_at(self.t)
+            if self.cfg.seg_len != c_old:          # t is a perfect square
+                build_index(self.cfg, self.K, self.omega, self.t,
+                            self.summaries)
+                self.restructures += 1
 
     def decode(self, q, out=None, selected=None, scores=None):
+        # the scratch size follows the window, which grows between
+        # restructures under the sqrt schedule
+        if workspace_bytes(self.cfg, self.k) > self.workspace.numel():
+            self.workspace = new_workspace(self.cfg, self.k, self.K.device)
         return decode(self.cfg, q, self.K, self.V, self.omega, self.summaries,
                       self.t, self.k, out=out, selected=selected, scores=scores,
                       workspace=self.workspace)

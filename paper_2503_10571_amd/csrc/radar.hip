@@ -1765,6 +1765,17 @@ extern "C" {
 
 int32_t radar_abi_version(void) { return RADAR_ABI_VERSION; }
 
+radar_status radar_schedule_sqrt(int64_t t, int32_t* seg_len, int32_t* window) {
+  if (!seg_len || !window) return RADAR_EINVAL;
+  if (t < 1 || t > ((int64_t)1 << 31)) return RADAR_ECAPACITY;
+  int64_t c = (int64_t)std::sqrt((double)t);
+  while (c * c > t) --c;
+  while ((c + 1) * (c + 1) <= t) ++c;
+  *seg_len = (int32_t)c;
+  *window = (int32_t)(t - c * c);
+  return RADAR_OK;
+}
+
 radar_status radar_set_decode_path(int32_t path) {
   if (path != RADAR_PATH_AUTO && path != RADAR_PATH_SPLIT && path != RADAR_PATH_FUSED)
     return RADAR_EINVAL;

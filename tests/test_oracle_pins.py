@@ -358,3 +358,48 @@ def test_selection_finds_planted_segment():
     summ = orc.segment_summaries(K, om, c)
     sc = orc.segment_scores(orc.random_features(K[45], om), summ)
     assert orc.top_segments(sc, 1)[0] == 45 // c
+
+
+# --------------------------------------------------------------------------
+# Algorithm 1's restructuring schedule
+# --------------------------------------------------------------------------
+def test_sqrt_schedule_matches_algorithm1_state_machine():
+    # Run Algorithm 1's bookkeeping literally (1-based tokens): t <- t + 1;
+    # if sqrt(t) is an integer, c <- sqrt(t) and the buffer W is emptied,
+    # otherwise token t joins W. The schedule must reproduce c, the
+    # candidate segments (c segments of c tokens) and W at every t.
+    c, W = 0, []
+    for t in range(1, 3000):
+        r = math.isqrt(t)
+        if r * r == t:
+            c, W = r, []
+        else:
+            W.append(t)
+        cs, w = orc.sqrt_schedule(t)
+        ws, n_cand = orc.window_split(t, cs, w)
+        assert cs == c and n_cand == c and ws == c * c
+        # W holds the 1-based tokens c^2 + 1 .. t, i.e. 0-based [c^2, t)
+        assert list(range(ws, t)) == [j - 1 for j in W]
+        # the buffer never exceeds 2 sqrt(t) - 1 tokens (Section 2.2)
+        assert len(W) <= 2 * math.sqrt(t) - 1
+
+
+def test_sqrt_schedule_decode_is_algorithm1_query():
+    # At a restructure step the query attends only the selected segments;
+    # with every segment selected that is full attention over [0, t).
+    rng = np.random.default_rng(31)
+    d, n, t = 8, 32, 49
+    c, w = orc.sqrt_schedule(t)
+    assert (c, w) == (7, 0)
+    q = rng.standard_normal((1, 1, d))
+    K = rng.standard_normal((1, 1, t, d))
+    V = rng.standard_normal((1, 1, t, d))
+    om = rng.standard_normal((n, d))
+    summ = orc.segment_summaries(K[0, 0], om, c)[None, None]
+    res = orc.decode(q, K, V, om, summ, t, c, c, w)
+    np.testing.assert_allclose(res["out"][0, 0], _sdpa(q[0, 0], K[0, 0], V[0, 0]),
+                               rtol=1e-12, atol=1e-13)
+    # with k = 2 the attended set is exactly two segments (W is empty)
+    res = orc.decode(q, K, V, om, summ, t, 2, c, w)
+    toks = orc.attended_tokens(res["selected"][0, 0], c, c * c, t)
+    assert len(toks) == 2 * c
