@@ -54,9 +54,11 @@ class Stepper:
     """Direct C-ABI calls with pre-marshalled arguments (the per-step host
     cost stays small next to the GPU time)."""
 
-    def __init__(self, cfg, inp, K, V, summ, ws, out, k, sqrt_schedule=False):
+    def __init__(self, cfg, inp, K, V, summ, ws, out, k, sqrt_schedule=False,
+                 exact=False):
         self.L = radar.lib()
         self.sqrt = sqrt_schedule
+        self.exact = exact
         self.restructures = 0
         self.cfg_c = cfg.c_struct()
         self.cfgp = ctypes.byref(self.cfg_c)
@@ -92,9 +94,15 @@ class Stepper:
                     raise radar.RadarError("radar_build_index", st)
                 self.restructures += 1
             self.cfg_c.window = t + 1 - c * c
-        st = self.L.radar_decode(self.cfgp, self.q[i], self.K, self.V, self.om,
-                                 self.summ, t + 1, self.k, self.out, sel, None,
-                                 self.ws, self.ws_n, self.stream)
+        if self.exact:
+            st = self.L.radar_decode_exact(self.cfgp, self.q[i], self.K, self.V,
+                                           t + 1, self.k, self.out, sel, None,
+                                           self.ws, self.ws_n, self.stream)
+        else:
+            st = self.L.radar_decode(self.cfgp, self.q[i], self.K, self.V,
+                                     self.om, self.summ, t + 1, self.k,
+                                     self.out, sel, None, self.ws, self.ws_n,
+                                     self.stream)
         if st:
             raise radar.RadarError("radar_decode", st)
 
@@ -110,10 +118,12 @@ def union_sizes(sel, G):
     return out
 
 
-def step_bytes(wl, t, U, s_kv, sqrt_schedule=False):
+def step_bytes(wl, t, U, s_kv, sqrt_schedule=False, exact=False):
     """Algorithmic HBM bytes of one step whose decode runs at length t (the
     append wrote row t - 1). U: union size per (b, kv head).
-    Returns (whole step, decode call, K/V gather)."""
+    Returns (whole step, decode call, K/V gather, candidate-key scan); with
+    exact=True the selection scans every candidate key instead of reading
+    phi(q)'s inputs and the summaries."""
     d, n = wl.head_dim, wl.n_features
     if sqrt_schedule:
         c, w = radar.schedule_sqrt(t)
@@ -130,8 +140,9 @@ def step_bytes(wl, t, U, s_kv, sqrt_schedule=False):
     close = BH * (c * d * s_kv + n * 4) if t % c == 0 else 0
     if sqrt_schedule and w == 0:       # restructure: all t keys re-summarised
         close += BH * (t * d * s_kv + (t // c) * n * 4)
-    decode = summ + kv + qo + om
-    return decode + app + close, decode, kv
+    scan = BH * n_cand * c * d * s_kv
+    decode = (scan if exact else summ + om) + kv + qo
+    return decode + app + close, decode, kv, scan
 
 
 def measured_traffic(kernel, workload):
@@ -235,6 +246,27 @@ def cpu_baseline(wl, inp, first_step, n_steps, n_heads, min_s=10.0,
                        "before the sample is untimed")}
 
 
+def recall_sweep(wl):
+    """Recall of Radar's selection against the exact segment search at the
+    workload's context length, for n in 64..512 and k in 1..64, over the
+    first decode query of the workload's inputs."""
+    from paper_2503_10571_amd import recall
+    log(f"[recall] generating {wl.name} inputs")
+    inp = workloads.make_inputs(wl, "cuda", steps=1)
+    cfg = radar.Config(wl.batch, wl.n_q_heads, wl.n_kv_heads, wl.head_dim,
+                       wl.n_features, wl.seg_len, wl.window, wl.t0 + 1,
+                       wl.torch_dtype())
+    omegas = {n: workloads.make_omega(n, wl.head_dim, seed=1000 + n,
+                                      dtype=wl.dtype, device="cuda")
+              for n in (64, 128, 256, 512)}
+    ks = [1, 2, 4, 8, 16, 32, 64]
+    rows = recall.sweep(cfg, inp.q[0].contiguous(), inp.K, inp.V, wl.t0,
+                        omegas, ks)
+    for r in rows:
+        r["workload"] = wl.name
+        print(json.dumps(r), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -251,6 +283,13 @@ def main():
     ap.add_argument("--build-reps", type=int, default=3)
     ap.add_argument("--path", default="auto", choices=["auto", "split", "fused"],
                     help="decode path (auto: the library's choice)")
+    ap.add_argument("--selector", default="radar", choices=["radar", "exact"],
+                    help="radar: Eq. 6 scores (the method); exact: the exact "
+                         "segment search, every candidate key scanned")
+    ap.add_argument("--recall", action="store_true",
+                    help="instead of timing: recall of Radar's selection "
+                         "against the exact search over n and k, one JSON "
+                         "line per (n, k)")
     ap.add_argument("--schedule", default="fixed", choices=["fixed", "sqrt"],
                     help="fixed: the workload's segment length and window; "
                          "sqrt: Algorithm 1's restructuring (c = sqrt(t) at "
@@ -267,6 +306,10 @@ def main():
     radar.set_decode_path({"auto": radar.PATH_AUTO, "split": radar.PATH_SPLIT,
                            "fused": radar.PATH_FUSED}[args.path])
     wl = workloads.WORKLOADS[args.workload]
+    if args.recall:
+        recall_sweep(wl)
+        return
+    exact = args.selector == "exact"
     W = args.warmup
     Ksteps = args.steps if args.steps is not None else wl.steps
     total = W + Ksteps
@@ -310,7 +353,7 @@ def main():
 
     # ---- decode steps ----------------------------------------------------
     stp = Stepper(cfg, inp, K, V, summ, ws, out, wl.top_k,
-                  sqrt_schedule=args.schedule == "sqrt")
+                  sqrt_schedule=args.schedule == "sqrt", exact=exact)
     sel_log = torch.empty(Ksteps, wl.batch, wl.n_q_heads, wl.top_k,
                           dtype=torch.int32, device=K.device)
     log(f"[bench] warmup {W} steps")
@@ -346,22 +389,27 @@ def main():
 
     # ---- algorithmic bytes ------------------------------------------------
     sel_np = sel_log.cpu().numpy()
-    tot_bytes, dec_bytes, kv_bytes = 0, 0, 0
+    tot_bytes, dec_bytes, kv_bytes, scan_bytes = 0, 0, 0, 0
     for j in range(Ksteps):
         t = wl.t0 + W + j + 1
         U = union_sizes(sel_np[j], wl.group)
-        b_all, b_dec, b_kv = step_bytes(wl, t, U, s_kv,
-                                        sqrt_schedule=args.schedule == "sqrt")
+        b_all, b_dec, b_kv, b_scan = step_bytes(
+            wl, t, U, s_kv, sqrt_schedule=args.schedule == "sqrt", exact=exact)
         tot_bytes += b_all
         dec_bytes += b_dec
         kv_bytes += b_kv
+        scan_bytes += b_scan
     step_gbps = tot_bytes / (ms * 1e-3) / 1e9
     path = radar.decode_path(dataclasses.replace(cfg, seg_len=seg_timed,
                                                  window=win_timed),
                              wl.t0 + W + 1, wl.top_k)
     # dominant kernel: the fused decode (all decode bytes), or the split
     # path's gather-attention kernel (the K/V bytes)
-    if path == radar.PATH_FUSED:
+    if exact:
+        # the exact selector runs the split path; its key scan dominates
+        path = radar.PATH_SPLIT
+        dom, dom_name, dom_bytes = "score", "k_segment_mass", scan_bytes
+    elif path == radar.PATH_FUSED:
         dom, dom_name, dom_bytes = "fused", "k_decode_fused", dec_bytes
     else:
         dom, dom_name, dom_bytes = "attend", "k_attend", kv_bytes
@@ -375,7 +423,7 @@ def main():
     log("[bench] kernels: " + json.dumps(kern))
 
     cpu = None
-    if args.cpu_baseline:
+    if args.cpu_baseline and not exact:
         log("[bench] cpu baseline (fp64 oracle)")
         cpu = cpu_baseline(wl, inp, W, Ksteps, n_heads=args.cpu_heads,
                            sqrt_schedule=args.schedule == "sqrt")
@@ -421,6 +469,7 @@ def main():
             "decode_path": {radar.PATH_SPLIT: "split",
                             radar.PATH_FUSED: "fused"}.get(path, "?"),
             "schedule": args.schedule,
+            "selector": args.selector,
             "restructures": restructures,
         },
         "hbm_GBps": round(step_gbps, 1),

@@ -83,12 +83,12 @@ typedef enum { RADAR_F32 = 0, RADAR_BF16 = 1 } radar_dtype;
 typedef struct {
   int32_t batch;       /* B >= 1                                            */
   int32_t n_q_heads;   /* Hq; Hq % Hkv == 0, G = Hq / Hkv in {1, 2, 4, 8}   */
-  int32_t n_kv_heads;  /* Hkv >= 1                                          */
+  int32_t n_kv_heads;  /* Hkv >= 1; B * Hkv <= 65535                        */
   int32_t head_dim;    /* d in {64, 128}                                    */
   int32_t n_features;  /* n in {64, 128, 256, 512}                          */
   int32_t seg_len;     /* c >= 1 (any value; need not divide anything)      */
   int32_t window;      /* w >= 0                                            */
-  int64_t capacity;    /* token rows per head in K and V (>= 1)             */
+  int64_t capacity;    /* token rows per head in K and V, 1 .. 2^31 - 1     */
   radar_dtype kv_dtype;
 } radar_config;
 
@@ -126,8 +126,22 @@ radar_status radar_decode(const radar_config* cfg, const void* q,
                           void* workspace, size_t workspace_bytes,
                           hipStream_t stream);
 
-/* Scratch bytes radar_decode and radar_attend_selected need for this shape
- * and k (0 if cfg is invalid). */
+/* Exact segment search (the exact-selection ablation of Section 3.3): like
+ * radar_decode, but each query head selects the k candidate segments with
+ * the largest exact attention mass beta_s = sum over the segment's keys of
+ * exp(q . k / sqrt(d)) (the quantity Theorem 2's proof calls beta) instead
+ * of the random-feature estimate. It reads every candidate key, O(t) bytes
+ * per query: a reference selector for recall measurements, not the fast
+ * path. `scores` (nullable) receives ln(beta) of the selected segments.
+ * Workspace as for radar_decode; summaries and Omega are not used. */
+radar_status radar_decode_exact(const radar_config* cfg, const void* q,
+                                const void* K, const void* V, int64_t t,
+                                int32_t k, void* out, int32_t* selected,
+                                float* scores, void* workspace,
+                                size_t workspace_bytes, hipStream_t stream);
+
+/* Scratch bytes radar_decode, radar_decode_exact and radar_attend_selected
+ * need for this shape and k (0 if cfg is invalid). */
 size_t radar_decode_workspace_bytes(const radar_config* cfg, int32_t k);
 
 /* Exact attention over caller-chosen segments (the last step of Algorithm 1
@@ -182,7 +196,7 @@ typedef enum {
   RADAR_K_APPEND = 0,   /* k/v row write                                   */
   RADAR_K_BUILD = 1,    /* segment summaries (build or segment close)      */
   RADAR_K_PHI_Q = 2,    /* phi(q)                                          */
-  RADAR_K_SCORE = 3,    /* Eq. 6 segment scores                            */
+  RADAR_K_SCORE = 3,    /* Eq. 6 segment scores (exact mass: its kernel)   */
   RADAR_K_TOPK = 4,     /* top-k and per-kv-head union (or given union)    */
   RADAR_K_ATTEND = 5,   /* gather-attention partials                       */
   RADAR_K_COMBINE = 6,  /* merge of the partials                           */

@@ -30,7 +30,7 @@ import numpy as np
 __all__ = [
     "random_features", "segment_summaries", "window_split", "segment_scores",
     "top_segments", "attended_tokens", "attend", "decode_head", "decode",
-    "full_attention", "sqrt_schedule",
+    "full_attention", "sqrt_schedule", "exact_segment_mass", "decode_exact",
 ]
 
 
@@ -202,3 +202,56 @@ def sqrt_schedule(t):
     while (c + 1) * (c + 1) <= t:
         c += 1
     return c, t - c * c
+
+
+def exact_segment_mass(q, keys, c, n_cand):
+    """Exact segment attention mass (the quantity Theorem 2's proof calls
+    beta): beta_s = sum over the c keys of segment s of exp(q . k / sqrt(d)),
+    the unnormalised attention weight the segment carries. Selecting the k
+    largest is the exact segment search of the ablation study (Section 3.3).
+    Returns ln(beta_s) for s < n_cand (the log keeps large logits finite;
+    each segment subtracts its own max logit before exponentiating)."""
+    q = _f64(q)
+    keys = _f64(keys)
+    d = q.shape[-1]
+    out = np.empty(n_cand)
+    for s in range(n_cand):
+        lg = keys[s * c:(s + 1) * c] @ q / np.sqrt(d)
+        m = lg.max()
+        out[s] = m + np.log(np.exp(lg - m).sum())
+    return out
+
+
+def decode_exact(q, K, V, t, k, c, w):
+    """decode() with the exact segment search in place of the random-feature
+    scores: every query head selects the k segments with the largest
+    beta_s; the union over the heads sharing a kv head plus the window is
+    attended exactly. Returns the same dict as decode() with `scores` and
+    `sel_scores` holding ln(beta)."""
+    q = _f64(q)
+    B, Hq, d = q.shape
+    Hkv = K.shape[1]
+    G = Hq // Hkv
+    ws, n_cand = window_split(t, c, w)
+    k_eff = min(k, n_cand)
+    out = np.zeros((B, Hq, d))
+    selected = -np.ones((B, Hq, k), dtype=np.int64)
+    sel_scores = np.full((B, Hq, k), np.nan)
+    scores, union = {}, {}
+    for b in range(B):
+        for g in range(Hkv):
+            heads = range(g * G, (g + 1) * G)
+            picks = []
+            for h in heads:
+                sc = exact_segment_mass(q[b, h], K[b, g], c, n_cand)
+                sel = top_segments(sc, k)
+                scores[(b, h)] = sc
+                selected[b, h, :k_eff] = sel
+                sel_scores[b, h, :k_eff] = sc[sel]
+                picks.extend(sel.tolist())
+            union[(b, g)] = sorted(set(picks))
+            toks = attended_tokens(union[(b, g)], c, ws, t)
+            for h in heads:
+                out[b, h] = attend(q[b, h], K[b, g], V[b, g], toks)
+    return dict(out=out, selected=selected, sel_scores=sel_scores,
+                scores=scores, union=union, ws=ws, n_cand=n_cand, k_eff=k_eff)

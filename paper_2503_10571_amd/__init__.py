@@ -83,6 +83,8 @@ def lib() -> ctypes.CDLL:
         L.radar_append.argtypes = [cfgp, _P, _P, _P, _P, _P, i64, _P, _P]
         L.radar_decode.argtypes = [cfgp, _P, _P, _P, _P, _P, i64, i32, _P, _P,
                                    _P, _P, sz, _P]
+        L.radar_decode_exact.argtypes = [cfgp, _P, _P, _P, i64, i32, _P, _P, _P,
+                                         _P, sz, _P]
         L.radar_decode_workspace_bytes.argtypes = [cfgp, i32]
         L.radar_decode_workspace_bytes.restype = sz
         L.radar_attend_selected.argtypes = [cfgp, _P, _P, _P, _P, i32, i64, _P,
@@ -102,8 +104,8 @@ def lib() -> ctypes.CDLL:
         L.radar_profile_read.argtypes = [ctypes.POINTER(ctypes.c_double),
                                          ctypes.POINTER(ctypes.c_int64), i32]
         for fn in ("radar_build_index", "radar_append", "radar_decode",
-                   "radar_attend_selected", "radar_profile_enable",
-                   "radar_profile_read"):
+                   "radar_decode_exact", "radar_attend_selected",
+                   "radar_profile_enable", "radar_profile_read"):
             getattr(L, fn).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -186,6 +188,27 @@ def decode(cfg: Config, q, K, V, omega, summaries, t: int, k: int, out=None,
         ctypes.byref(cfg.c_struct()), _ptr(q), _ptr(K), _ptr(V), _ptr(omega),
         _ptr(summaries), t, k, _ptr(out), _ptr(selected), _ptr(scores),
         _ptr(workspace), workspace.numel(), _stream(q)))
+    return out
+
+
+def decode_exact(cfg: Config, q, K, V, t: int, k: int, out=None,
+                 selected=None, scores=None, workspace=None):
+    """radar_decode_exact: top-k segments by exact attention mass, then the
+    same attention as decode(). scores receives ln(beta) of the picks."""
+    for x, nm in ((q, "q"), (K, "K"), (V, "V")):
+        _need(x, cfg.dtype, nm)
+    if out is None:
+        out = torch.empty_like(q)
+    if workspace is None:
+        workspace = new_workspace(cfg, k, q.device)
+    if selected is not None:
+        _need(selected, torch.int32, "selected")
+    if scores is not None:
+        _need(scores, torch.float32, "scores")
+    _check("radar_decode_exact", lib().radar_decode_exact(
+        ctypes.byref(cfg.c_struct()), _ptr(q), _ptr(K), _ptr(V), t, k, _ptr(out),
+        _ptr(selected), _ptr(scores), _ptr(workspace), workspace.numel(),
+        _stream(q)))
     return out
 
 

@@ -864,6 +864,85 @@ __global__ __launch_bounds__(256) void k_topk_union(
 }
 
 // ---------------------------------------------------------------------------
+// k_segment_mass: exact segment attention mass, ln(beta_s) per query head
+// ---------------------------------------------------------------------------
+// beta_s = sum over the keys of segment s of exp(q . k / sqrt(d)) (the
+// segment's unnormalised attention weight; selecting its top-k is the exact
+// segment search). One wave per candidate segment: the logits of each
+// <= 64-token tile come from the same row-contiguous loads and
+// transpose-reduce as the attention tiles, and an online log-sum-exp in
+// base 2 carries across the segment's tiles. Writes ln(beta_s) to
+// scores[b][h][s].
+template <typename T, int D, int G>
+__global__ __launch_bounds__(256) void k_segment_mass(
+    const T* __restrict__ q, const T* __restrict__ K, float* __restrict__ scores,
+    int Hq, int Hkv, int64_t cap, int c, int n_cand, int nc_cap, float qscale) {
+  constexpr int EPL = Elem<T>::kPer16;
+  constexpr int LPR = D / EPL;
+  constexpr int RPI = kWave / LPR;
+  constexpr int ITER = kTile / RPI;
+  constexpr float kLn2 = 0.69314718055994530942f;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int64_t bh = blockIdx.y;
+  const int64_t b = bh / Hkv, hk = bh % Hkv;
+  const int s = blockIdx.x * 4 + wave;
+  if (s >= n_cand) return;                 // wave-uniform; no barriers below
+  const int r = lane / LPR, jj = lane % LPR;
+
+  float qf[G][EPL];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    const uint4 u = *reinterpret_cast<const uint4*>(
+        q + ((b * Hq + hk * G + g) * D + jj * EPL));
+    unpack16<T>(u, qf[g]);
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) qf[g][e] *= qscale;
+  }
+  float m[G], l[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) { m[g] = -INFINITY; l[g] = 0.f; }
+
+  for (int off = 0; off < c; off += kTile) {
+    const int len = min(kTile, c - off);
+    const T* kbase = K + (bh * cap + (int64_t)s * c + off) * D + jj * EPL;
+    uint4 kr[ITER];
+#pragma unroll
+    for (int i = 0; i < ITER; ++i)
+      kr[i] = ld_stream(kbase + (int64_t)min(i * RPI + r, len - 1) * D);
+    float pl[G][ITER];
+#pragma unroll
+    for (int i = 0; i < ITER; ++i) {
+      float kf[EPL];
+      unpack16<T>(kr[i], kf);
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        float a = 0.f;
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) a = fmaf(qf[g][e], kf[e], a);
+        pl[g][i] = a;
+      }
+    }
+    const bool mine_ok = (jj * RPI + r) < len;
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      transpose_reduce<LPR>(pl[g], lane);
+      const float lg = pl[g][0];
+      const float mt = wave_max(mine_ok ? lg : -INFINITY);
+      const float mn = fmaxf(m[g], mt);
+      const float p = mine_ok ? fast_exp2(lg - mn) : 0.f;
+      l[g] = fmaf(l[g], fast_exp2(m[g] - mn), wave_sum(p));
+      m[g] = mn;
+    }
+  }
+  if (lane == 0) {
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+      scores[(b * Hq + hk * G + g) * (int64_t)nc_cap + s] = (m[g] + __log2f(l[g])) * kLn2;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // k_union_given: union of caller-given selections (attention on a supplied
 // selection, the last step of Algorithm 1 alone)
 // ---------------------------------------------------------------------------
@@ -1446,7 +1525,9 @@ radar_status check_cfg(const radar_config* cfg, Shape* s) {
   if (cfg->head_dim != 64 && cfg->head_dim != 128) return RADAR_EUNSUPPORTED;
   const int n = cfg->n_features;
   if (n != 64 && n != 128 && n != 256 && n != 512) return RADAR_EUNSUPPORTED;
-  if (cfg->capacity > (int64_t)1 << 31) return RADAR_EUNSUPPORTED;
+  // row counts fit int32; (b, kv head) pairs fit a grid's y dimension
+  if (cfg->capacity > INT32_MAX) return RADAR_EUNSUPPORTED;
+  if ((int64_t)cfg->batch * cfg->n_kv_heads > 65535) return RADAR_EUNSUPPORTED;
   s->B = cfg->batch; s->Hq = cfg->n_q_heads; s->Hkv = cfg->n_kv_heads; s->G = G;
   s->d = cfg->head_dim; s->n = n; s->c = cfg->seg_len; s->w = cfg->window;
   s->cap = cfg->capacity; s->s_cap = cfg->capacity / cfg->seg_len;
@@ -1658,6 +1739,23 @@ radar_status launch_attend(const Shape& s, const void* q, const void* K,
     else launch_attend_d<float, 128>(s, q, K, V, w, L, ag.grid_x, ag.tpw, ws, t, out, st);
   }
   return launch_status();
+}
+
+// ---- exact segment search ---------------------------------------------------
+template <typename T, int D>
+void launch_segment_mass_d(const Shape& s, const void* q, const void* K, float* scores,
+                           int n_cand, hipStream_t st) {
+  const dim3 grid((unsigned)ceil_div(n_cand, 4), (unsigned)(s.B * s.Hkv));
+  const int nc_cap = (int)std::max<int64_t>(1, s.s_cap);
+  const float qscale = kLog2e / std::sqrt((float)s.d);
+  const T* qt = reinterpret_cast<const T*>(q);
+  const T* Kt = reinterpret_cast<const T*>(K);
+  switch (s.G) {
+    case 1: launch(RADAR_K_SCORE, k_segment_mass<T, D, 1>, grid, dim3(256), 0, st, qt, Kt, scores, s.Hq, s.Hkv, s.cap, s.c, n_cand, nc_cap, qscale); break;
+    case 2: launch(RADAR_K_SCORE, k_segment_mass<T, D, 2>, grid, dim3(256), 0, st, qt, Kt, scores, s.Hq, s.Hkv, s.cap, s.c, n_cand, nc_cap, qscale); break;
+    case 4: launch(RADAR_K_SCORE, k_segment_mass<T, D, 4>, grid, dim3(256), 0, st, qt, Kt, scores, s.Hq, s.Hkv, s.cap, s.c, n_cand, nc_cap, qscale); break;
+    default: launch(RADAR_K_SCORE, k_segment_mass<T, D, 8>, grid, dim3(256), 0, st, qt, Kt, scores, s.Hq, s.Hkv, s.cap, s.c, n_cand, nc_cap, qscale); break;
+  }
 }
 
 // ---- fused path -------------------------------------------------------------
@@ -1936,6 +2034,52 @@ radar_status radar_decode(const radar_config* cfg, const void* q, const void* K,
       else launch_phi_q<float, 128>(s, q, omega, phiq, stream);
     }
     launch_score(s, phiq, summaries, sc, n_cand, stream);
+  }
+  launch(RADAR_K_TOPK, k_topk_union, dim3((unsigned)(s.B * s.Hkv)), dim3(256), 0, stream,
+         sc, s.Hq, s.Hkv, s.G, n_cand, (int)std::max<int64_t>(1, s.s_cap), k, k_eff,
+         reinterpret_cast<int*>(w + L.uni), reinterpret_cast<int*>(w + L.ucnt), L.umax,
+         selected, scores);
+  r = launch_status();
+  if (r != RADAR_OK) return r;
+  return launch_attend(s, q, K, V, ag, ws, t, out, w, L, stream);
+}
+
+radar_status radar_decode_exact(const radar_config* cfg, const void* q,
+                                const void* K, const void* V, int64_t t,
+                                int32_t k, void* out, int32_t* selected,
+                                float* scores, void* workspace,
+                                size_t workspace_bytes, hipStream_t stream) {
+  Shape s;
+  radar_status r = check_cfg(cfg, &s);
+  if (r != RADAR_OK) return r;
+  if (!q || !K || !V || !out) return RADAR_EINVAL;
+  if (!aligned16(q) || !aligned16(K) || !aligned16(V) || !aligned16(out) ||
+      (selected && !aligned16(selected)) || (scores && !aligned16(scores)))
+    return RADAR_EINVAL;
+  if (k < 1 || k > kMaxK) return RADAR_EUNSUPPORTED;
+  if (t < 1 || t > s.cap) return RADAR_ECAPACITY;
+  const WsLayout L = ws_layout(s, k);
+  if (!workspace || !aligned16(workspace)) return RADAR_EWORKSPACE;
+  if (workspace_bytes < L.total) return RADAR_EWORKSPACE;
+  int64_t ws;
+  int n_cand;
+  window_split(s, t, &ws, &n_cand);
+  if (n_cand > kMaxCand) return RADAR_EUNSUPPORTED;
+  const int k_eff = std::min(k, n_cand);
+  const int u_bound = std::min(s.G * k_eff, n_cand);
+  const AttendGrid ag = attend_grid(s, L, u_bound, ws, t);
+  if (ag.grid_x > kMaxWg) return RADAR_EUNSUPPORTED;
+
+  unsigned char* w = reinterpret_cast<unsigned char*>(workspace);
+  float* sc = reinterpret_cast<float*>(w + L.scores);
+  if (n_cand > 0) {
+    if (s.dt == RADAR_BF16) {
+      if (s.d == 64) launch_segment_mass_d<bf16_t, 64>(s, q, K, sc, n_cand, stream);
+      else launch_segment_mass_d<bf16_t, 128>(s, q, K, sc, n_cand, stream);
+    } else {
+      if (s.d == 64) launch_segment_mass_d<float, 64>(s, q, K, sc, n_cand, stream);
+      else launch_segment_mass_d<float, 128>(s, q, K, sc, n_cand, stream);
+    }
   }
   launch(RADAR_K_TOPK, k_topk_union, dim3((unsigned)(s.B * s.Hkv)), dim3(256), 0, stream,
          sc, s.Hq, s.Hkv, s.G, n_cand, (int)std::max<int64_t>(1, s.s_cap), k, k_eff,

@@ -1,0 +1,138 @@
+"""Recall diagnostics: Radar's segment selection against the exact search.
+
+Radar ranks segments by the random-feature estimate of Eq. 6; the exact
+segment search (the selector of the ablation in Section 3.3) ranks them by
+beta_s, the summed unnormalised attention weights of the segment's keys.
+Theorem 2 bounds when the estimate recovers the top segment; these helpers
+measure how much of the exact selection, and of the attention mass, Radar
+keeps as n and k vary (the quantities behind the n / k study of Section 3.3,
+here on any keys the caller supplies):
+
+  set_recall   |S_radar ∩ S_exact| / |S_exact| per query head;
+  mass_ratio   attention mass of Radar's segments over that of the exact
+               top-k (<= 1: the exact top-k maximises the mass);
+  captured_mass  share of the full softmax kept by the selected segments
+               plus the window;
+  sweep        both, plus each selector's output error against full
+               attention, over a grid of (n, k).
+
+Selections, outputs and full attention come from the library's own decode
+calls; the per-segment attention mass is a plain fp32 softmax over the
+context in torch (a diagnostic, not part of the decode path).
+"""
+from __future__ import annotations
+
+import dataclasses
+
+import torch
+
+from . import Config, build_index, decode, decode_exact, new_summaries
+
+
+def set_recall(sel: torch.Tensor, ref: torch.Tensor) -> torch.Tensor:
+    """sel, ref: [B][Hq][k] segment ids, -1 padded. Fraction of ref's ids
+    that sel also holds, per (b, q head); 1 where ref is empty."""
+    hit = (sel.unsqueeze(-1) == ref.unsqueeze(-2)) & (sel.unsqueeze(-1) >= 0)
+    found = hit.any(dim=-2).sum(-1).float()
+    size = (ref >= 0).sum(-1).float()
+    return torch.where(size > 0, found / size.clamp(min=1), torch.ones_like(size))
+
+
+def segment_mass(q: torch.Tensor, K: torch.Tensor, t: int, c: int,
+                 n_cand: int) -> torch.Tensor:
+    """Softmax attention mass of each candidate segment, [B][Hq][n_cand]
+    fp32: sum over the segment's keys of softmax(q . k / sqrt(d)) taken over
+    all t tokens. q [B][Hq][d], K [B][Hkv][cap][d]."""
+    B, Hq, d = q.shape
+    Hkv = K.shape[1]
+    G = Hq // Hkv
+    out = torch.empty(B, Hq, n_cand, dtype=torch.float32, device=q.device)
+    for b in range(B):
+        kf = K[b, :, :t].float()                                  # [Hkv, t, d]
+        qf = q[b].float().view(Hkv, G, d).transpose(1, 2).contiguous()
+        p = torch.softmax(torch.matmul(kf, qf) / d ** 0.5, dim=1)  # [Hkv, t, G]
+        seg = p[:, :n_cand * c].reshape(Hkv, n_cand, c, G).sum(2)
+        out[b] = seg.permute(0, 2, 1).reshape(Hq, n_cand)
+    return out
+
+
+def mass_ratio(sel: torch.Tensor, ref: torch.Tensor,
+               mass: torch.Tensor) -> torch.Tensor:
+    """Attention mass of sel's segments over that of ref's, per (b, q head);
+    1 where ref selects nothing."""
+    def total(s):
+        m = torch.gather(mass, 2, s.clamp(min=0).long())
+        return torch.where(s >= 0, m, torch.zeros_like(m)).sum(-1)
+    den = total(ref)
+    return torch.where(den > 0, total(sel) / den.clamp(min=1e-30),
+                       torch.ones_like(den))
+
+
+def captured_mass(sel: torch.Tensor, mass: torch.Tensor) -> torch.Tensor:
+    """Share of the full softmax that attention over sel's segments plus the
+    window keeps, per (b, q head): the selected segments' mass plus the
+    mass outside every candidate segment (the window). The output error of
+    attention restricted to these tokens is at most 2 (1 - captured) max|v|."""
+    m = torch.gather(mass, 2, sel.clamp(min=0).long())
+    picked = torch.where(sel >= 0, m, torch.zeros_like(m)).sum(-1)
+    return picked + (1.0 - mass.sum(-1)).clamp(min=0)
+
+
+def _rel_err(x: torch.Tensor, ref: torch.Tensor) -> torch.Tensor:
+    """max_i |x_i - ref_i| / max_i |ref_i| per (b, q head)."""
+    x, ref = x.float(), ref.float()
+    return (x - ref).abs().amax(-1) / ref.abs().amax(-1).clamp(min=1e-30)
+
+
+def sweep(cfg: Config, q: torch.Tensor, K: torch.Tensor, V: torch.Tensor,
+          t: int, omegas: dict, ks) -> list:
+    """Radar vs exact segment search at context length t for every n in
+    omegas (n -> Omega [n][d] fp32) and every k in ks. Returns one dict per
+    (n, k) with the mean / minimum set recall and mass ratio over the query
+    heads and the mean output error of both selectors against full
+    attention."""
+    c, w = cfg.seg_len, cfg.window
+    ws = c * (max(0, t - w) // c)
+    n_cand = ws // c
+    mass = segment_mass(q, K, t, c, n_cand) if n_cand else None
+    # full attention: a window that covers the whole context (no candidate
+    # segment, so the summaries and Omega are not read)
+    n0, om0 = next(iter(omegas.items()))
+    full_cfg = dataclasses.replace(cfg, window=cfg.capacity, n_features=n0)
+    full = decode(full_cfg, q, K, V, om0, new_summaries(full_cfg, q.device),
+                  t, 1)
+    rows = []
+    B, Hq = q.shape[0], q.shape[1]
+
+    def ids(k):
+        return torch.empty(B, Hq, k, dtype=torch.int32, device=q.device)
+    exact = {}
+    for k in ks:
+        se = ids(k)
+        out_e = decode_exact(cfg, q, K, V, t, k, selected=se)
+        exact[k] = (se, _rel_err(out_e, full))
+    for n, omega in omegas.items():
+        ncfg = dataclasses.replace(cfg, n_features=n)
+        summ = new_summaries(ncfg, q.device)
+        build_index(ncfg, K, omega, t, summ)
+        for k in ks:
+            sr = ids(k)
+            out_r = decode(ncfg, q, K, V, omega, summ, t, k, selected=sr)
+            se, err_e = exact[k]
+            rec = set_recall(sr, se)
+            one = torch.ones_like(rec)
+            mr = mass_ratio(sr, se, mass) if mass is not None else one
+            cr = captured_mass(sr, mass) if mass is not None else one
+            ce = captured_mass(se, mass) if mass is not None else one
+            err_r = _rel_err(out_r, full)
+            rows.append({
+                "n": n, "k": k, "n_cand": n_cand,
+                "recall_mean": float(rec.mean()), "recall_min": float(rec.min()),
+                "mass_ratio_mean": float(mr.mean()),
+                "mass_ratio_min": float(mr.min()),
+                "captured_radar": float(cr.mean()),
+                "captured_exact": float(ce.mean()),
+                "out_err_radar": float(err_r.mean()),
+                "out_err_exact": float(err_e.mean()),
+            })
+    return rows

@@ -44,8 +44,10 @@ def f64(x: torch.Tensor) -> np.ndarray:
     return x.detach().float().cpu().double().numpy()
 
 
-def check_selection(gpu_sel, ora_scores, k_eff, n_cand):
-    """Tie-band set check for one query head. gpu_sel: the k ids (-1 pad)."""
+def check_selection(gpu_sel, ora_scores, k_eff, n_cand, band_abs=None):
+    """Tie-band set check for one query head. gpu_sel: the k ids (-1 pad).
+    The band around the oracle's k-th score is relative (TIE_BAND) unless
+    band_abs gives an absolute half-width (for log-scale scores)."""
     sel = [int(s) for s in gpu_sel if s >= 0]
     assert len(sel) == k_eff, (sel, k_eff)
     assert len(set(sel)) == k_eff, sel
@@ -55,7 +57,10 @@ def check_selection(gpu_sel, ora_scores, k_eff, n_cand):
         return 0
     order = orc.top_segments(ora_scores, k_eff)
     s_k = ora_scores[order[-1]]
-    hi, lo = s_k * (1 + TIE_BAND), s_k * (1 - TIE_BAND)
+    if band_abs is None:
+        hi, lo = s_k * (1 + TIE_BAND), s_k * (1 - TIE_BAND)
+    else:
+        hi, lo = s_k + band_abs, s_k - band_abs
     must = {int(s) for s in np.nonzero(ora_scores > hi)[0]}
     assert must <= set(sel), ("missed", sorted(must - set(sel)))
     bad = [s for s in sel if ora_scores[s] < lo]

@@ -113,9 +113,22 @@ def test_validation_before_launch(L):
         assert L.radar_build_index(by(bad.c_struct()), good, good, 1, good,
                                    None) == 1
     for bad in (_cfg(head_dim=256), _cfg(n_features=1024),
-                _cfg(n_q_heads=96, n_kv_heads=32)):
+                _cfg(n_q_heads=96, n_kv_heads=32), _cfg(capacity=1 << 31),
+                _cfg(batch=2048, n_q_heads=32, n_kv_heads=32)):
         assert L.radar_build_index(by(bad.c_struct()), good, good, 1, good,
                                    None) == 3
+    # decode_exact: same checks as decode
+    ex = [by(cfg), good, good, good]
+    assert L.radar_decode_exact(*ex, 1000, 0, good, None, None, good, ws,
+                                None) == 3
+    assert L.radar_decode_exact(*ex, 131585, 16, good, None, None, good, ws,
+                                None) == 2
+    assert L.radar_decode_exact(*ex, 1000, 16, null, None, None, good, ws,
+                                None) == 1
+    assert L.radar_decode_exact(*ex, 1000, 16, good, None, None, good, ws - 1,
+                                None) == 5
+    assert L.radar_decode_exact(by(big), good, good, good, 40000, 16, good,
+                                None, None, good, wsb, None) == 3
     # attend_selected
     assert L.radar_attend_selected(by(cfg), good, good, good, null, 4, 100,
                                    good, good, ws, None) == 1

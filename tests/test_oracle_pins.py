@@ -403,3 +403,68 @@ def test_sqrt_schedule_decode_is_algorithm1_query():
     res = orc.decode(q, K, V, om, summ, t, 2, c, w)
     toks = orc.attended_tokens(res["selected"][0, 0], c, c * c, t)
     assert len(toks) == 2 * c
+
+
+# --------------------------------------------------------------------------
+# exact segment search (segment attention mass beta)
+# --------------------------------------------------------------------------
+def test_exact_mass_one_token_segments_is_token_topk():
+    # c = 1: beta_s = exp(q . k_s / sqrt(d)), so the exact search is the
+    # token top-k of the problem statement (Eq. 3) by the logit itself.
+    rng = np.random.default_rng(41)
+    d, T, k = 16, 40, 7
+    q = rng.standard_normal(d)
+    K = rng.standard_normal((T, d)) * 2
+    lnb = orc.exact_segment_mass(q, K, 1, T)
+    np.testing.assert_allclose(lnb, K @ q / 4.0, rtol=1e-13, atol=1e-13)
+    assert orc.top_segments(lnb, k).tolist() == np.argsort(-(K @ q))[:k].tolist()
+
+
+def test_exact_mass_constant_segment_and_full_normaliser():
+    rng = np.random.default_rng(43)
+    d, c, ns = 9, 6, 5
+    q = rng.standard_normal(d) * 3
+    U = rng.standard_normal((ns, d)) * 3
+    K = np.repeat(U, c, axis=0)
+    # identical keys: beta_s = c exp(q . u_s / sqrt(d))
+    np.testing.assert_allclose(orc.exact_segment_mass(q, K, c, ns),
+                               np.log(c) + U @ q / 3.0, rtol=1e-13)
+    # the segments' masses add up to the softmax normaliser of the tokens
+    K = rng.standard_normal((c * ns, d)) * 3
+    lnz = torch.logsumexp(torch.as_tensor(K @ q / 3.0), 0).item()
+    lnb = orc.exact_segment_mass(q, K, c, ns)
+    assert abs(np.log(np.exp(lnb - lnb.max()).sum()) + lnb.max() - lnz) < 1e-12
+
+
+def test_radar_score_estimates_exact_mass():
+    # E_Omega[phi(q) . phi_bar(s)] = beta_s / c (Lemma 1 with Eq. 5-6): the
+    # random-feature score is an unbiased estimate of the exact mass.
+    rng = np.random.default_rng(47)
+    d, c, ns, n, M = 8, 4, 5, 64, 3000
+    K = rng.standard_normal((c * ns, d)) * 0.35
+    q = rng.standard_normal(d) * 0.35
+    beta = np.exp(orc.exact_segment_mass(q, K, c, ns))
+    est = np.zeros(ns)
+    sq = np.zeros(ns)
+    for om in rng.standard_normal((M, n, d)):
+        a = orc.segment_scores(orc.random_features(q, om),
+                               orc.segment_summaries(K, om, c))
+        est += a
+        sq += a * a
+    mean = est / M
+    se = np.sqrt((sq / M - mean ** 2) / M)
+    assert (np.abs(mean - beta / c) <= 5 * se).all(), (mean, beta / c, se)
+
+
+def test_decode_exact_all_selected_is_full_attention():
+    rng = np.random.default_rng(53)
+    B, Hq, Hkv, d, t, c, w = 1, 4, 2, 8, 45, 4, 6
+    q = rng.standard_normal((B, Hq, d))
+    K = rng.standard_normal((B, Hkv, t, d))
+    V = rng.standard_normal((B, Hkv, t, d))
+    _, n_cand = orc.window_split(t, c, w)
+    res = orc.decode_exact(q, K, V, t, n_cand, c, w)
+    for h in range(Hq):
+        np.testing.assert_allclose(res["out"][0, h],
+                                   _sdpa(q[0, h], K[0, h // 2], V[0, h // 2]),
+                                   rtol=1e-12, atol=1e-13)
