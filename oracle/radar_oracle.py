@@ -57,32 +57,43 @@ def random_features(x, omega):
     return np.exp(proj - half_sq) / np.sqrt(n)
 
 
-def segment_summaries(keys, omega, c, n_seg=None, first=0):
+def segment_summaries(keys, omega, c, n_seg=None, first=0, offset=0):
     """Segment embeddings (Section 2.2, Eq. 5): the mean of phi over the c keys
-    of each segment. Segment s (0-based) holds tokens [s*c, s*c + c).
+    of each segment. Segment s (0-based) holds tokens [offset + s*c,
+    offset + s*c + c); offset is the number of sink tokens that precede the
+    segments (0 without sinks).
 
     keys: [T, d] of one head; returns [n_seg - first, n] for segments
-    first .. n_seg-1 (n_seg defaults to floor(T / c), the full segments).
+    first .. n_seg-1 (n_seg defaults to floor((T - offset) / c), the full
+    segments).
     """
     keys = _f64(keys)
     if n_seg is None:
-        n_seg = keys.shape[0] // c
+        n_seg = max(0, keys.shape[0] - offset) // c
     n = np.asarray(omega).shape[0]
     out = np.empty((n_seg - first, n))
     for s in range(first, n_seg):
-        out[s - first] = random_features(keys[s * c:(s + 1) * c], omega).mean(0)
+        lo = offset + s * c
+        out[s - first] = random_features(keys[lo:lo + c], omega).mean(0)
     return out
 
 
-def window_split(t, c, w):
+def window_split(t, c, w, n_sink=0):
     """Partition of the context [0, t) used at a decode step (Algorithm 1's
     buffer W, generalised to a recent window of at least w tokens).
 
     Returns (ws, n_cand): W = [ws, t) is always attended; segments
-    0 .. n_cand-1 (tokens [0, ws)) are the scoring candidates.
+    0 .. n_cand-1 are the scoring candidates. Without sinks they cover
+    [0, ws). With n_sink attention-sink tokens, tokens [0, min(n_sink, t))
+    are always attended and belong to no segment; segment s covers
+    [n_sink + s*c, n_sink + s*c + c), and the split applies to the tokens
+    after the sinks: ws = n_sink + c * floor(max(0, t - n_sink - w) / c)
+    (ws = t when t <= n_sink).
     """
-    ws = c * (max(0, t - w) // c)
-    return ws, ws // c
+    sink = min(n_sink, t)
+    rest = t - sink
+    ws_rel = c * (max(0, rest - w) // c)
+    return sink + ws_rel, ws_rel // c
 
 
 def segment_scores(phi_q, summaries):
@@ -100,11 +111,13 @@ def top_segments(scores, k):
     return np.asarray(order[:min(k, len(scores))], dtype=np.int64)
 
 
-def attended_tokens(segments, c, ws, t):
-    """Token positions attended: the union of the selected segments' tokens
-    and the window W = [ws, t) (Algorithm 1, S <- S u W)."""
+def attended_tokens(segments, c, ws, t, n_sink=0):
+    """Token positions attended: the sink tokens [0, min(n_sink, ws)), the
+    union of the selected segments' tokens and the window W = [ws, t)
+    (Algorithm 1, S <- S u W)."""
     segs = sorted(set(int(s) for s in segments))
-    toks = [np.arange(s * c, s * c + c) for s in segs]
+    toks = [np.arange(0, min(n_sink, ws))]
+    toks += [np.arange(n_sink + s * c, n_sink + s * c + c) for s in segs]
     toks.append(np.arange(ws, t))
     return np.concatenate(toks).astype(np.int64)
 
@@ -137,15 +150,65 @@ def decode_head(phi_q, summaries, n_cand, k):
     return sc, sel
 
 
-def decode(q, K, V, omega, summaries, t, k, c, w):
+def _decode(q, K, V, t, k, c, w, n_sink, per_head, head_scores):
+    """Shared body of decode() and decode_exact(): head_scores(b, g, h,
+    n_cand) gives one query head's candidate scores."""
+    q = _f64(q)
+    B, Hq, d = q.shape
+    Hkv = K.shape[1]
+    G = Hq // Hkv
+    lens = [int(t)] * B if np.ndim(t) == 0 else [int(x) for x in t]
+    assert len(lens) == B
+    out = np.zeros((B, Hq, d))
+    selected = -np.ones((B, Hq, k), dtype=np.int64)
+    sel_scores = np.full((B, Hq, k), np.nan)
+    scores, union = {}, {}
+    ws_b, nc_b, ke_b = [], [], []
+    for b in range(B):
+        tb = lens[b]
+        ws, n_cand = window_split(tb, c, w, n_sink)
+        k_eff = min(k, n_cand)
+        ws_b.append(ws); nc_b.append(n_cand); ke_b.append(k_eff)
+        for g in range(Hkv):
+            heads = range(g * G, (g + 1) * G)
+            own = {}
+            for h in heads:
+                sc = head_scores(b, g, h, n_cand)
+                sel = top_segments(sc, k)
+                scores[(b, h)] = sc
+                selected[b, h, :k_eff] = sel
+                sel_scores[b, h, :k_eff] = sc[sel]
+                own[h] = sel.tolist()
+            union[(b, g)] = sorted(set(s for h in heads for s in own[h]))
+            for h in heads:
+                segs = own[h] if per_head else union[(b, g)]
+                toks = attended_tokens(segs, c, ws, tb, n_sink)
+                out[b, h] = attend(q[b, h], K[b, g], V[b, g], toks)
+    res = dict(out=out, selected=selected, sel_scores=sel_scores,
+               scores=scores, union=union, ws_b=ws_b, n_cand_b=nc_b,
+               k_eff_b=ke_b)
+    if np.ndim(t) == 0:
+        res.update(ws=ws_b[0], n_cand=nc_b[0], k_eff=ke_b[0])
+    return res
+
+
+def decode(q, K, V, omega, summaries, t, k, c, w, n_sink=0, per_head=False):
     """One decode step for every (batch, query head) (Algorithm 1, querying
     procedure): phi(q) -> segment scores over the candidates -> top-k ->
     union over the query heads sharing a kv head -> exact attention over the
     union's tokens plus the window.
 
     q: [B, Hq, d]; K, V: [B, Hkv, >=t, d]; summaries: [B, Hkv, >=n_cand, n]
-    (the oracle's own, from `segment_summaries`); t: current length (the
-    query's own token is position t-1).
+    (the oracle's own, from `segment_summaries` with offset=n_sink); t:
+    current length (the query's own token is position t-1), one int for the
+    whole batch or one per sequence (a ragged batch: each sequence b is
+    decoded at its own length t[b]).
+
+    Options outside the paper's single-head description:
+      n_sink    tokens [0, n_sink) are attention sinks (always attended,
+                never in a segment); see window_split.
+      per_head  grouped-query attention where every query head attends its
+                own selection plus W instead of its group's union.
 
     Returns dict with
       out      [B, Hq, d]
@@ -153,36 +216,15 @@ def decode(q, K, V, omega, summaries, t, k, c, w):
       sel_scores [B, Hq, k] (nan padded)
       scores   list per (b, h): all candidate scores
       union    list per (b, g): sorted union of the group's selections
-      ws, n_cand
+      ws_b, n_cand_b, k_eff_b  per sequence; ws, n_cand, k_eff when t is
+                one int
     """
-    q = _f64(q)
-    B, Hq, d = q.shape
-    Hkv = K.shape[1]
-    G = Hq // Hkv
-    ws, n_cand = window_split(t, c, w)
-    k_eff = min(k, n_cand)
-    out = np.zeros((B, Hq, d))
-    selected = -np.ones((B, Hq, k), dtype=np.int64)
-    sel_scores = np.full((B, Hq, k), np.nan)
-    scores = {}
-    union = {}
-    for b in range(B):
-        for g in range(Hkv):
-            heads = range(g * G, (g + 1) * G)
-            picks = []
-            for h in heads:
-                phi_q = random_features(q[b, h], omega)
-                sc, sel = decode_head(phi_q, summaries[b, g], n_cand, k)
-                scores[(b, h)] = sc
-                selected[b, h, :k_eff] = sel
-                sel_scores[b, h, :k_eff] = sc[sel]
-                picks.extend(sel.tolist())
-            union[(b, g)] = sorted(set(picks))
-            toks = attended_tokens(union[(b, g)], c, ws, t)
-            for h in heads:
-                out[b, h] = attend(q[b, h], K[b, g], V[b, g], toks)
-    return dict(out=out, selected=selected, sel_scores=sel_scores,
-                scores=scores, union=union, ws=ws, n_cand=n_cand, k_eff=k_eff)
+    q64 = _f64(q)
+
+    def head_scores(b, g, h, n_cand):
+        phi_q = random_features(q64[b, h], omega)
+        return decode_head(phi_q, summaries[b, g], n_cand, k)[0]
+    return _decode(q64, K, V, t, k, c, w, n_sink, per_head, head_scores)
 
 
 def sqrt_schedule(t):
@@ -204,54 +246,35 @@ def sqrt_schedule(t):
     return c, t - c * c
 
 
-def exact_segment_mass(q, keys, c, n_cand):
+def exact_segment_mass(q, keys, c, n_cand, offset=0):
     """Exact segment attention mass (the quantity Theorem 2's proof calls
     beta): beta_s = sum over the c keys of segment s of exp(q . k / sqrt(d)),
     the unnormalised attention weight the segment carries. Selecting the k
     largest is the exact segment search of the ablation study (Section 3.3).
     Returns ln(beta_s) for s < n_cand (the log keeps large logits finite;
-    each segment subtracts its own max logit before exponentiating)."""
+    each segment subtracts its own max logit before exponentiating).
+    Segment s covers keys [offset + s*c, offset + s*c + c)."""
     q = _f64(q)
     keys = _f64(keys)
     d = q.shape[-1]
     out = np.empty(n_cand)
     for s in range(n_cand):
-        lg = keys[s * c:(s + 1) * c] @ q / np.sqrt(d)
+        lo = offset + s * c
+        lg = keys[lo:lo + c] @ q / np.sqrt(d)
         m = lg.max()
         out[s] = m + np.log(np.exp(lg - m).sum())
     return out
 
 
-def decode_exact(q, K, V, t, k, c, w):
+def decode_exact(q, K, V, t, k, c, w, n_sink=0, per_head=False):
     """decode() with the exact segment search in place of the random-feature
     scores: every query head selects the k segments with the largest
-    beta_s; the union over the heads sharing a kv head plus the window is
-    attended exactly. Returns the same dict as decode() with `scores` and
-    `sel_scores` holding ln(beta)."""
-    q = _f64(q)
-    B, Hq, d = q.shape
-    Hkv = K.shape[1]
-    G = Hq // Hkv
-    ws, n_cand = window_split(t, c, w)
-    k_eff = min(k, n_cand)
-    out = np.zeros((B, Hq, d))
-    selected = -np.ones((B, Hq, k), dtype=np.int64)
-    sel_scores = np.full((B, Hq, k), np.nan)
-    scores, union = {}, {}
-    for b in range(B):
-        for g in range(Hkv):
-            heads = range(g * G, (g + 1) * G)
-            picks = []
-            for h in heads:
-                sc = exact_segment_mass(q[b, h], K[b, g], c, n_cand)
-                sel = top_segments(sc, k)
-                scores[(b, h)] = sc
-                selected[b, h, :k_eff] = sel
-                sel_scores[b, h, :k_eff] = sc[sel]
-                picks.extend(sel.tolist())
-            union[(b, g)] = sorted(set(picks))
-            toks = attended_tokens(union[(b, g)], c, ws, t)
-            for h in heads:
-                out[b, h] = attend(q[b, h], K[b, g], V[b, g], toks)
-    return dict(out=out, selected=selected, sel_scores=sel_scores,
-                scores=scores, union=union, ws=ws, n_cand=n_cand, k_eff=k_eff)
+    beta_s; the union over the heads sharing a kv head (or, per_head, the
+    head's own selection) plus the sinks and the window is attended exactly.
+    Returns the same dict as decode() with `scores` and `sel_scores`
+    holding ln(beta)."""
+    q64 = _f64(q)
+
+    def head_scores(b, g, h, n_cand):
+        return exact_segment_mass(q64[b, h], K[b, g], c, n_cand, offset=n_sink)
+    return _decode(q64, K, V, t, k, c, w, n_sink, per_head, head_scores)

@@ -468,3 +468,152 @@ def test_decode_exact_all_selected_is_full_attention():
         np.testing.assert_allclose(res["out"][0, h],
                                    _sdpa(q[0, h], K[0, h // 2], V[0, h // 2]),
                                    rtol=1e-12, atol=1e-13)
+
+
+# --------------------------------------------------------------------------
+# serving options: attention sinks, per-head GQA attention, ragged batches
+# --------------------------------------------------------------------------
+def _summ(K, om, c, n_sink, B, Hkv, t):
+    return np.stack([np.stack([orc.segment_summaries(K[b, g, :t], om, c,
+                                                     offset=n_sink)
+                               for g in range(Hkv)]) for b in range(B)])
+
+
+@pytest.mark.parametrize("t,c,w,n_sink", [
+    (50, 8, 8, 4), (50, 8, 0, 1), (3, 4, 2, 5), (5, 4, 2, 5), (64, 8, 0, 8),
+    (100, 7, 3, 20), (21, 4, 30, 2)])
+def test_sink_layout_partitions_the_context(t, c, w, n_sink):
+    """Sinks, candidate segments and the window are disjoint and cover
+    [0, t); the candidates are whole c-blocks after the sinks; the window
+    holds at least min(w, t - sinks) and fewer than w + c tokens."""
+    ws, n_cand = orc.window_split(t, c, w, n_sink)
+    toks = orc.attended_tokens(range(n_cand), c, ws, t, n_sink)
+    assert sorted(toks.tolist()) == list(range(t))
+    sink = min(n_sink, t)
+    assert ws == sink + n_cand * c
+    rest = t - sink
+    if rest <= w:
+        assert t - ws == rest
+    else:
+        assert w <= t - ws <= w + c - 1
+    if t <= n_sink:
+        assert (ws, n_cand) == (t, 0)
+
+
+@pytest.mark.parametrize("t,c,w,n_sink,Hq,Hkv", [
+    (50, 8, 8, 4, 2, 2), (37, 4, 6, 3, 4, 2), (5, 4, 2, 9, 2, 1),
+    (64, 8, 0, 8, 2, 2), (9, 4, 0, 1, 1, 1)])
+def test_sinks_all_selected_is_full_attention(t, c, w, n_sink, Hq, Hkv):
+    rng = np.random.default_rng(t + n_sink)
+    B, d, n = 2, 8, 16
+    q = rng.standard_normal((B, Hq, d))
+    K = rng.standard_normal((B, Hkv, t + 2, d))
+    V = rng.standard_normal((B, Hkv, t + 2, d))
+    om = rng.standard_normal((n, d))
+    summ = _summ(K, om, c, n_sink, B, Hkv, t)
+    _, n_cand = orc.window_split(t, c, w, n_sink)
+    G = Hq // Hkv
+    for per_head in (False, True):
+        res = orc.decode(q, K, V, om, summ, t, max(n_cand, 1), c, w,
+                         n_sink=n_sink, per_head=per_head)
+        ex = orc.decode_exact(q, K, V, t, max(n_cand, 1), c, w,
+                              n_sink=n_sink, per_head=per_head)
+        for b in range(B):
+            for h in range(Hq):
+                ref = _sdpa(q[b, h], K[b, h // G, :t], V[b, h // G, :t])
+                np.testing.assert_allclose(res["out"][b, h], ref, rtol=1e-12,
+                                           atol=1e-13)
+                np.testing.assert_allclose(ex["out"][b, h], ref, rtol=1e-12,
+                                           atol=1e-13)
+
+
+def test_sink_is_attended_even_when_unselected():
+    """One sink key aligned with the query carries almost all the softmax
+    weight: the output tends to that token's value although no segment
+    holds it (exp(-25) bounds the rest)."""
+    rng = np.random.default_rng(5)
+    d, t, c, w, n = 8, 60, 4, 4, 32
+    q = rng.standard_normal((1, 1, d))
+    q /= np.linalg.norm(q)
+    K = rng.standard_normal((1, 1, t, d)) * 0.3
+    K[0, 0, 0] = 75.0 * q[0, 0]                 # logit 75 / sqrt(8) ~ 26.5
+    V = rng.standard_normal((1, 1, t, d))
+    om = rng.standard_normal((n, d))
+    summ = _summ(K, om, c, 1, 1, 1, t)
+    res = orc.decode(q, K, V, om, summ, t, 1, c, w, n_sink=1)
+    assert 0 not in res["selected"][0, 0]       # segment ids count after sinks
+    np.testing.assert_allclose(res["out"][0, 0], V[0, 0, 0], atol=1e-8)
+    # without the sink option token 0 sits in segment 0 and may be dropped
+    summ0 = _summ(K, om, c, 0, 1, 1, t)
+    res0 = orc.decode(q, K, V, om, summ0, t, 1, c, w)
+    toks0 = orc.attended_tokens(res0["selected"][0, 0], c, res0["ws"], t)
+    assert (0 in toks0) == np.allclose(res0["out"][0, 0], V[0, 0, 0],
+                                       atol=1e-8)
+
+
+def test_sink_summaries_are_the_shifted_segments():
+    rng = np.random.default_rng(8)
+    K = rng.standard_normal((70, 8))
+    om = rng.standard_normal((16, 8))
+    # the offset path equals the hand-pinned offset-0 path on shifted keys
+    got = orc.segment_summaries(K, om, 6, offset=5)
+    assert got.shape == ((70 - 5) // 6, 16)
+    np.testing.assert_array_equal(got, orc.segment_summaries(K[5:], om, 6))
+    np.testing.assert_array_equal(
+        orc.segment_summaries(K, om, 6, n_seg=7, first=3, offset=5), got[3:7])
+
+
+def test_per_head_gqa_is_mha_on_repeated_kv():
+    """Per-head GQA attention equals MHA (one kv head per query head) on the
+    group's K / V and summaries repeated per head: there each head's union
+    is its own selection."""
+    rng = np.random.default_rng(17)
+    B, Hq, Hkv, d, c, w, n, k, t, s0 = 2, 8, 2, 8, 4, 5, 32, 2, 61, 3
+    G = Hq // Hkv
+    q = rng.standard_normal((B, Hq, d))
+    K = rng.standard_normal((B, Hkv, t, d))
+    V = rng.standard_normal((B, Hkv, t, d))
+    om = rng.standard_normal((n, d))
+    summ = _summ(K, om, c, s0, B, Hkv, t)
+    gqa = orc.decode(q, K, V, om, summ, t, k, c, w, n_sink=s0, per_head=True)
+    Kr, Vr, Sr = (np.repeat(x, G, axis=1) for x in (K, V, summ))
+    mha = orc.decode(q, Kr, Vr, om, Sr, t, k, c, w, n_sink=s0)
+    np.testing.assert_array_equal(gqa["selected"], mha["selected"])
+    np.testing.assert_allclose(gqa["out"], mha["out"], rtol=1e-13, atol=1e-14)
+    # the union mode differs from it once the group's selections differ
+    uni = orc.decode(q, K, V, om, summ, t, k, c, w, n_sink=s0)
+    np.testing.assert_array_equal(uni["selected"], gqa["selected"])
+    differ = [(b, g) for b in range(B) for g in range(Hkv)
+              if len(uni["union"][(b, g)]) > k]
+    assert differ
+    b, g = differ[0]
+    assert not np.allclose(uni["out"][b, g * G:(g + 1) * G],
+                           gqa["out"][b, g * G:(g + 1) * G])
+
+
+def test_ragged_batch_is_per_sequence_decode():
+    rng = np.random.default_rng(23)
+    B, Hq, Hkv, d, c, w, n, k, s0 = 4, 4, 2, 8, 5, 6, 32, 3, 2
+    lens = [9, 64, 1, 40]
+    T = max(lens)
+    q = rng.standard_normal((B, Hq, d))
+    K = rng.standard_normal((B, Hkv, T, d))
+    V = rng.standard_normal((B, Hkv, T, d))
+    om = rng.standard_normal((n, d))
+    summ = _summ(K, om, c, s0, B, Hkv, T)
+    for per_head in (False, True):
+        rag = orc.decode(q, K, V, om, summ, lens, k, c, w, n_sink=s0,
+                         per_head=per_head)
+        rex = orc.decode_exact(q, K, V, lens, k, c, w, n_sink=s0,
+                               per_head=per_head)
+        for b, tb in enumerate(lens):
+            one = orc.decode(q[b:b + 1], K[b:b + 1, :, :tb], V[b:b + 1, :, :tb],
+                             om, summ[b:b + 1], tb, k, c, w, n_sink=s0,
+                             per_head=per_head)
+            np.testing.assert_array_equal(rag["selected"][b], one["selected"][0])
+            np.testing.assert_allclose(rag["out"][b], one["out"][0], rtol=1e-14)
+            ex1 = orc.decode_exact(q[b:b + 1], K[b:b + 1, :, :tb],
+                                   V[b:b + 1, :, :tb], tb, k, c, w, n_sink=s0,
+                                   per_head=per_head)
+            np.testing.assert_allclose(rex["out"][b], ex1["out"][0], rtol=1e-14)
+            assert rag["n_cand_b"][b] == orc.window_split(tb, c, w, s0)[1]
