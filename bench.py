@@ -79,7 +79,8 @@ class Stepper:
     def step(self, i, sel=None):
         t = self.t0 + i
         st = self.L.radar_append(self.cfgp, self.K, self.V, self.kn[i],
-                                 self.vn[i], self.om, t, self.summ, self.stream)
+                                 self.vn[i], self.om, t, None, self.summ,
+                                 self.stream)
         if st:
             raise radar.RadarError("radar_append", st)
         if self.sqrt:
@@ -96,11 +97,11 @@ class Stepper:
             self.cfg_c.window = t + 1 - c * c
         if self.exact:
             st = self.L.radar_decode_exact(self.cfgp, self.q[i], self.K, self.V,
-                                           t + 1, self.k, self.out, sel, None,
-                                           self.ws, self.ws_n, self.stream)
+                                           t + 1, None, self.k, self.out, sel,
+                                           None, self.ws, self.ws_n, self.stream)
         else:
             st = self.L.radar_decode(self.cfgp, self.q[i], self.K, self.V,
-                                     self.om, self.summ, t + 1, self.k,
+                                     self.om, self.summ, t + 1, None, self.k,
                                      self.out, sel, None, self.ws, self.ws_n,
                                      self.stream)
         if st:

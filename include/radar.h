@@ -54,7 +54,26 @@
  *  Each query head selects k_eff = min(k, n_cand) of them, ordered by score
  *  descending and then by segment index ascending. With grouped-query
  *  attention (Hq = G * Hkv) every query head of a group attends the union of
- *  the group's selections plus W.
+ *  the group's selections plus W (RADAR_GQA_UNION), or only its own
+ *  selection plus W (RADAR_GQA_PER_HEAD).
+ *
+ *  Attention sinks (n_sink > 0, as in the sink token of Appendix E): tokens
+ *  [0, min(n_sink, t)) are attended by every query head and belong to no
+ *  segment. Segment s then covers [n_sink + s*c, n_sink + s*c + c), and the
+ *  window rule above applies to the tokens after the sinks:
+ *  ws = n_sink + c * floor(max(0, t - n_sink - w) / c) (W is empty while
+ *  t <= n_sink). Summary row s still holds segment s.
+ *
+ *  Ragged batches: radar_decode, radar_decode_exact and radar_attend_selected
+ *  take an optional device array lens[B] (int64) of per-sequence context
+ *  lengths; the call's t is then their upper bound (grid sizes derive from
+ *  it) and sequence b is decoded exactly as a call with t = lens[b] would
+ *  decode it. A length outside [1, t] is not checked on the host: that
+ *  sequence selects nothing (ids -1, scores NaN) and its outputs are NaN.
+ *  radar_append takes pos[B] likewise. Build the index of a ragged batch
+ *  with t = the longest length: a segment that a shorter sequence has not
+ *  yet filled is summarised again by the append that completes it, before
+ *  it can become a candidate.
  */
 #ifndef RADAR_H
 #define RADAR_H
@@ -67,7 +86,7 @@
 extern "C" {
 #endif
 
-#define RADAR_ABI_VERSION 1
+#define RADAR_ABI_VERSION 2
 
 typedef enum {
   RADAR_OK = 0,
@@ -80,6 +99,11 @@ typedef enum {
 
 typedef enum { RADAR_F32 = 0, RADAR_BF16 = 1 } radar_dtype;
 
+typedef enum {
+  RADAR_GQA_UNION = 0,    /* each head attends its group's union (default)  */
+  RADAR_GQA_PER_HEAD = 1  /* each head attends its own selection            */
+} radar_gqa;
+
 typedef struct {
   int32_t batch;       /* B >= 1                                            */
   int32_t n_q_heads;   /* Hq; Hq % Hkv == 0, G = Hq / Hkv in {1, 2, 4, 8}   */
@@ -90,41 +114,47 @@ typedef struct {
   int32_t window;      /* w >= 0                                            */
   int64_t capacity;    /* token rows per head in K and V, 1 .. 2^31 - 1     */
   radar_dtype kv_dtype;
+  int32_t n_sink;      /* attention-sink tokens, 0 .. capacity (0: none)    */
+  radar_gqa gqa_mode;  /* which segments a grouped query head attends       */
 } radar_config;
 
 /* Index build (Eq. 4 and Eq. 5; Algorithm 1's restructuring step that
  * pre-computes the segment embeddings). Writes summaries rows
- * 0 .. floor(t / c) - 1 of every (b, kv head) from K[:, :, 0:t). Rows at and
- * beyond floor(t / c) are not touched. Requires 1 <= t <= capacity. */
+ * 0 .. floor((t - n_sink) / c) - 1 of every (b, kv head) from the rows of K
+ * before t. Rows beyond are not touched. Requires 1 <= t <= capacity. */
 radar_status radar_build_index(const radar_config* cfg, const void* K,
                                const float* omega, int64_t t,
                                float* summaries, hipStream_t stream);
 
 /* Append one token (Algorithm 1: the new key joins the buffer W). Writes
  * k_new / v_new ([B][Hkv][d]) to row t of K / V. If the row completes a
- * segment ((t + 1) % c == 0) the summary of segment (t + 1) / c - 1 is
- * computed with exactly the code path of radar_build_index, so appending
- * and rebuilding give bit-identical summaries. Requires 0 <= t < capacity;
- * the caller's context length becomes t + 1. */
+ * segment (r = t - n_sink >= 0 and (r + 1) % c == 0) the summary of segment
+ * (r + 1) / c - 1 is computed with exactly the code path of
+ * radar_build_index, so appending and rebuilding give bit-identical
+ * summaries. Requires 0 <= t < capacity; the caller's context length
+ * becomes t + 1. With pos (nullable, device int64 [B]) sequence b writes
+ * row pos[b] instead and t is ignored; a pos[b] outside [0, capacity) is
+ * skipped (no write, no summary). */
 radar_status radar_append(const radar_config* cfg, void* K, void* V,
                           const void* k_new, const void* v_new,
-                          const float* omega, int64_t t, float* summaries,
-                          hipStream_t stream);
+                          const float* omega, int64_t t, const int64_t* pos,
+                          float* summaries, hipStream_t stream);
 
 /* Decode one query per (b, q head) (Algorithm 1, querying step): phi(q)
  * (Eq. 4), scores of the n_cand candidate segments (Eq. 6), top-k, and exact
  * softmax attention (Eq. 1-2) over the selected segments plus W, with the
  * softmax scale 1/sqrt(d). t is the context length including the query's own
- * token (append first, then decode). k >= 1.
- * `selected` and `scores` may be NULL. `workspace` must hold at least
- * radar_decode_workspace_bytes(cfg, k) bytes; its contents on entry do not
- * matter and it must not be used by another call at the same time. */
+ * token (append first, then decode); lens (nullable, device int64 [B])
+ * gives per-sequence lengths with t their bound (see Ragged batches).
+ * k >= 1. `selected` and `scores` may be NULL. `workspace` must hold at
+ * least radar_decode_workspace_bytes(cfg, k) bytes; its contents on entry do
+ * not matter and it must not be used by another call at the same time. */
 radar_status radar_decode(const radar_config* cfg, const void* q,
                           const void* K, const void* V, const float* omega,
-                          const float* summaries, int64_t t, int32_t k,
-                          void* out, int32_t* selected, float* scores,
-                          void* workspace, size_t workspace_bytes,
-                          hipStream_t stream);
+                          const float* summaries, int64_t t,
+                          const int64_t* lens, int32_t k, void* out,
+                          int32_t* selected, float* scores, void* workspace,
+                          size_t workspace_bytes, hipStream_t stream);
 
 /* Exact segment search (the exact-selection ablation of Section 3.3): like
  * radar_decode, but each query head selects the k candidate segments with
@@ -136,9 +166,10 @@ radar_status radar_decode(const radar_config* cfg, const void* q,
  * Workspace as for radar_decode; summaries and Omega are not used. */
 radar_status radar_decode_exact(const radar_config* cfg, const void* q,
                                 const void* K, const void* V, int64_t t,
-                                int32_t k, void* out, int32_t* selected,
-                                float* scores, void* workspace,
-                                size_t workspace_bytes, hipStream_t stream);
+                                const int64_t* lens, int32_t k, void* out,
+                                int32_t* selected, float* scores,
+                                void* workspace, size_t workspace_bytes,
+                                hipStream_t stream);
 
 /* Scratch bytes radar_decode, radar_decode_exact and radar_attend_selected
  * need for this shape and k (0 if cfg is invalid). */
@@ -147,13 +178,14 @@ size_t radar_decode_workspace_bytes(const radar_config* cfg, int32_t k);
 /* Exact attention over caller-chosen segments (the last step of Algorithm 1
  * with the selection supplied): selected [B][Hq][k] holds segment ids, -1
  * for none; ids outside [0, n_cand) are ignored. Each query head attends the
- * union of its group's ids plus W, exactly as radar_decode does (an empty
- * union with an empty W, possible only when w = 0, gives a zero output). */
+ * union of its group's ids (or its own ids, RADAR_GQA_PER_HEAD) plus the
+ * sinks and W, exactly as radar_decode does; a head that attends no token
+ * gets a zero output. lens as for radar_decode. */
 radar_status radar_attend_selected(const radar_config* cfg, const void* q,
                                    const void* K, const void* V,
                                    const int32_t* selected, int32_t k,
-                                   int64_t t, void* out, void* workspace,
-                                   size_t workspace_bytes,
+                                   int64_t t, const int64_t* lens, void* out,
+                                   void* workspace, size_t workspace_bytes,
                                    hipStream_t stream);
 
 /* Algorithm 1's dynamic restructuring (Section 2.2, Appendix A): the
@@ -187,8 +219,9 @@ typedef enum {
  * RADAR_PATH_AUTO). For tests and tuning; results stay within tolerance. */
 radar_status radar_set_decode_path(int32_t path);
 
-/* The path radar_decode would take for this shape, t and k on this thread
- * (RADAR_PATH_SPLIT or RADAR_PATH_FUSED; -1 if the arguments are invalid). */
+/* The path radar_decode would take for this shape, t (the length, or the
+ * bound of a ragged call's lengths) and k on this thread (RADAR_PATH_SPLIT or
+ * RADAR_PATH_FUSED; -1 if the arguments are invalid). */
 int32_t radar_decode_path(const radar_config* cfg, int64_t t, int32_t k);
 
 /* Kernel kinds reported by the measurement hook below. */

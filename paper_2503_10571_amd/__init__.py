@@ -17,7 +17,9 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libradar.so")
 
+ABI_VERSION = 2
 RADAR_F32, RADAR_BF16 = 0, 1
+GQA_UNION, GQA_PER_HEAD = 0, 1
 STATUS = {0: "ok", 1: "invalid argument", 2: "position outside the cache capacity",
           3: "shape not supported by this build", 4: "HIP launch failed",
           5: "workspace missing or too small"}
@@ -37,12 +39,16 @@ class _Config(ctypes.Structure):
                 ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("n_features", ctypes.c_int32), ("seg_len", ctypes.c_int32),
                 ("window", ctypes.c_int32), ("capacity", ctypes.c_int64),
-                ("kv_dtype", ctypes.c_int32)]
+                ("kv_dtype", ctypes.c_int32), ("n_sink", ctypes.c_int32),
+                ("gqa_mode", ctypes.c_int32)]
 
 
 @dataclasses.dataclass(frozen=True)
 class Config:
-    """Shape of one Radar layer (mirrors radar_config)."""
+    """Shape of one Radar layer (mirrors radar_config). n_sink: leading
+    attention-sink tokens (always attended, in no segment); gqa_mode:
+    GQA_UNION (each query head attends its group's union) or GQA_PER_HEAD
+    (its own selection)."""
     batch: int
     n_q_heads: int
     n_kv_heads: int
@@ -52,12 +58,15 @@ class Config:
     window: int
     capacity: int
     dtype: torch.dtype = torch.bfloat16
+    n_sink: int = 0
+    gqa_mode: int = GQA_UNION
 
     def c_struct(self) -> _Config:
         dt = {torch.float32: RADAR_F32, torch.bfloat16: RADAR_BF16}[self.dtype]
         return _Config(self.batch, self.n_q_heads, self.n_kv_heads,
                        self.head_dim, self.n_features, self.seg_len,
-                       self.window, self.capacity, dt)
+                       self.window, self.capacity, dt, self.n_sink,
+                       self.gqa_mode)
 
     @property
     def summary_rows(self) -> int:
@@ -77,22 +86,25 @@ def lib() -> ctypes.CDLL:
                 f"{LIB_PATH} is missing: build it with "
                 "`python -m paper_2503_10571_amd._build` (hipcc, gfx950)")
         L = ctypes.CDLL(LIB_PATH)
+        L.radar_abi_version.restype = ctypes.c_int32
+        if L.radar_abi_version() != ABI_VERSION:
+            raise RuntimeError(f"{LIB_PATH} has ABI {L.radar_abi_version()}, "
+                               f"this binding expects {ABI_VERSION}: rebuild it")
         cfgp = ctypes.POINTER(_Config)
         i64, i32, sz = ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
         L.radar_build_index.argtypes = [cfgp, _P, _P, i64, _P, _P]
-        L.radar_append.argtypes = [cfgp, _P, _P, _P, _P, _P, i64, _P, _P]
-        L.radar_decode.argtypes = [cfgp, _P, _P, _P, _P, _P, i64, i32, _P, _P,
-                                   _P, _P, sz, _P]
-        L.radar_decode_exact.argtypes = [cfgp, _P, _P, _P, i64, i32, _P, _P, _P,
-                                         _P, sz, _P]
+        L.radar_append.argtypes = [cfgp, _P, _P, _P, _P, _P, i64, _P, _P, _P]
+        L.radar_decode.argtypes = [cfgp, _P, _P, _P, _P, _P, i64, _P, i32, _P,
+                                   _P, _P, _P, sz, _P]
+        L.radar_decode_exact.argtypes = [cfgp, _P, _P, _P, i64, _P, i32, _P, _P,
+                                         _P, _P, sz, _P]
         L.radar_decode_workspace_bytes.argtypes = [cfgp, i32]
         L.radar_decode_workspace_bytes.restype = sz
         L.radar_attend_selected.argtypes = [cfgp, _P, _P, _P, _P, i32, i64, _P,
-                                            _P, sz, _P]
+                                            _P, _P, sz, _P]
         L.radar_status_string.argtypes = [ctypes.c_int]
         L.radar_status_string.restype = ctypes.c_char_p
         L.radar_last_error.restype = ctypes.c_char_p
-        L.radar_abi_version.restype = ctypes.c_int32
         L.radar_profile_enable.argtypes = [i32]
         L.radar_schedule_sqrt.argtypes = [i64, ctypes.POINTER(i32),
                                           ctypes.POINTER(i32)]
@@ -159,23 +171,30 @@ def build_index(cfg: Config, K, omega, t: int, summaries) -> None:
         _stream(K)))
 
 
-def append(cfg: Config, K, V, k_new, v_new, omega, t: int, summaries) -> None:
-    """radar_append: write row t; refresh the summary of a segment it fills."""
+def _lens(x, cfg: Config, name):
+    """Optional per-sequence int64 [B] device array."""
+    if x is None:
+        return None
+    _need(x, torch.int64, name)
+    if x.numel() != cfg.batch:
+        raise ValueError(f"{name} must hold batch = {cfg.batch} lengths")
+    return x
+
+
+def append(cfg: Config, K, V, k_new, v_new, omega, t: int, summaries,
+           pos=None) -> None:
+    """radar_append: write row t (or row pos[b] of sequence b); refresh the
+    summary of a segment the row completes."""
     for x, nm in ((K, "K"), (V, "V"), (k_new, "k_new"), (v_new, "v_new")):
         _need(x, cfg.dtype, nm)
     _need(omega, torch.float32, "omega"); _need(summaries, torch.float32, "summaries")
+    pos = _lens(pos, cfg, "pos")
     _check("radar_append", lib().radar_append(
         ctypes.byref(cfg.c_struct()), _ptr(K), _ptr(V), _ptr(k_new), _ptr(v_new),
-        _ptr(omega), t, _ptr(summaries), _stream(K)))
+        _ptr(omega), t, _ptr(pos), _ptr(summaries), _stream(K)))
 
 
-def decode(cfg: Config, q, K, V, omega, summaries, t: int, k: int, out=None,
-           selected=None, scores=None, workspace=None):
-    """radar_decode: one query per (b, q head). Returns out (and writes the
-    optional selected / scores tensors)."""
-    for x, nm in ((q, "q"), (K, "K"), (V, "V")):
-        _need(x, cfg.dtype, nm)
-    _need(omega, torch.float32, "omega"); _need(summaries, torch.float32, "summaries")
+def _outputs(cfg, q, k, out, selected, scores, workspace):
     if out is None:
         out = torch.empty_like(q)
     if workspace is None:
@@ -184,48 +203,55 @@ def decode(cfg: Config, q, K, V, omega, summaries, t: int, k: int, out=None,
         _need(selected, torch.int32, "selected")
     if scores is not None:
         _need(scores, torch.float32, "scores")
+    return out, workspace
+
+
+def decode(cfg: Config, q, K, V, omega, summaries, t: int, k: int, out=None,
+           selected=None, scores=None, workspace=None, lens=None):
+    """radar_decode: one query per (b, q head) at context length t (or at
+    lens[b] <= t per sequence). Returns out (and writes the optional
+    selected / scores tensors)."""
+    for x, nm in ((q, "q"), (K, "K"), (V, "V")):
+        _need(x, cfg.dtype, nm)
+    _need(omega, torch.float32, "omega"); _need(summaries, torch.float32, "summaries")
+    lens = _lens(lens, cfg, "lens")
+    out, workspace = _outputs(cfg, q, k, out, selected, scores, workspace)
     _check("radar_decode", lib().radar_decode(
         ctypes.byref(cfg.c_struct()), _ptr(q), _ptr(K), _ptr(V), _ptr(omega),
-        _ptr(summaries), t, k, _ptr(out), _ptr(selected), _ptr(scores),
-        _ptr(workspace), workspace.numel(), _stream(q)))
+        _ptr(summaries), t, _ptr(lens), k, _ptr(out), _ptr(selected),
+        _ptr(scores), _ptr(workspace), workspace.numel(), _stream(q)))
     return out
 
 
 def decode_exact(cfg: Config, q, K, V, t: int, k: int, out=None,
-                 selected=None, scores=None, workspace=None):
+                 selected=None, scores=None, workspace=None, lens=None):
     """radar_decode_exact: top-k segments by exact attention mass, then the
     same attention as decode(). scores receives ln(beta) of the picks."""
     for x, nm in ((q, "q"), (K, "K"), (V, "V")):
         _need(x, cfg.dtype, nm)
-    if out is None:
-        out = torch.empty_like(q)
-    if workspace is None:
-        workspace = new_workspace(cfg, k, q.device)
-    if selected is not None:
-        _need(selected, torch.int32, "selected")
-    if scores is not None:
-        _need(scores, torch.float32, "scores")
+    lens = _lens(lens, cfg, "lens")
+    out, workspace = _outputs(cfg, q, k, out, selected, scores, workspace)
     _check("radar_decode_exact", lib().radar_decode_exact(
-        ctypes.byref(cfg.c_struct()), _ptr(q), _ptr(K), _ptr(V), t, k, _ptr(out),
-        _ptr(selected), _ptr(scores), _ptr(workspace), workspace.numel(),
-        _stream(q)))
+        ctypes.byref(cfg.c_struct()), _ptr(q), _ptr(K), _ptr(V), t, _ptr(lens),
+        k, _ptr(out), _ptr(selected), _ptr(scores), _ptr(workspace),
+        workspace.numel(), _stream(q)))
     return out
 
 
 def attend_selected(cfg: Config, q, K, V, selected, t: int, out=None,
-                    workspace=None):
-    """radar_attend_selected: exact attention over given segment ids plus W."""
+                    workspace=None, lens=None):
+    """radar_attend_selected: exact attention over given segment ids plus
+    the sinks and W."""
     for x, nm in ((q, "q"), (K, "K"), (V, "V")):
         _need(x, cfg.dtype, nm)
     _need(selected, torch.int32, "selected")
+    lens = _lens(lens, cfg, "lens")
     k = selected.shape[-1]
-    if out is None:
-        out = torch.empty_like(q)
-    if workspace is None:
-        workspace = new_workspace(cfg, k, q.device)
+    out, workspace = _outputs(cfg, q, k, out, None, None, workspace)
     _check("radar_attend_selected", lib().radar_attend_selected(
         ctypes.byref(cfg.c_struct()), _ptr(q), _ptr(K), _ptr(V), _ptr(selected),
-        k, t, _ptr(out), _ptr(workspace), workspace.numel(), _stream(q)))
+        k, t, _ptr(lens), _ptr(out), _ptr(workspace), workspace.numel(),
+        _stream(q)))
     return out
 
 

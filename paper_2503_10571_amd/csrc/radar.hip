@@ -54,6 +54,52 @@ typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4_t;
 typedef __bf16 bf16x2v_t __attribute__((ext_vector_type(2)));
 
 // ---------------------------------------------------------------------------
+// token layout of one sequence at a decode step
+// ---------------------------------------------------------------------------
+// A sequence of length len starts with sink = min(n_sink, len) attention-sink
+// tokens. The kernels address K / V from the first row after the sinks
+// (the host offsets the pointers by n_sink rows), so in these row numbers
+// candidate segment s covers [s c, s c + c) for s < n_cand, the window is
+// [ws, t) with t = len - sink and ws = c floor(max(0, t - w) / c), and the
+// sinks are rows [-n_sink, -n_sink + sink). A length outside [1, t_max]
+// marks the sequence invalid: it selects nothing, attends nothing, and its
+// outputs are NaN.
+struct SeqArgs {
+  const int64_t* lens;  // [B] per-sequence lengths (device), or null: all t_max
+  int64_t t_max;
+  int c, w, n_sink, k;
+};
+
+// Lengths stay below 2^31 (the capacity limit), so the split is computed in
+// 32-bit arithmetic.
+struct Span {
+  int t, ws, n_cand, k_eff, sink;
+  bool ok;
+};
+
+__host__ __device__ inline Span make_span(int64_t len, const SeqArgs& a) {
+  Span p;
+  p.ok = len >= 1 && len <= a.t_max;
+  const int L = p.ok ? (int)len : 0;
+  p.sink = L < a.n_sink ? L : a.n_sink;
+  p.t = L - p.sink;
+  const unsigned past = p.t > a.w ? (unsigned)(p.t - a.w) : 0u;
+  p.n_cand = (int)(past / (unsigned)a.c);
+  p.ws = p.n_cand * a.c;
+  p.k_eff = p.n_cand < a.k ? p.n_cand : a.k;
+  return p;
+}
+
+__device__ __forceinline__ Span seq_span(const SeqArgs& a, int64_t b) {
+  return make_span(a.lens ? a.lens[b] : a.t_max, a);
+}
+
+// union entries: segment id in the low 16 bits, the mask of the group's
+// query heads that selected it in bits 16 .. 23
+constexpr int kUniIdBits = 16;
+constexpr unsigned kAllHeads = 0xffu;
+
+// ---------------------------------------------------------------------------
 // element helpers
 // ---------------------------------------------------------------------------
 template <typename T> struct Elem;
@@ -299,7 +345,8 @@ __global__ __launch_bounds__(256) void k_build(
     const T* __restrict__ K, const float* __restrict__ omega,
     float* __restrict__ summ, int n, int c, int64_t cap, int64_t s_cap,
     int seg_first, int seg_count, int64_t n_items, float s1, float s2,
-    float out_scale, int64_t kv_head_stride_rows) {
+    float out_scale, int64_t kv_head_stride_rows,
+    const int64_t* __restrict__ pos, int Hkv, int n_sink) {
   using MC = MfmaCfg<T>;
   using BT = BuildTile<T, D>;
   constexpr int KB = D / MC::kK;
@@ -344,12 +391,28 @@ __global__ __launch_bounds__(256) void k_build(
 #pragma unroll
   for (int f = 0; f < FT; ++f) psum[f] = 0.f;
 
-  // Base row pointer of an item (one (b, kv head, segment)); computed once
-  // per segment, in 32-bit arithmetic (item counts stay below 2^31).
+  // Segment of an item (one (b, kv head, segment); 32-bit arithmetic, item
+  // counts stay below 2^31): seg_first + item % seg_count, or, with pos
+  // (item = (b, kv head), one per-sequence segment close), the segment that
+  // row pos[b] completes, -1 if it completes none. Rows count from the
+  // first row after the n_sink sinks, where the K pointer starts.
+  auto seg_of = [&](int64_t it) -> int {
+    const uint32_t u = (uint32_t)it;
+    if (!pos) return seg_first + (int)(u % (uint32_t)seg_count);
+    const int64_t p = pos[u / (uint32_t)Hkv];
+    const int64_t r = p - n_sink;
+    if (p >= cap || r < 0 || (r + 1) % c != 0) return -1;
+    return (int)((r + 1) / c - 1);
+  };
+  // first active item at or after it on this workgroup's stride
+  auto next_active = [&](int64_t it) -> int64_t {
+    while (it < n_items && seg_of(it) < 0) it += gridDim.x;
+    return it;
+  };
+  // base row pointer of an item, computed once per segment
   auto item_base = [&](int64_t it) -> const T* {
-    const uint32_t u = (uint32_t)it, sc = (uint32_t)seg_count;
-    const uint32_t bh = u / sc, s = (uint32_t)seg_first + u % sc;
-    return K + ((int64_t)bh * kv_head_stride_rows + (int64_t)s * c) * D;
+    const uint32_t bh = (uint32_t)it / (uint32_t)seg_count;
+    return K + ((int64_t)bh * kv_head_stride_rows + (int64_t)seg_of(it) * c) * D;
   };
 
   uint4 pre[CPT];
@@ -451,7 +514,7 @@ __global__ __launch_bounds__(256) void k_build(
   // Pipeline, one barrier per tile: tile i is multiplied from one LDS buffer
   // while tile i+1 is in flight to registers; after the multiply the
   // registers go to the other buffer.
-  int64_t item = blockIdx.x;
+  int64_t item = next_active(blockIdx.x);
   int tl = 0, buf = 0;
   const T* base = nullptr;
   if (item < n_items) {
@@ -466,7 +529,7 @@ __global__ __launch_bounds__(256) void k_build(
     int ntl = tl + 1;
     const T* nbase = base;
     if (ntl == ntiles) {
-      nitem += gridDim.x;
+      nitem = next_active(nitem + gridDim.x);
       ntl = 0;
       if (nitem < n_items) nbase = item_base(nitem);
     }
@@ -477,8 +540,8 @@ __global__ __launch_bounds__(256) void k_build(
     else compute(buf, valid, std::false_type{});
 
     if (tl == ntiles - 1) {                // segment complete
-      const uint32_t u = (uint32_t)item, sc = (uint32_t)seg_count;
-      const int64_t bh = u / sc, sg = seg_first + u % sc;
+      const int64_t bh = (uint32_t)item / (uint32_t)seg_count;
+      const int64_t sg = seg_of(item);
       float* dst = summ + (bh * s_cap + sg) * n + fbase;
 #pragma unroll
       for (int f = 0; f < FT; ++f) {
@@ -502,14 +565,20 @@ __global__ __launch_bounds__(256) void k_build(
 // ---------------------------------------------------------------------------
 // k_append: K[b][h][t] = k_new[b][h], V likewise
 // ---------------------------------------------------------------------------
+// (row pos[b] of sequence b when pos is given; rows outside [0, cap) are
+// skipped)
 template <typename T, int D>
 __global__ __launch_bounds__(64) void k_append(T* __restrict__ K, T* __restrict__ V,
                                                const T* __restrict__ kn,
                                                const T* __restrict__ vn,
-                                               int64_t cap, int64_t t) {
+                                               int64_t cap, int64_t t,
+                                               const int64_t* __restrict__ pos,
+                                               int Hkv) {
   constexpr int CPR = D * (int)sizeof(T) / 16;
   const int64_t bh = blockIdx.x;
   const int i = threadIdx.x;
+  if (pos) t = pos[bh / Hkv];
+  if (t < 0 || t >= cap) return;
   if (i < CPR) {
     const uint4* sk = reinterpret_cast<const uint4*>(kn + bh * D) + i;
     const uint4* sv = reinterpret_cast<const uint4*>(vn + bh * D) + i;
@@ -712,25 +781,30 @@ __device__ void head_topk(const float* __restrict__ src, int n_cand, int k,
   }
 }
 
-// Union of the group's selections: sel[0 .. M) holds segment ids (-1 = none,
-// every other id < kMaxCand). The ids are set in an LDS bitmap, the first
-// wave turns the words' popcounts into prefix offsets, and each lane lists
-// its word's set bits: the distinct ids in ascending order go to uni and
-// their count to *ucnt. bits: kMaxCand / 32 words of LDS.
+// Union of the group's selections: sel[h * per .. h * per + per) holds the
+// segment ids of head h < G (-1 = none, every other id < kMaxCand). The ids
+// are set in an LDS bitmap (one per head when masks are wanted); the first
+// wave ORs the heads' words, turns the popcounts into prefix offsets, and
+// each lane lists its word's set bits: the distinct ids in ascending order go
+// to uni, each with the mask of the heads that chose it (all heads without
+// masks), and their count to *ucnt. bits: G * kMaxCand / 32 words of LDS.
 constexpr int kBitmapWords = kMaxCand / 32;
 static_assert(kBitmapWords == kWave, "one bitmap word per lane");
-__device__ void group_union(const int* sel, unsigned* bits, int M, int* uni,
-                            int* ucnt) {
+__device__ void group_union(const int* sel, unsigned* bits, int G, int per,
+                            bool masks, int* uni, int* ucnt) {
   const int tid = threadIdx.x;
-  for (int i = tid; i < kBitmapWords; i += blockDim.x) bits[i] = 0u;
+  const int nmaps = masks ? G : 1;
+  for (int i = tid; i < nmaps * kBitmapWords; i += blockDim.x) bits[i] = 0u;
   __syncthreads();
-  for (int i = tid; i < M; i += blockDim.x) {
+  for (int i = tid; i < G * per; i += blockDim.x) {
     const int id = sel[i];
-    if (id >= 0) atomicOr(&bits[id >> 5], 1u << (id & 31));
+    const int map = masks ? i / per : 0;
+    if (id >= 0) atomicOr(&bits[map * kBitmapWords + (id >> 5)], 1u << (id & 31));
   }
   __syncthreads();
   if (tid < kWave) {
-    uint32_t word = bits[tid];
+    uint32_t word = 0u;
+    for (int g = 0; g < nmaps; ++g) word |= bits[g * kBitmapWords + tid];
     const int pc = __popc(word);
     // exclusive prefix sum of the popcounts over the 64 lanes
     int incl = pc;
@@ -742,7 +816,13 @@ __device__ void group_union(const int* sel, unsigned* bits, int M, int* uni,
     int pos = incl - pc;
     while (word) {
       const int bit = __ffs(word) - 1;
-      uni[pos++] = tid * 32 + bit;
+      unsigned m = kAllHeads;
+      if (masks) {
+        m = 0u;
+        for (int g = 0; g < G; ++g)
+          m |= ((bits[g * kBitmapWords + tid] >> bit) & 1u) << g;
+      }
+      uni[pos++] = (tid * 32 + bit) | (int)(m << kUniIdBits);
       word &= word - 1u;
     }
     if (tid == kWave - 1) *ucnt = incl;
@@ -761,7 +841,7 @@ template <int N, int G>
 __global__ __launch_bounds__(256) void k_score(const float* __restrict__ phiq,
                                                const float* __restrict__ summ,
                                                float* __restrict__ scores,
-                                               int Hq, int Hkv, int n_cand,
+                                               int Hq, int Hkv, SeqArgs sa,
                                                int64_t s_cap, int nc_cap) {
   constexpr int FPL = N / 64;
   constexpr int RB = N <= 256 ? 2 : 1;     // 16-row batches per wave
@@ -769,6 +849,7 @@ __global__ __launch_bounds__(256) void k_score(const float* __restrict__ phiq,
   const int wave = threadIdx.x >> 6;
   const int64_t bh = blockIdx.y;
   const int64_t b = bh / Hkv, hk = bh % Hkv;
+  const int n_cand = seq_span(sa, b).n_cand;
   const int wrow0 = blockIdx.x * (64 * RB) + wave * (16 * RB);
   if (wrow0 >= n_cand) return;             // wave-uniform; no barriers below
 
@@ -831,18 +912,19 @@ __global__ __launch_bounds__(256) void k_score(const float* __restrict__ phiq,
 // group. The heads' sorted selections go to LDS and the union of the group
 // (ascending ids) to the workspace for the attention stage.
 __global__ __launch_bounds__(256) void k_topk_union(
-    const float* __restrict__ scores, int Hq, int Hkv, int G, int n_cand,
-    int nc_cap, int k, int k_eff, int* __restrict__ uni,
-    int* __restrict__ ucnt, int umax, int32_t* __restrict__ selected,
-    float* __restrict__ sel_scores) {
+    const float* __restrict__ scores, int Hq, int Hkv, int G, SeqArgs sa,
+    int nc_cap, int per_head, int* __restrict__ uni, int* __restrict__ ucnt,
+    int umax, int32_t* __restrict__ selected, float* __restrict__ sel_scores) {
   __shared__ int sel_lds[kMaxG * kMaxK];
-  __shared__ unsigned bits_lds[kBitmapWords];
+  __shared__ unsigned bits_lds[kMaxG * kBitmapWords];
   __shared__ unsigned hist_lds[4][256];
   __shared__ u64 list_lds[4][kMaxK];
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int64_t bh = blockIdx.x;
   const int64_t b = bh / Hkv, hk = bh % Hkv;
+  const Span sp = seq_span(sa, b);
+  const int n_cand = sp.n_cand, k_eff = sp.k_eff, k = sa.k;
   const int npl = (n_cand + 63) / 64;
   unsigned* hist = hist_lds[wave];
   u64* list = list_lds[wave];
@@ -860,7 +942,8 @@ __global__ __launch_bounds__(256) void k_topk_union(
     else head_topk<32>(src, n_cand, k, k_eff, row, so, sco, lane, hist, list);
   }
   __syncthreads();
-  group_union(sel_lds, bits_lds, G * k_eff, uni + bh * umax, ucnt + bh);
+  group_union(sel_lds, bits_lds, G, k_eff, per_head != 0, uni + bh * umax,
+              ucnt + bh);
 }
 
 // ---------------------------------------------------------------------------
@@ -876,7 +959,7 @@ __global__ __launch_bounds__(256) void k_topk_union(
 template <typename T, int D, int G>
 __global__ __launch_bounds__(256) void k_segment_mass(
     const T* __restrict__ q, const T* __restrict__ K, float* __restrict__ scores,
-    int Hq, int Hkv, int64_t cap, int c, int n_cand, int nc_cap, float qscale) {
+    int Hq, int Hkv, int64_t cap, SeqArgs sa, int nc_cap, float qscale) {
   constexpr int EPL = Elem<T>::kPer16;
   constexpr int LPR = D / EPL;
   constexpr int RPI = kWave / LPR;
@@ -886,8 +969,9 @@ __global__ __launch_bounds__(256) void k_segment_mass(
   const int wave = threadIdx.x >> 6;
   const int64_t bh = blockIdx.y;
   const int64_t b = bh / Hkv, hk = bh % Hkv;
+  const int c = sa.c;
   const int s = blockIdx.x * 4 + wave;
-  if (s >= n_cand) return;                 // wave-uniform; no barriers below
+  if (s >= seq_span(sa, b).n_cand) return; // wave-uniform; no barriers below
   const int r = lane / LPR, jj = lane % LPR;
 
   float qf[G][EPL];
@@ -948,11 +1032,13 @@ __global__ __launch_bounds__(256) void k_segment_mass(
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_union_given(
     const int32_t* __restrict__ given, int given_k, int Hq, int Hkv, int G,
-    int n_cand, int* __restrict__ uni, int* __restrict__ ucnt, int umax) {
+    SeqArgs sa, int per_head, int* __restrict__ uni, int* __restrict__ ucnt,
+    int umax) {
   __shared__ int sel_lds[kMaxG * kMaxK];
-  __shared__ unsigned bits_lds[kBitmapWords];
+  __shared__ unsigned bits_lds[kMaxG * kBitmapWords];
   const int64_t bh = blockIdx.x;
   const int64_t b = bh / Hkv, hk = bh % Hkv;
+  const int n_cand = seq_span(sa, b).n_cand;
   const int M = G * given_k;
   for (int i = threadIdx.x; i < M; i += 256) {
     const int hl = i / given_k, r = i % given_k;
@@ -960,7 +1046,8 @@ __global__ __launch_bounds__(256) void k_union_given(
     sel_lds[i] = (id >= 0 && id < n_cand) ? id : -1;
   }
   __syncthreads();
-  group_union(sel_lds, bits_lds, M, uni + bh * umax, ucnt + bh);
+  group_union(sel_lds, bits_lds, G, given_k, per_head != 0, uni + bh * umax,
+              ucnt + bh);
 }
 
 // ---------------------------------------------------------------------------
@@ -1005,10 +1092,12 @@ struct TileAttn {
   }
 
   // rows [row0, row0 + len) of K and V (row0 counts rows from the base
-  // pointers); 1 <= len <= 64; wave-uniform call
+  // pointers); 1 <= len <= 64; wave-uniform call. Head g of the group takes
+  // part only if bit g of hmask is set (a head that has attended nothing
+  // yet keeps m = -inf, l = 0, acc = 0).
   __device__ __forceinline__ void tile(const T* __restrict__ K,
                                        const T* __restrict__ V, int64_t row0,
-                                       int len, int lane) {
+                                       int len, int lane, unsigned hmask) {
     const int r = lane / LPR;
     const int jj = lane % LPR;
     const T* kbase = K + row0 * D + jj * EPL;
@@ -1047,10 +1136,12 @@ struct TileAttn {
     float p[G];
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      const float mt = wave_max(mine_ok ? lg[g] : -INFINITY);
+      const bool on = mine_ok && ((hmask >> g) & 1u);
+      const float mt = wave_max(on ? lg[g] : -INFINITY);
       const float mn = fmaxf(m[g], mt);
-      const float scale = fast_exp2(m[g] - mn);   // 0 on the first tile
-      p[g] = mine_ok ? fast_exp2(lg[g] - mn) : 0.f;
+      const float mref = mn == -INFINITY ? 0.f : mn;
+      const float scale = fast_exp2(m[g] - mref);  // 0 on the head's first tile
+      p[g] = on ? fast_exp2(lg[g] - mref) : 0.f;
       l[g] = fmaf(l[g], scale, wave_sum(p[g]));
       m[g] = mn;
 #pragma unroll
@@ -1090,15 +1181,17 @@ struct TileAttn {
 // k_attend: split attention, one partial (max, sum, acc[d]) per workgroup
 // ---------------------------------------------------------------------------
 // Tiles of a (b, kv head): tiles_per_seg per union segment, then ceil(|W| /
-// 64) window tiles. Workgroup j takes tiles [4 tpw j, 4 tpw (j + 1)); wave w
-// takes every fourth of them from 4 tpw j + w, with an online softmax across
-// its tiles, and the workgroup merges its four waves in LDS.
+// 64) window tiles, then ceil(sinks / 64) sink tiles. Workgroup j takes
+// tiles [4 tpw j, 4 tpw (j + 1)); wave w takes every fourth of them from
+// 4 tpw j + w, with an online softmax across its tiles, and the workgroup
+// merges its four waves in LDS. With per_head set, a segment tile counts
+// only for the heads that selected the segment.
 template <typename T, int D, int G>
 __global__ __launch_bounds__(256) void k_attend(
     const T* __restrict__ q, const T* __restrict__ K, const T* __restrict__ V,
     const int* __restrict__ uni, const int* __restrict__ ucnt,
-    float* __restrict__ part, int Hq, int Hkv, int64_t cap, int c,
-    int tiles_per_seg, int64_t ws, int64_t t, int umax, int maxwg, int tpw,
+    float* __restrict__ part, int Hq, int Hkv, int64_t cap,
+    int tiles_per_seg, SeqArgs sa, int per_head, int umax, int maxwg, int tpw,
     float qscale) {
   using TA = TileAttn<T, D, G>;
   constexpr int EPL = TA::EPL, LPR = TA::LPR;
@@ -1113,11 +1206,13 @@ __global__ __launch_bounds__(256) void k_attend(
   const int64_t bh = blockIdx.y;
   const int64_t b = bh / Hkv, hk = bh % Hkv;
   const int j = blockIdx.x;
+  const Span sp = seq_span(sa, b);
+  const int c = sa.c;
 
   const int U = ucnt[bh];
   const int seg_tiles = U * tiles_per_seg;
-  const int win_tiles = (int)((t - ws + kTile - 1) / kTile);
-  const int total = seg_tiles + win_tiles;
+  const int win_tiles = (int)(((int64_t)sp.t - sp.ws + kTile - 1) / kTile);
+  const int total = seg_tiles + win_tiles + (sp.sink + kTile - 1) / kTile;
   const int nwg = (total + 4 * tpw - 1) / (4 * tpw);
   if (j >= nwg) return;
 
@@ -1127,16 +1222,23 @@ __global__ __launch_bounds__(256) void k_attend(
   for (int ti = j * 4 * tpw + wave; ti < t_end; ti += 4) {   // wave-uniform
     int64_t start;
     int len;
+    unsigned hm = kAllHeads;
     if (ti < seg_tiles) {
-      const int s = uni[bh * umax + ti / tiles_per_seg];
+      const int e = uni[bh * umax + ti / tiles_per_seg];
+      const int s = e & ((1 << kUniIdBits) - 1);
+      if (per_head) hm = (unsigned)e >> kUniIdBits;
       const int off = (ti % tiles_per_seg) * kTile;
       start = (int64_t)s * c + off;
       len = min(kTile, c - off);
+    } else if (ti < seg_tiles + win_tiles) {
+      start = sp.ws + (int64_t)(ti - seg_tiles) * kTile;
+      len = (int)min((int64_t)kTile, sp.t - start);
     } else {
-      start = ws + (int64_t)(ti - seg_tiles) * kTile;
-      len = (int)min((int64_t)kTile, t - start);
+      const int off = (ti - seg_tiles - win_tiles) * kTile;
+      start = (int64_t)off - sa.n_sink;
+      len = min(kTile, sp.sink - off);
     }
-    ta.tile(K, V, bh * cap + start, len, lane);
+    ta.tile(K, V, bh * cap + start, len, lane, hm);
   }
   ta.reduce_rows();
 
@@ -1198,9 +1300,8 @@ __global__ __launch_bounds__(512) void k_decode_fused(
     const float* __restrict__ omega, const float* __restrict__ summ,
     T* __restrict__ out, int32_t* __restrict__ selected,
     float* __restrict__ sel_scores, int Hq, int Hkv, int64_t cap,
-    int64_t s_cap, int c, int tiles_per_seg, int64_t ws, int64_t t,
-    int n_cand, int k, int k_eff, float s1, float s2, float inv_sqrt_n,
-    float qscale) {
+    int64_t s_cap, int tiles_per_seg, SeqArgs sa, int per_head, float s1,
+    float s2, float inv_sqrt_n, float qscale) {
   constexpr int NW = kFusedWaves;
   constexpr int QPL = D / 16;              // q elements per lane (phase 1)
   constexpr int FPL = N / 64;              // features per lane (phase 2)
@@ -1215,7 +1316,7 @@ __global__ __launch_bounds__(512) void k_decode_fused(
   // phi(q) and the scores live only until the top-k; the merge reuses them
   __shared__ __attribute__((aligned(16))) float area[AREA];
   __shared__ int sel_lds[G * kMaxK];
-  __shared__ unsigned bits_lds[kBitmapWords];
+  __shared__ unsigned bits_lds[G * kBitmapWords];
   __shared__ int uni_lds[G * kMaxK];
   __shared__ unsigned hist_lds[G][256];
   __shared__ u64 list_lds[G][kMaxK];
@@ -1231,6 +1332,9 @@ __global__ __launch_bounds__(512) void k_decode_fused(
   const int64_t bh = blockIdx.x;
   const int64_t b = bh / Hkv, hk = bh % Hkv;
   const T* q0 = q + (b * Hq + hk * G) * D;
+  const Span sp = seq_span(sa, b);
+  const int c = sa.c, k = sa.k, n_cand = sp.n_cand, k_eff = sp.k_eff;
+  const int64_t ws = sp.ws, t = sp.t;
 
   if (n_cand > 0) {                        // uniform
     // ---- 1. phi(q) -----------------------------------------------------
@@ -1335,10 +1439,11 @@ __global__ __launch_bounds__(512) void k_decode_fused(
     __syncthreads();
   }
 
-  // ---- 3. top-k (waves < G) | window tiles (the other waves) -------------
+  // ---- 3. top-k (waves < G) | window and sink tiles (the other waves) ----
   TA ta;
   ta.init(q0, qscale, lane);
   const int win_tiles = (int)((t - ws + kTile - 1) / kTile);
+  const int extra_tiles = win_tiles + (sp.sink + kTile - 1) / kTile;
   if (wave < G) {
     const int64_t hq = hk * G + wave;
     int32_t* so = selected ? selected + (b * Hq + hq) * (int64_t)k : nullptr;
@@ -1354,23 +1459,34 @@ __global__ __launch_bounds__(512) void k_decode_fused(
     else if (npl <= 8) head_topk<8>(src, n_cand, k, k_eff, row, so, sco, lane, hist, list);
     else head_topk<16>(src, n_cand, k, k_eff, row, so, sco, lane, hist, list);
   } else {
-    for (int i = wave - G; i < win_tiles; i += NW - G) {
-      const int64_t start = ws + (int64_t)i * kTile;
-      ta.tile(K, V, bh * cap + start, (int)min((int64_t)kTile, t - start), lane);
+    for (int i = wave - G; i < extra_tiles; i += NW - G) {
+      int64_t start;
+      int len;
+      if (i < win_tiles) {
+        start = ws + (int64_t)i * kTile;
+        len = (int)min((int64_t)kTile, t - start);
+      } else {
+        const int off = (i - win_tiles) * kTile;
+        start = (int64_t)off - sa.n_sink;
+        len = min(kTile, sp.sink - off);
+      }
+      ta.tile(K, V, bh * cap + start, len, lane, kAllHeads);
     }
   }
   __syncthreads();
 
   // ---- 4. union -----------------------------------------------------------
-  group_union(sel_lds, bits_lds, G * k_eff, uni_lds, &ucnt_lds);
+  group_union(sel_lds, bits_lds, G, k_eff, per_head != 0, uni_lds, &ucnt_lds);
   __syncthreads();
   const int seg_tiles = ucnt_lds * tiles_per_seg;
 
   // ---- 5. segment tiles ---------------------------------------------------
   for (int i = wave; i < seg_tiles; i += NW) {
-    const int s = uni_lds[i / tiles_per_seg];
+    const int e = uni_lds[i / tiles_per_seg];
+    const int s = e & ((1 << kUniIdBits) - 1);
+    const unsigned hm = per_head ? (unsigned)e >> kUniIdBits : kAllHeads;
     const int off = (i % tiles_per_seg) * kTile;
-    ta.tile(K, V, bh * cap + (int64_t)s * c + off, min(kTile, c - off), lane);
+    ta.tile(K, V, bh * cap + (int64_t)s * c + off, min(kTile, c - off), lane, hm);
   }
 
   // ---- 6. merge -----------------------------------------------------------
@@ -1401,7 +1517,8 @@ __global__ __launch_bounds__(512) void k_decode_fused(
       a = fmaf(wacc[(w * G + g) * D + e], f, a);
       L = fmaf(wl[w][g], f, L);
     }
-    out[(b * Hq + hk * G + g) * D + e] = from_f32<T>(a / L);
+    const float o = !sp.ok ? __uint_as_float(0x7fc00000u) : (L > 0.f ? a / L : 0.f);
+    out[(b * Hq + hk * G + g) * D + e] = from_f32<T>(o);
   }
 }
 
@@ -1417,7 +1534,7 @@ template <typename T, int D>
 __global__ __launch_bounds__(kCombineThreads) void k_combine(
     const float* __restrict__ part, const int* __restrict__ ucnt,
     T* __restrict__ out, int Hq, int Hkv, int G, int tiles_per_seg,
-    int win_tiles, int maxwg, int tpw) {
+    SeqArgs sa, int maxwg, int tpw) {
   constexpr int PSTRIDE = D + 4;
   constexpr int NT = kCombineThreads;
   constexpr int NWAVE = NT / kWave;
@@ -1431,9 +1548,13 @@ __global__ __launch_bounds__(kCombineThreads) void k_combine(
   const int64_t hk = hq / G;
   const int g = (int)(hq % G);
   const int64_t bh = b * Hkv + hk;
-  const int nwg = (ucnt[bh] * tiles_per_seg + win_tiles + 4 * tpw - 1) / (4 * tpw);
-  if (nwg == 0) {                          // nothing attended (given ids only)
-    if (tid < D) out[bhq * D + tid] = from_f32<T>(0.f);
+  const Span sp = seq_span(sa, b);
+  const int extra = (int)(((int64_t)sp.t - sp.ws + kTile - 1) / kTile) +
+                    (sp.sink + kTile - 1) / kTile;
+  const int nwg = (ucnt[bh] * tiles_per_seg + extra + 4 * tpw - 1) / (4 * tpw);
+  if (!sp.ok || nwg == 0) {                // invalid length / nothing attended
+    if (tid < D)
+      out[bhq * D + tid] = from_f32<T>(sp.ok ? 0.f : __uint_as_float(0x7fc00000u));
     return;
   }
   const float* pb = part + ((bh * maxwg) * G + g) * (int64_t)PSTRIDE;
@@ -1447,6 +1568,10 @@ __global__ __launch_bounds__(kCombineThreads) void k_combine(
   float M = red_lds[0];
 #pragma unroll
   for (int i = 1; i < NWAVE; ++i) M = fmaxf(M, red_lds[i]);
+  if (M == -INFINITY) {                    // this head attended nothing
+    if (tid < D) out[bhq * D + tid] = from_f32<T>(0.f);
+    return;
+  }
   float ls = 0.f;
   for (int w = tid; w < nwg; w += NT) {
     const float f = fast_exp2(pb[w * wstride] - M);
@@ -1506,7 +1631,7 @@ void launch(int kind, F kern, dim3 grid, dim3 block, size_t shm, hipStream_t st,
 }
 
 struct Shape {
-  int B, Hq, Hkv, G, d, n, c, w;
+  int B, Hq, Hkv, G, d, n, c, w, n_sink, per_head;
   int64_t cap, s_cap;
   radar_dtype dt;
 };
@@ -1520,6 +1645,9 @@ radar_status check_cfg(const radar_config* cfg, Shape* s) {
       cfg->n_q_heads % cfg->n_kv_heads != 0)
     return RADAR_EINVAL;
   if (cfg->kv_dtype != RADAR_F32 && cfg->kv_dtype != RADAR_BF16) return RADAR_EINVAL;
+  if (cfg->n_sink < 0 || cfg->n_sink > cfg->capacity) return RADAR_EINVAL;
+  if (cfg->gqa_mode != RADAR_GQA_UNION && cfg->gqa_mode != RADAR_GQA_PER_HEAD)
+    return RADAR_EINVAL;
   const int G = cfg->n_q_heads / cfg->n_kv_heads;
   if (G != 1 && G != 2 && G != 4 && G != 8) return RADAR_EUNSUPPORTED;
   if (cfg->head_dim != 64 && cfg->head_dim != 128) return RADAR_EUNSUPPORTED;
@@ -1531,7 +1659,8 @@ radar_status check_cfg(const radar_config* cfg, Shape* s) {
   s->B = cfg->batch; s->Hq = cfg->n_q_heads; s->Hkv = cfg->n_kv_heads; s->G = G;
   s->d = cfg->head_dim; s->n = n; s->c = cfg->seg_len; s->w = cfg->window;
   s->cap = cfg->capacity; s->s_cap = cfg->capacity / cfg->seg_len;
-  s->dt = cfg->kv_dtype;
+  s->dt = cfg->kv_dtype; s->n_sink = cfg->n_sink;
+  s->per_head = cfg->gqa_mode == RADAR_GQA_PER_HEAD;
   return RADAR_OK;
 }
 
@@ -1548,7 +1677,8 @@ WsLayout ws_layout(const Shape& s, int k) {
   L.tiles_per_seg = (int)ceil_div(s.c, kTile);
   L.umax = (int)std::max<int64_t>(1, std::min<int64_t>((int64_t)s.G * k, s.s_cap));
   const int64_t wmax = std::min<int64_t>(s.cap, (int64_t)s.w + s.c);
-  const int64_t wt = ceil_div(wmax, kTile);
+  const int64_t wt = ceil_div(wmax, kTile) +
+                     ceil_div(std::min<int64_t>(s.n_sink, s.cap), kTile);
   L.maxwg = (int)ceil_div((int64_t)L.umax * L.tiles_per_seg + wt, 4);
   const size_t bh = (size_t)s.B * s.Hkv;
   size_t off = 0;
@@ -1585,7 +1715,7 @@ int num_cu() {
 template <typename T, int D, int FT>
 radar_status launch_build_t(const Shape& s, const void* K, const float* omega,
                             float* summ, int seg_first, int seg_count,
-                            hipStream_t st) {
+                            const int64_t* pos, hipStream_t st) {
   const int slices = s.n / (64 * FT);
   const int64_t items = (int64_t)s.B * s.Hkv * seg_count;
   if (items == 0) return RADAR_OK;
@@ -1602,37 +1732,50 @@ radar_status launch_build_t(const Shape& s, const void* K, const float* omega,
   const float out_scale = 1.f / ((float)s.c * std::sqrt((float)s.n));
   launch(RADAR_K_BUILD, kern, dim3((unsigned)gx, (unsigned)slices), dim3(256), 0, st,
                      reinterpret_cast<const T*>(K), omega, summ, s.n, s.c, s.cap,
-                     s.s_cap, seg_first, seg_count, items, s1, s2, out_scale, s.cap);
+                     s.s_cap, seg_first, seg_count, items, s1, s2, out_scale, s.cap,
+                     pos, s.Hkv, s.n_sink);
   return launch_status();
 }
 
 template <typename T, int D>
 radar_status launch_build_d(const Shape& s, const void* K, const float* omega,
                             float* summ, int seg_first, int seg_count,
-                            hipStream_t st) {
+                            const int64_t* pos, hipStream_t st) {
   // features per workgroup = 64 * FT; FT capped so the resident Omega slice
   // stays at 128 VGPRs or fewer
   constexpr int FTMAX = (D * sizeof(T) <= 256) ? 8 : 4;
   const int ft = std::min(s.n / 64, FTMAX);
   switch (ft) {
-    case 1: return launch_build_t<T, D, 1>(s, K, omega, summ, seg_first, seg_count, st);
-    case 2: return launch_build_t<T, D, 2>(s, K, omega, summ, seg_first, seg_count, st);
-    case 4: return launch_build_t<T, D, 4>(s, K, omega, summ, seg_first, seg_count, st);
+    case 1: return launch_build_t<T, D, 1>(s, K, omega, summ, seg_first, seg_count, pos, st);
+    case 2: return launch_build_t<T, D, 2>(s, K, omega, summ, seg_first, seg_count, pos, st);
+    case 4: return launch_build_t<T, D, 4>(s, K, omega, summ, seg_first, seg_count, pos, st);
     default:
       if constexpr (FTMAX >= 8)
-        return launch_build_t<T, D, 8>(s, K, omega, summ, seg_first, seg_count, st);
+        return launch_build_t<T, D, 8>(s, K, omega, summ, seg_first, seg_count, pos, st);
       return RADAR_EUNSUPPORTED;
   }
 }
 
+// K: the first row after the sinks (after_sinks); pos: per-sequence segment
+// closes (seg_first / seg_count then 0 / 1)
 radar_status launch_build(const Shape& s, const void* K, const float* omega,
                           float* summ, int seg_first, int seg_count,
-                          hipStream_t st) {
+                          const int64_t* pos, hipStream_t st) {
   if (s.dt == RADAR_BF16)
-    return s.d == 64 ? launch_build_d<bf16_t, 64>(s, K, omega, summ, seg_first, seg_count, st)
-                     : launch_build_d<bf16_t, 128>(s, K, omega, summ, seg_first, seg_count, st);
-  return s.d == 64 ? launch_build_d<float, 64>(s, K, omega, summ, seg_first, seg_count, st)
-                   : launch_build_d<float, 128>(s, K, omega, summ, seg_first, seg_count, st);
+    return s.d == 64 ? launch_build_d<bf16_t, 64>(s, K, omega, summ, seg_first, seg_count, pos, st)
+                     : launch_build_d<bf16_t, 128>(s, K, omega, summ, seg_first, seg_count, pos, st);
+  return s.d == 64 ? launch_build_d<float, 64>(s, K, omega, summ, seg_first, seg_count, pos, st)
+                   : launch_build_d<float, 128>(s, K, omega, summ, seg_first, seg_count, pos, st);
+}
+
+// K / V rows after the n_sink sink rows of the first (b, kv head): the
+// kernels address segments and the window from there
+template <typename P>
+P* after_sinks(const Shape& s, P* p) {
+  const size_t esz = s.dt == RADAR_BF16 ? 2 : 4;
+  using B = typename std::conditional<std::is_const<P>::value, const unsigned char,
+                                      unsigned char>::type;
+  return reinterpret_cast<P*>(reinterpret_cast<B*>(p) + (size_t)s.n_sink * s.d * esz);
 }
 
 // ---- decode pieces -------------------------------------------------------
@@ -1646,67 +1789,79 @@ void launch_phi_q(const Shape& s, const void* q, const float* omega, float* phiq
          1.f / std::sqrt((float)s.n));
 }
 
+// n_cand: the largest candidate count of the call (grid size); each
+// workgroup reads its sequence's own from sa
 template <int N, int G>
 void launch_score_ng(const Shape& s, const float* phiq, const float* summ,
-                     float* scores, int n_cand, hipStream_t st) {
+                     float* scores, int n_cand, const SeqArgs& sa, hipStream_t st) {
   constexpr int rows_per_wg = 64 * (N <= 256 ? 2 : 1);
   const dim3 grid((unsigned)ceil_div(n_cand, rows_per_wg), (unsigned)(s.B * s.Hkv));
   const int nc_cap = (int)std::max<int64_t>(1, s.s_cap);
   launch(RADAR_K_SCORE, k_score<N, G>, grid, dim3(256), 0, st, phiq, summ, scores,
-         s.Hq, s.Hkv, n_cand, s.s_cap, nc_cap);
+         s.Hq, s.Hkv, sa, s.s_cap, nc_cap);
 }
 
 template <int N>
 void launch_score_n(const Shape& s, const float* phiq, const float* summ,
-                    float* scores, int n_cand, hipStream_t st) {
+                    float* scores, int n_cand, const SeqArgs& sa, hipStream_t st) {
   switch (s.G) {
-    case 1: launch_score_ng<N, 1>(s, phiq, summ, scores, n_cand, st); break;
-    case 2: launch_score_ng<N, 2>(s, phiq, summ, scores, n_cand, st); break;
-    case 4: launch_score_ng<N, 4>(s, phiq, summ, scores, n_cand, st); break;
-    default: launch_score_ng<N, 8>(s, phiq, summ, scores, n_cand, st); break;
+    case 1: launch_score_ng<N, 1>(s, phiq, summ, scores, n_cand, sa, st); break;
+    case 2: launch_score_ng<N, 2>(s, phiq, summ, scores, n_cand, sa, st); break;
+    case 4: launch_score_ng<N, 4>(s, phiq, summ, scores, n_cand, sa, st); break;
+    default: launch_score_ng<N, 8>(s, phiq, summ, scores, n_cand, sa, st); break;
   }
 }
 
 void launch_score(const Shape& s, const float* phiq, const float* summ,
-                  float* scores, int n_cand, hipStream_t st) {
+                  float* scores, int n_cand, const SeqArgs& sa, hipStream_t st) {
   switch (s.n) {
-    case 64: launch_score_n<64>(s, phiq, summ, scores, n_cand, st); break;
-    case 128: launch_score_n<128>(s, phiq, summ, scores, n_cand, st); break;
-    case 256: launch_score_n<256>(s, phiq, summ, scores, n_cand, st); break;
-    default: launch_score_n<512>(s, phiq, summ, scores, n_cand, st); break;
+    case 64: launch_score_n<64>(s, phiq, summ, scores, n_cand, sa, st); break;
+    case 128: launch_score_n<128>(s, phiq, summ, scores, n_cand, sa, st); break;
+    case 256: launch_score_n<256>(s, phiq, summ, scores, n_cand, sa, st); break;
+    default: launch_score_n<512>(s, phiq, summ, scores, n_cand, sa, st); break;
   }
 }
 
 template <typename T, int D, int G>
 void launch_attend_g(const Shape& s, const void* q, const void* K, const void* V,
                      unsigned char* w, const WsLayout& L, int grid_x, int tpw,
-                     int64_t ws, int64_t t, hipStream_t st) {
+                     const SeqArgs& sa, hipStream_t st) {
   const float qscale = kLog2e / std::sqrt((float)s.d);
   launch(RADAR_K_ATTEND, k_attend<T, D, G>,
          dim3((unsigned)grid_x, (unsigned)(s.B * s.Hkv)), dim3(256), 0, st,
          reinterpret_cast<const T*>(q), reinterpret_cast<const T*>(K),
          reinterpret_cast<const T*>(V), reinterpret_cast<const int*>(w + L.uni),
          reinterpret_cast<const int*>(w + L.ucnt), reinterpret_cast<float*>(w + L.part),
-         s.Hq, s.Hkv, s.cap, s.c, L.tiles_per_seg, ws, t, L.umax, L.maxwg, tpw,
+         s.Hq, s.Hkv, s.cap, L.tiles_per_seg, sa, s.per_head, L.umax, L.maxwg, tpw,
          qscale);
 }
 
 template <typename T, int D>
 void launch_attend_d(const Shape& s, const void* q, const void* K, const void* V,
                      unsigned char* w, const WsLayout& L, int grid_x, int tpw,
-                     int64_t ws, int64_t t, void* out, hipStream_t st) {
+                     const SeqArgs& sa, void* out, hipStream_t st) {
   switch (s.G) {
-    case 1: launch_attend_g<T, D, 1>(s, q, K, V, w, L, grid_x, tpw, ws, t, st); break;
-    case 2: launch_attend_g<T, D, 2>(s, q, K, V, w, L, grid_x, tpw, ws, t, st); break;
-    case 4: launch_attend_g<T, D, 4>(s, q, K, V, w, L, grid_x, tpw, ws, t, st); break;
-    default: launch_attend_g<T, D, 8>(s, q, K, V, w, L, grid_x, tpw, ws, t, st); break;
+    case 1: launch_attend_g<T, D, 1>(s, q, K, V, w, L, grid_x, tpw, sa, st); break;
+    case 2: launch_attend_g<T, D, 2>(s, q, K, V, w, L, grid_x, tpw, sa, st); break;
+    case 4: launch_attend_g<T, D, 4>(s, q, K, V, w, L, grid_x, tpw, sa, st); break;
+    default: launch_attend_g<T, D, 8>(s, q, K, V, w, L, grid_x, tpw, sa, st); break;
   }
-  const int win_tiles = (int)ceil_div(t - ws, kTile);
   launch(RADAR_K_COMBINE, k_combine<T, D>, dim3((unsigned)(s.B * s.Hq)),
          dim3(kCombineThreads), 0,
          st, reinterpret_cast<const float*>(w + L.part),
          reinterpret_cast<const int*>(w + L.ucnt), reinterpret_cast<T*>(out), s.Hq,
-         s.Hkv, s.G, L.tiles_per_seg, win_tiles, L.maxwg, tpw);
+         s.Hkv, s.G, L.tiles_per_seg, sa, L.maxwg, tpw);
+}
+
+// Tiles beyond the union's segments per (b, kv head), the window's and the
+// sinks': exact for one shared length, an upper bound over lengths in
+// [1, t_max] for per-sequence lengths (a window never exceeds w + c - 1
+// tokens nor the tokens after the sinks).
+int64_t extra_tiles(const Shape& s, const SeqArgs& sa) {
+  const Span sp = make_span(sa.t_max, sa);
+  const int64_t win = sa.lens ? std::min<int64_t>(sp.t, (int64_t)s.w + s.c - 1)
+                              : sp.t - sp.ws;
+  return ceil_div(win, kTile) + ceil_div(sp.sink, kTile);
 }
 
 // Split of the attention work: tiles per wave (tpw) so that the grid still
@@ -1718,25 +1873,26 @@ struct AttendGrid {
   int grid_x, tpw;
 };
 
-AttendGrid attend_grid(const Shape& s, const WsLayout& L, int u_bound, int64_t ws,
-                       int64_t t) {
-  const int64_t per_bh = (int64_t)u_bound * L.tiles_per_seg + ceil_div(t - ws, kTile);
+AttendGrid attend_grid(const Shape& s, const WsLayout& L, int u_bound,
+                       int64_t extra) {
+  const int64_t per_bh = (int64_t)u_bound * L.tiles_per_seg + extra;
   const int64_t tiles = per_bh * s.B * s.Hkv;
   const int64_t tpw = std::min<int64_t>(8, std::max<int64_t>(1, tiles / (4 * 8 * num_cu())));
   return {(int)ceil_div(per_bh, 4 * tpw), (int)tpw};
 }
 
-// exact attention over the union in the workspace, then the merge
+// exact attention over the union in the workspace, then the merge; K and V
+// start after the sinks
 radar_status launch_attend(const Shape& s, const void* q, const void* K,
-                           const void* V, const AttendGrid& ag, int64_t ws, int64_t t,
+                           const void* V, const AttendGrid& ag, const SeqArgs& sa,
                            void* out, unsigned char* w, const WsLayout& L,
                            hipStream_t st) {
   if (s.dt == RADAR_BF16) {
-    if (s.d == 64) launch_attend_d<bf16_t, 64>(s, q, K, V, w, L, ag.grid_x, ag.tpw, ws, t, out, st);
-    else launch_attend_d<bf16_t, 128>(s, q, K, V, w, L, ag.grid_x, ag.tpw, ws, t, out, st);
+    if (s.d == 64) launch_attend_d<bf16_t, 64>(s, q, K, V, w, L, ag.grid_x, ag.tpw, sa, out, st);
+    else launch_attend_d<bf16_t, 128>(s, q, K, V, w, L, ag.grid_x, ag.tpw, sa, out, st);
   } else {
-    if (s.d == 64) launch_attend_d<float, 64>(s, q, K, V, w, L, ag.grid_x, ag.tpw, ws, t, out, st);
-    else launch_attend_d<float, 128>(s, q, K, V, w, L, ag.grid_x, ag.tpw, ws, t, out, st);
+    if (s.d == 64) launch_attend_d<float, 64>(s, q, K, V, w, L, ag.grid_x, ag.tpw, sa, out, st);
+    else launch_attend_d<float, 128>(s, q, K, V, w, L, ag.grid_x, ag.tpw, sa, out, st);
   }
   return launch_status();
 }
@@ -1744,17 +1900,17 @@ radar_status launch_attend(const Shape& s, const void* q, const void* K,
 // ---- exact segment search ---------------------------------------------------
 template <typename T, int D>
 void launch_segment_mass_d(const Shape& s, const void* q, const void* K, float* scores,
-                           int n_cand, hipStream_t st) {
+                           int n_cand, const SeqArgs& sa, hipStream_t st) {
   const dim3 grid((unsigned)ceil_div(n_cand, 4), (unsigned)(s.B * s.Hkv));
   const int nc_cap = (int)std::max<int64_t>(1, s.s_cap);
   const float qscale = kLog2e / std::sqrt((float)s.d);
   const T* qt = reinterpret_cast<const T*>(q);
   const T* Kt = reinterpret_cast<const T*>(K);
   switch (s.G) {
-    case 1: launch(RADAR_K_SCORE, k_segment_mass<T, D, 1>, grid, dim3(256), 0, st, qt, Kt, scores, s.Hq, s.Hkv, s.cap, s.c, n_cand, nc_cap, qscale); break;
-    case 2: launch(RADAR_K_SCORE, k_segment_mass<T, D, 2>, grid, dim3(256), 0, st, qt, Kt, scores, s.Hq, s.Hkv, s.cap, s.c, n_cand, nc_cap, qscale); break;
-    case 4: launch(RADAR_K_SCORE, k_segment_mass<T, D, 4>, grid, dim3(256), 0, st, qt, Kt, scores, s.Hq, s.Hkv, s.cap, s.c, n_cand, nc_cap, qscale); break;
-    default: launch(RADAR_K_SCORE, k_segment_mass<T, D, 8>, grid, dim3(256), 0, st, qt, Kt, scores, s.Hq, s.Hkv, s.cap, s.c, n_cand, nc_cap, qscale); break;
+    case 1: launch(RADAR_K_SCORE, k_segment_mass<T, D, 1>, grid, dim3(256), 0, st, qt, Kt, scores, s.Hq, s.Hkv, s.cap, sa, nc_cap, qscale); break;
+    case 2: launch(RADAR_K_SCORE, k_segment_mass<T, D, 2>, grid, dim3(256), 0, st, qt, Kt, scores, s.Hq, s.Hkv, s.cap, sa, nc_cap, qscale); break;
+    case 4: launch(RADAR_K_SCORE, k_segment_mass<T, D, 4>, grid, dim3(256), 0, st, qt, Kt, scores, s.Hq, s.Hkv, s.cap, sa, nc_cap, qscale); break;
+    default: launch(RADAR_K_SCORE, k_segment_mass<T, D, 8>, grid, dim3(256), 0, st, qt, Kt, scores, s.Hq, s.Hkv, s.cap, sa, nc_cap, qscale); break;
   }
 }
 
@@ -1764,8 +1920,7 @@ thread_local int g_path_override = RADAR_PATH_AUTO;
 template <typename T, int D, int G, int N>
 radar_status launch_fused_n(const Shape& s, const void* q, const void* K,
                             const void* V, const float* omega,
-                            const float* summ, int64_t ws, int64_t t,
-                            int n_cand, int k, int k_eff, void* out,
+                            const float* summ, const SeqArgs& sa, void* out,
                             int32_t* selected, float* sel_scores,
                             hipStream_t st) {
   const float s1 = kLog2e / std::pow((float)s.d, 0.25f);
@@ -1774,7 +1929,7 @@ radar_status launch_fused_n(const Shape& s, const void* q, const void* K,
          dim3(kFusedWaves * 64), 0, st, reinterpret_cast<const T*>(q),
          reinterpret_cast<const T*>(K), reinterpret_cast<const T*>(V), omega, summ,
          reinterpret_cast<T*>(out), selected, sel_scores, s.Hq, s.Hkv, s.cap,
-         s.s_cap, s.c, (int)ceil_div(s.c, kTile), ws, t, n_cand, k, k_eff, s1, s2,
+         s.s_cap, (int)ceil_div(s.c, kTile), sa, s.per_head, s1, s2,
          1.f / std::sqrt((float)s.n), kLog2e / std::sqrt((float)s.d));
   return launch_status();
 }
@@ -1782,76 +1937,86 @@ radar_status launch_fused_n(const Shape& s, const void* q, const void* K,
 template <typename T, int D, int G>
 radar_status launch_fused_g(const Shape& s, const void* q, const void* K,
                             const void* V, const float* omega,
-                            const float* summ, int64_t ws, int64_t t,
-                            int n_cand, int k, int k_eff, void* out,
+                            const float* summ, const SeqArgs& sa, void* out,
                             int32_t* selected, float* sel_scores,
                             hipStream_t st) {
   switch (s.n) {
-    case 64: return launch_fused_n<T, D, G, 64>(s, q, K, V, omega, summ, ws, t, n_cand, k, k_eff, out, selected, sel_scores, st);
-    case 128: return launch_fused_n<T, D, G, 128>(s, q, K, V, omega, summ, ws, t, n_cand, k, k_eff, out, selected, sel_scores, st);
-    case 256: return launch_fused_n<T, D, G, 256>(s, q, K, V, omega, summ, ws, t, n_cand, k, k_eff, out, selected, sel_scores, st);
-    default: return launch_fused_n<T, D, G, 512>(s, q, K, V, omega, summ, ws, t, n_cand, k, k_eff, out, selected, sel_scores, st);
+    case 64: return launch_fused_n<T, D, G, 64>(s, q, K, V, omega, summ, sa, out, selected, sel_scores, st);
+    case 128: return launch_fused_n<T, D, G, 128>(s, q, K, V, omega, summ, sa, out, selected, sel_scores, st);
+    case 256: return launch_fused_n<T, D, G, 256>(s, q, K, V, omega, summ, sa, out, selected, sel_scores, st);
+    default: return launch_fused_n<T, D, G, 512>(s, q, K, V, omega, summ, sa, out, selected, sel_scores, st);
   }
 }
 
 template <typename T, int D>
 radar_status launch_fused_d(const Shape& s, const void* q, const void* K,
                             const void* V, const float* omega,
-                            const float* summ, int64_t ws, int64_t t,
-                            int n_cand, int k, int k_eff, void* out,
+                            const float* summ, const SeqArgs& sa, void* out,
                             int32_t* selected, float* sel_scores,
                             hipStream_t st) {
   switch (s.G) {
-    case 1: return launch_fused_g<T, D, 1>(s, q, K, V, omega, summ, ws, t, n_cand, k, k_eff, out, selected, sel_scores, st);
-    case 2: return launch_fused_g<T, D, 2>(s, q, K, V, omega, summ, ws, t, n_cand, k, k_eff, out, selected, sel_scores, st);
-    default: return launch_fused_g<T, D, 4>(s, q, K, V, omega, summ, ws, t, n_cand, k, k_eff, out, selected, sel_scores, st);
+    case 1: return launch_fused_g<T, D, 1>(s, q, K, V, omega, summ, sa, out, selected, sel_scores, st);
+    case 2: return launch_fused_g<T, D, 2>(s, q, K, V, omega, summ, sa, out, selected, sel_scores, st);
+    default: return launch_fused_g<T, D, 4>(s, q, K, V, omega, summ, sa, out, selected, sel_scores, st);
   }
 }
 
+// K and V start after the sinks
 radar_status launch_fused(const Shape& s, const void* q, const void* K, const void* V,
-                          const float* omega, const float* summ, int64_t ws,
-                          int64_t t, int n_cand, int k, int k_eff, void* out,
-                          int32_t* selected, float* sel_scores, hipStream_t st) {
+                          const float* omega, const float* summ, const SeqArgs& sa,
+                          void* out, int32_t* selected, float* sel_scores,
+                          hipStream_t st) {
   if (s.dt == RADAR_BF16)
-    return s.d == 64 ? launch_fused_d<bf16_t, 64>(s, q, K, V, omega, summ, ws, t, n_cand, k, k_eff, out, selected, sel_scores, st)
-                     : launch_fused_d<bf16_t, 128>(s, q, K, V, omega, summ, ws, t, n_cand, k, k_eff, out, selected, sel_scores, st);
+    return s.d == 64 ? launch_fused_d<bf16_t, 64>(s, q, K, V, omega, summ, sa, out, selected, sel_scores, st)
+                     : launch_fused_d<bf16_t, 128>(s, q, K, V, omega, summ, sa, out, selected, sel_scores, st);
   // fp32 caches with d = 128 keep the split path: their tiles need more
   // registers than the fused kernel has to spare
   if (s.d == 64)
-    return launch_fused_d<float, 64>(s, q, K, V, omega, summ, ws, t, n_cand, k, k_eff, out, selected, sel_scores, st);
+    return launch_fused_d<float, 64>(s, q, K, V, omega, summ, sa, out, selected, sel_scores, st);
   return RADAR_EUNSUPPORTED;
 }
 
-// Which decode path a call takes: the fused one-workgroup-per-(b, kv head)
-// kernel when there are enough pairs to occupy every CU (or when forced),
-// and the shape fits its LDS plan; the split multi-kernel path otherwise.
-// A pair's HBM bytes in one decode step (summary rows plus the K/V of the
-// largest union and the window), the quantity one fused workgroup streams.
-int64_t pair_bytes(const Shape& s, int64_t t, int k) {
-  const int64_t past = std::max<int64_t>(0, t - s.w);
-  const int64_t ws = (int64_t)s.c * (past / s.c), n_cand = ws / s.c;
-  const int64_t u = std::min<int64_t>((int64_t)s.G * std::min<int64_t>(k, n_cand), n_cand);
+// A pair's HBM bytes in one decode step at length t (summary rows plus the
+// K/V of the largest union, the window and the sinks), the quantity one
+// fused workgroup streams.
+int64_t pair_bytes(const Shape& s, const SeqArgs& sa) {
+  const Span sp = make_span(sa.t_max, sa);
+  const int64_t u = std::min<int64_t>((int64_t)s.G * sp.k_eff, sp.n_cand);
   const int64_t skv = s.dt == RADAR_BF16 ? 2 : 4;
-  return n_cand * s.n * 4 + (u * s.c + (t - ws)) * 2 * s.d * skv;
+  return (int64_t)sp.n_cand * s.n * 4 +
+         (u * s.c + (sp.t - sp.ws) + sp.sink) * 2 * s.d * skv;
 }
 
 // Which decode path a call takes. Fused when the shape fits its LDS plan and
 // either there are enough (b, kv head) pairs to occupy every CU, or each
 // pair's step is small enough (<= 256 KB) that one workgroup streams it in a
 // few microseconds, less than the split path's extra launches cost.
-int choose_path(const Shape& s, int64_t t, int n_cand, int k) {
+int choose_path(const Shape& s, const SeqArgs& sa) {
+  const int n_cand = make_span(sa.t_max, sa).n_cand;
   const bool fits = s.G <= kFusedMaxG && n_cand <= kFusedMaxCand &&
                     !(s.dt == RADAR_F32 && s.d == 128);
   if (!fits || g_path_override == RADAR_PATH_SPLIT) return RADAR_PATH_SPLIT;
   if (g_path_override == RADAR_PATH_FUSED) return RADAR_PATH_FUSED;
   if ((int64_t)s.B * s.Hkv >= num_cu()) return RADAR_PATH_FUSED;
-  return pair_bytes(s, t, k) <= (256 << 10) ? RADAR_PATH_FUSED : RADAR_PATH_SPLIT;
+  return pair_bytes(s, sa) <= (256 << 10) ? RADAR_PATH_FUSED : RADAR_PATH_SPLIT;
 }
 
-void window_split(const Shape& s, int64_t t, int64_t* ws, int* n_cand) {
-  const int64_t past = std::max<int64_t>(0, t - s.w);
-  *ws = (int64_t)s.c * (past / s.c);
-  *n_cand = (int)(*ws / s.c);
+// Argument checks shared by the decode-side calls: pointers, k, the length
+// bound t and the workspace. Fills the per-call sequence arguments.
+radar_status check_decode(const radar_config* cfg, Shape* s, int64_t t,
+                          const int64_t* lens, int32_t k, void* workspace,
+                          size_t workspace_bytes, WsLayout* L, SeqArgs* sa) {
+  radar_status r = check_cfg(cfg, s);
+  if (r != RADAR_OK) return r;
+  if (lens && !aligned16(lens)) return RADAR_EINVAL;
+  if (k < 1 || k > kMaxK) return RADAR_EUNSUPPORTED;
+  if (t < 1 || t > s->cap) return RADAR_ECAPACITY;
+  *L = ws_layout(*s, k);
+  if (!workspace || !aligned16(workspace)) return RADAR_EWORKSPACE;
+  if (workspace_bytes < L->total) return RADAR_EWORKSPACE;
+  *sa = SeqArgs{lens, t, s->c, s->w, s->n_sink, k};
+  if (make_span(t, *sa).n_cand > kMaxCand) return RADAR_EUNSUPPORTED;
+  return RADAR_OK;
 }
 
 }  // namespace
@@ -1885,10 +2050,7 @@ int32_t radar_decode_path(const radar_config* cfg, int64_t t, int32_t k) {
   Shape s;
   if (check_cfg(cfg, &s) != RADAR_OK || k < 1 || k > kMaxK || t < 1 || t > s.cap)
     return -1;
-  int64_t ws;
-  int n_cand;
-  window_split(s, t, &ws, &n_cand);
-  return choose_path(s, t, n_cand, k);
+  return choose_path(s, SeqArgs{nullptr, t, s.c, s.w, s.n_sink, k});
 }
 
 radar_status radar_profile_enable(int32_t on) {
@@ -1947,85 +2109,83 @@ radar_status radar_build_index(const radar_config* cfg, const void* K,
   if (!K || !omega || !summaries) return RADAR_EINVAL;
   if (!aligned16(K) || !aligned16(omega) || !aligned16(summaries)) return RADAR_EINVAL;
   if (t < 1 || t > s.cap) return RADAR_ECAPACITY;
-  const int64_t n_seg = t / s.c;
+  const int64_t n_seg = std::max<int64_t>(0, t - s.n_sink) / s.c;
   if (n_seg == 0) return RADAR_OK;
-  return launch_build(s, K, omega, summaries, 0, (int)n_seg, stream);
+  return launch_build(s, after_sinks(s, K), omega, summaries, 0, (int)n_seg,
+                      nullptr, stream);
 }
 
 radar_status radar_append(const radar_config* cfg, void* K, void* V,
                           const void* k_new, const void* v_new,
-                          const float* omega, int64_t t, float* summaries,
-                          hipStream_t stream) {
+                          const float* omega, int64_t t, const int64_t* pos,
+                          float* summaries, hipStream_t stream) {
   Shape s;
   radar_status r = check_cfg(cfg, &s);
   if (r != RADAR_OK) return r;
   if (!K || !V || !k_new || !v_new || !omega || !summaries) return RADAR_EINVAL;
   if (!aligned16(K) || !aligned16(V) || !aligned16(k_new) || !aligned16(v_new) ||
-      !aligned16(omega) || !aligned16(summaries))
+      !aligned16(omega) || !aligned16(summaries) || (pos && !aligned16(pos)))
     return RADAR_EINVAL;
-  if (t < 0 || t >= s.cap) return RADAR_ECAPACITY;
+  if (!pos && (t < 0 || t >= s.cap)) return RADAR_ECAPACITY;
   const unsigned grid = (unsigned)(s.B * s.Hkv);
   if (s.dt == RADAR_BF16) {
     if (s.d == 64)
       launch(RADAR_K_APPEND, k_append<bf16_t, 64>, dim3(grid), dim3(64), 0, stream,
-                         (bf16_t*)K, (bf16_t*)V, (const bf16_t*)k_new, (const bf16_t*)v_new, s.cap, t);
+             (bf16_t*)K, (bf16_t*)V, (const bf16_t*)k_new, (const bf16_t*)v_new, s.cap, t, pos, s.Hkv);
     else
       launch(RADAR_K_APPEND, k_append<bf16_t, 128>, dim3(grid), dim3(64), 0, stream,
-                         (bf16_t*)K, (bf16_t*)V, (const bf16_t*)k_new, (const bf16_t*)v_new, s.cap, t);
+             (bf16_t*)K, (bf16_t*)V, (const bf16_t*)k_new, (const bf16_t*)v_new, s.cap, t, pos, s.Hkv);
   } else {
     if (s.d == 64)
       launch(RADAR_K_APPEND, k_append<float, 64>, dim3(grid), dim3(64), 0, stream,
-                         (float*)K, (float*)V, (const float*)k_new, (const float*)v_new, s.cap, t);
+             (float*)K, (float*)V, (const float*)k_new, (const float*)v_new, s.cap, t, pos, s.Hkv);
     else
       launch(RADAR_K_APPEND, k_append<float, 128>, dim3(grid), dim3(64), 0, stream,
-                         (float*)K, (float*)V, (const float*)k_new, (const float*)v_new, s.cap, t);
+             (float*)K, (float*)V, (const float*)k_new, (const float*)v_new, s.cap, t, pos, s.Hkv);
   }
   r = launch_status();
   if (r != RADAR_OK) return r;
-  if ((t + 1) % s.c == 0) {
-    const int seg = (int)((t + 1) / s.c - 1);
-    return launch_build(s, K, omega, summaries, seg, 1, stream);
-  }
+  const void* Kp = after_sinks(s, static_cast<const void*>(K));
+  if (pos) return launch_build(s, Kp, omega, summaries, 0, 1, pos, stream);
+  const int64_t row = t - s.n_sink;          // row after the sinks
+  if (row >= 0 && (row + 1) % s.c == 0)
+    return launch_build(s, Kp, omega, summaries, (int)((row + 1) / s.c - 1), 1,
+                        nullptr, stream);
   return RADAR_OK;
 }
 
 radar_status radar_decode(const radar_config* cfg, const void* q, const void* K,
                           const void* V, const float* omega,
-                          const float* summaries, int64_t t, int32_t k,
-                          void* out, int32_t* selected, float* scores,
+                          const float* summaries, int64_t t, const int64_t* lens,
+                          int32_t k, void* out, int32_t* selected, float* scores,
                           void* workspace, size_t workspace_bytes,
                           hipStream_t stream) {
-  Shape s;
-  radar_status r = check_cfg(cfg, &s);
-  if (r != RADAR_OK) return r;
-  if (!q || !K || !V || !omega || !summaries || !out) return RADAR_EINVAL;
+  if (!cfg || !q || !K || !V || !omega || !summaries || !out) return RADAR_EINVAL;
   if (!aligned16(q) || !aligned16(K) || !aligned16(V) || !aligned16(omega) ||
       !aligned16(summaries) || !aligned16(out) ||
       (selected && !aligned16(selected)) || (scores && !aligned16(scores)))
     return RADAR_EINVAL;
-  if (k < 1 || k > kMaxK) return RADAR_EUNSUPPORTED;
-  if (t < 1 || t > s.cap) return RADAR_ECAPACITY;
-  const WsLayout L = ws_layout(s, k);
-  if (!workspace || !aligned16(workspace)) return RADAR_EWORKSPACE;
-  if (workspace_bytes < L.total) return RADAR_EWORKSPACE;
-  int64_t ws;
-  int n_cand;
-  window_split(s, t, &ws, &n_cand);
-  if (n_cand > kMaxCand) return RADAR_EUNSUPPORTED;
-  const int k_eff = std::min(k, n_cand);
+  Shape s;
+  WsLayout L;
+  SeqArgs sa;
+  radar_status r = check_decode(cfg, &s, t, lens, k, workspace, workspace_bytes, &L, &sa);
+  if (r != RADAR_OK) return r;
+  const Span top = make_span(t, sa);
+  const void* Kp = after_sinks(s, K);
+  const void* Vp = after_sinks(s, V);
 
-  if (choose_path(s, t, n_cand, k) == RADAR_PATH_FUSED)
-    return launch_fused(s, q, K, V, omega, summaries, ws, t, n_cand, k, k_eff, out,
-                        selected, scores, stream);
+  if (choose_path(s, sa) == RADAR_PATH_FUSED)
+    return launch_fused(s, q, Kp, Vp, omega, summaries, sa, out, selected, scores,
+                        stream);
 
-  const int u_bound = std::min(s.G * k_eff, n_cand);
-  const AttendGrid ag = attend_grid(s, L, u_bound, ws, t);
+  const int u_bound = std::min(s.G * top.k_eff, top.n_cand);
+  const AttendGrid ag = attend_grid(s, L, u_bound, extra_tiles(s, sa));
   if (ag.grid_x > kMaxWg) return RADAR_EUNSUPPORTED;
 
   unsigned char* w = reinterpret_cast<unsigned char*>(workspace);
   float* phiq = reinterpret_cast<float*>(w + L.phiq);
   float* sc = reinterpret_cast<float*>(w + L.scores);
-  if (n_cand > 0) {
+  if (top.n_cand > 0) {
     if (s.dt == RADAR_BF16) {
       if (s.d == 64) launch_phi_q<bf16_t, 64>(s, q, omega, phiq, stream);
       else launch_phi_q<bf16_t, 128>(s, q, omega, phiq, stream);
@@ -2033,95 +2193,87 @@ radar_status radar_decode(const radar_config* cfg, const void* q, const void* K,
       if (s.d == 64) launch_phi_q<float, 64>(s, q, omega, phiq, stream);
       else launch_phi_q<float, 128>(s, q, omega, phiq, stream);
     }
-    launch_score(s, phiq, summaries, sc, n_cand, stream);
+    launch_score(s, phiq, summaries, sc, top.n_cand, sa, stream);
   }
   launch(RADAR_K_TOPK, k_topk_union, dim3((unsigned)(s.B * s.Hkv)), dim3(256), 0, stream,
-         sc, s.Hq, s.Hkv, s.G, n_cand, (int)std::max<int64_t>(1, s.s_cap), k, k_eff,
+         sc, s.Hq, s.Hkv, s.G, sa, (int)std::max<int64_t>(1, s.s_cap), s.per_head,
          reinterpret_cast<int*>(w + L.uni), reinterpret_cast<int*>(w + L.ucnt), L.umax,
          selected, scores);
   r = launch_status();
   if (r != RADAR_OK) return r;
-  return launch_attend(s, q, K, V, ag, ws, t, out, w, L, stream);
+  return launch_attend(s, q, Kp, Vp, ag, sa, out, w, L, stream);
 }
 
 radar_status radar_decode_exact(const radar_config* cfg, const void* q,
                                 const void* K, const void* V, int64_t t,
-                                int32_t k, void* out, int32_t* selected,
-                                float* scores, void* workspace,
-                                size_t workspace_bytes, hipStream_t stream) {
-  Shape s;
-  radar_status r = check_cfg(cfg, &s);
-  if (r != RADAR_OK) return r;
-  if (!q || !K || !V || !out) return RADAR_EINVAL;
+                                const int64_t* lens, int32_t k, void* out,
+                                int32_t* selected, float* scores,
+                                void* workspace, size_t workspace_bytes,
+                                hipStream_t stream) {
+  if (!cfg || !q || !K || !V || !out) return RADAR_EINVAL;
   if (!aligned16(q) || !aligned16(K) || !aligned16(V) || !aligned16(out) ||
       (selected && !aligned16(selected)) || (scores && !aligned16(scores)))
     return RADAR_EINVAL;
-  if (k < 1 || k > kMaxK) return RADAR_EUNSUPPORTED;
-  if (t < 1 || t > s.cap) return RADAR_ECAPACITY;
-  const WsLayout L = ws_layout(s, k);
-  if (!workspace || !aligned16(workspace)) return RADAR_EWORKSPACE;
-  if (workspace_bytes < L.total) return RADAR_EWORKSPACE;
-  int64_t ws;
-  int n_cand;
-  window_split(s, t, &ws, &n_cand);
-  if (n_cand > kMaxCand) return RADAR_EUNSUPPORTED;
-  const int k_eff = std::min(k, n_cand);
-  const int u_bound = std::min(s.G * k_eff, n_cand);
-  const AttendGrid ag = attend_grid(s, L, u_bound, ws, t);
+  Shape s;
+  WsLayout L;
+  SeqArgs sa;
+  radar_status r = check_decode(cfg, &s, t, lens, k, workspace, workspace_bytes, &L, &sa);
+  if (r != RADAR_OK) return r;
+  const Span top = make_span(t, sa);
+  const void* Kp = after_sinks(s, K);
+  const void* Vp = after_sinks(s, V);
+  const int u_bound = std::min(s.G * top.k_eff, top.n_cand);
+  const AttendGrid ag = attend_grid(s, L, u_bound, extra_tiles(s, sa));
   if (ag.grid_x > kMaxWg) return RADAR_EUNSUPPORTED;
 
   unsigned char* w = reinterpret_cast<unsigned char*>(workspace);
   float* sc = reinterpret_cast<float*>(w + L.scores);
-  if (n_cand > 0) {
+  if (top.n_cand > 0) {
     if (s.dt == RADAR_BF16) {
-      if (s.d == 64) launch_segment_mass_d<bf16_t, 64>(s, q, K, sc, n_cand, stream);
-      else launch_segment_mass_d<bf16_t, 128>(s, q, K, sc, n_cand, stream);
+      if (s.d == 64) launch_segment_mass_d<bf16_t, 64>(s, q, Kp, sc, top.n_cand, sa, stream);
+      else launch_segment_mass_d<bf16_t, 128>(s, q, Kp, sc, top.n_cand, sa, stream);
     } else {
-      if (s.d == 64) launch_segment_mass_d<float, 64>(s, q, K, sc, n_cand, stream);
-      else launch_segment_mass_d<float, 128>(s, q, K, sc, n_cand, stream);
+      if (s.d == 64) launch_segment_mass_d<float, 64>(s, q, Kp, sc, top.n_cand, sa, stream);
+      else launch_segment_mass_d<float, 128>(s, q, Kp, sc, top.n_cand, sa, stream);
     }
   }
   launch(RADAR_K_TOPK, k_topk_union, dim3((unsigned)(s.B * s.Hkv)), dim3(256), 0, stream,
-         sc, s.Hq, s.Hkv, s.G, n_cand, (int)std::max<int64_t>(1, s.s_cap), k, k_eff,
+         sc, s.Hq, s.Hkv, s.G, sa, (int)std::max<int64_t>(1, s.s_cap), s.per_head,
          reinterpret_cast<int*>(w + L.uni), reinterpret_cast<int*>(w + L.ucnt), L.umax,
          selected, scores);
   r = launch_status();
   if (r != RADAR_OK) return r;
-  return launch_attend(s, q, K, V, ag, ws, t, out, w, L, stream);
+  return launch_attend(s, q, Kp, Vp, ag, sa, out, w, L, stream);
 }
 
 radar_status radar_attend_selected(const radar_config* cfg, const void* q,
                                    const void* K, const void* V,
                                    const int32_t* selected, int32_t k, int64_t t,
-                                   void* out, void* workspace,
-                                   size_t workspace_bytes, hipStream_t stream) {
-  Shape s;
-  radar_status r = check_cfg(cfg, &s);
-  if (r != RADAR_OK) return r;
-  if (!q || !K || !V || !selected || !out) return RADAR_EINVAL;
+                                   const int64_t* lens, void* out,
+                                   void* workspace, size_t workspace_bytes,
+                                   hipStream_t stream) {
+  if (!cfg || !q || !K || !V || !selected || !out) return RADAR_EINVAL;
   if (!aligned16(q) || !aligned16(K) || !aligned16(V) || !aligned16(selected) ||
       !aligned16(out))
     return RADAR_EINVAL;
-  if (k < 1 || k > kMaxK) return RADAR_EUNSUPPORTED;
-  if (t < 1 || t > s.cap) return RADAR_ECAPACITY;
-  const WsLayout L = ws_layout(s, k);
-  if (!workspace || !aligned16(workspace)) return RADAR_EWORKSPACE;
-  if (workspace_bytes < L.total) return RADAR_EWORKSPACE;
-  int64_t ws;
-  int n_cand;
-  window_split(s, t, &ws, &n_cand);
-  if (n_cand > kMaxCand) return RADAR_EUNSUPPORTED;
-  const int u_bound = std::min(s.G * k, n_cand);
-  const AttendGrid ag = attend_grid(s, L, u_bound, ws, t);
+  Shape s;
+  WsLayout L;
+  SeqArgs sa;
+  radar_status r = check_decode(cfg, &s, t, lens, k, workspace, workspace_bytes, &L, &sa);
+  if (r != RADAR_OK) return r;
+  const Span top = make_span(t, sa);
+  const int u_bound = std::min(s.G * k, top.n_cand);
+  const AttendGrid ag = attend_grid(s, L, u_bound, extra_tiles(s, sa));
   if (ag.grid_x > kMaxWg) return RADAR_EUNSUPPORTED;
   unsigned char* w = reinterpret_cast<unsigned char*>(workspace);
   launch(RADAR_K_TOPK, k_union_given, dim3((unsigned)(s.B * s.Hkv)), dim3(256), 0,
-         stream, selected, k, s.Hq, s.Hkv, s.G, n_cand,
+         stream, selected, k, s.Hq, s.Hkv, s.G, sa, s.per_head,
          reinterpret_cast<int*>(w + L.uni), reinterpret_cast<int*>(w + L.ucnt),
          L.umax);
   r = launch_status();
   if (r != RADAR_OK) return r;
-  return launch_attend(s, q, K, V, ag, ws, t, out, w, L, stream);
+  return launch_attend(s, q, after_sinks(s, K), after_sinks(s, V), ag, sa, out, w,
+                       L, stream);
 }
 
 }  // extern "C"

@@ -34,10 +34,12 @@ SCORE_TOL = 2e-5
 SUMM_TOL = 1e-4
 
 
-def config_of(wl: workloads.Workload, capacity: int) -> radar.Config:
+def config_of(wl: workloads.Workload, capacity: int, n_sink: int = 0,
+              per_head: bool = False) -> radar.Config:
     return radar.Config(wl.batch, wl.n_q_heads, wl.n_kv_heads, wl.head_dim,
                         wl.n_features, wl.seg_len, wl.window, capacity,
-                        wl.torch_dtype())
+                        wl.torch_dtype(), n_sink,
+                        radar.GQA_PER_HEAD if per_head else radar.GQA_UNION)
 
 
 def f64(x: torch.Tensor) -> np.ndarray:
@@ -86,15 +88,22 @@ class Stats:
 
 class Episode:
     """One workload run: build the index at t0, then `steps` x (append,
-    decode). Oracle checks on the sampled (batch, kv head) groups."""
+    decode). Oracle checks on the sampled (batch, kv head) groups.
+
+    n_sink / per_head select the attention-sink and per-head GQA options.
+    lens0 (one length <= t0 per sequence) makes the batch ragged: sequence b
+    starts at length lens0[b] (its cache rows beyond are stale), appends at
+    its own position and decodes at its own length."""
 
     def __init__(self, wl, steps, groups=None, device="cuda",
-                 path=radar.PATH_AUTO):
+                 path=radar.PATH_AUTO, n_sink=0, per_head=False, lens0=None):
         self.wl = wl
         self.steps = steps
         self.path = path
+        self.n_sink, self.per_head = n_sink, per_head
+        self.lens0 = list(lens0) if lens0 is not None else None
         self.inp = workloads.make_inputs(wl, device, steps=steps)
-        self.cfg = config_of(wl, wl.t0 + steps)
+        self.cfg = config_of(wl, wl.t0 + steps, n_sink, per_head)
         B, Hkv = wl.batch, wl.n_kv_heads
         self.groups = groups if groups is not None else \
             [(b, g) for b in range(B) for g in range(Hkv)]
@@ -103,11 +112,20 @@ class Episode:
         self.vals = {}
         self.summ64 = {}
         for (b, g) in self.groups:
-            kk = f64(self.inp.keys_at(steps, b, g))
+            if self.lens0 is None:
+                kk = f64(self.inp.keys_at(steps, b, g))
+                vv = f64(self.inp.values_at(steps, b, g))
+            else:
+                L0 = self.lens0[b]
+                kk = np.concatenate([f64(self.inp.K[b, g, :L0]),
+                                     f64(self.inp.k_new[:steps, b, g])])
+                vv = np.concatenate([f64(self.inp.V[b, g, :L0]),
+                                     f64(self.inp.v_new[:steps, b, g])])
             self.keys[(b, g)] = kk
-            self.vals[(b, g)] = f64(self.inp.values_at(steps, b, g))
+            self.vals[(b, g)] = vv
             self.summ64[(b, g)] = orc.segment_summaries(kk, self.omega64,
-                                                        wl.seg_len)
+                                                        wl.seg_len,
+                                                        offset=n_sink)
         self.stats = Stats()
 
     def run(self, check_steps=None):
@@ -123,55 +141,67 @@ class Episode:
         K, V = inp.K.clone(), inp.V.clone()
         summ = radar.new_summaries(cfg, dev)
         radar.build_index(cfg, K, inp.omega, wl.t0, summ)
-        self.check_summaries(summ, wl.t0)
+        lens = [wl.t0] * wl.batch if self.lens0 is None else list(self.lens0)
+        self.check_summaries(summ, lens)
         ws = radar.new_workspace(cfg, wl.top_k, dev)
         sel = torch.empty(wl.batch, wl.n_q_heads, wl.top_k, dtype=torch.int32,
                           device=dev)
         sc = torch.empty(wl.batch, wl.n_q_heads, wl.top_k, dtype=torch.float32,
                          device=dev)
         out = torch.empty_like(inp.q[0])
-        t = wl.t0
         for i in range(self.steps):
-            radar.append(cfg, K, V, inp.k_new[i].contiguous(),
-                         inp.v_new[i].contiguous(), inp.omega, t, summ)
-            t += 1
+            if self.lens0 is None:
+                radar.append(cfg, K, V, inp.k_new[i].contiguous(),
+                             inp.v_new[i].contiguous(), inp.omega, lens[0], summ)
+            else:
+                pos = torch.tensor(lens, dtype=torch.int64, device=dev)
+                radar.append(cfg, K, V, inp.k_new[i].contiguous(),
+                             inp.v_new[i].contiguous(), inp.omega, 0, summ,
+                             pos=pos)
+            lens = [x + 1 for x in lens]
             q = inp.q[i].contiguous()
-            radar.decode(cfg, q, K, V, inp.omega, summ, t, wl.top_k, out=out,
-                         selected=sel, scores=sc, workspace=ws)
+            lens_dev = None if self.lens0 is None else \
+                torch.tensor(lens, dtype=torch.int64, device=dev)
+            radar.decode(cfg, q, K, V, inp.omega, summ, max(lens), wl.top_k,
+                         out=out, selected=sel, scores=sc, workspace=ws,
+                         lens=lens_dev)
             if check_steps is None or i in check_steps:
                 torch.cuda.synchronize()
-                self.check_step(i, t, q, out, sel, sc)
-        self.check_summaries(summ, t)
+                self.check_step(i, lens, q, out, sel, sc)
+        self.check_summaries(summ, lens)
         self.K, self.V, self.summ = K, V, summ
         return self.stats
 
-    def check_summaries(self, summ, t):
+    def check_summaries(self, summ, lens):
         c = self.wl.seg_len
-        n_seg = t // c
         for (b, g) in self.groups:
+            n_seg = max(0, lens[b] - self.n_sink) // c
             got = f64(summ[b, g, :n_seg])
             ref = self.summ64[(b, g)][:n_seg]
             err = float(np.max(np.abs(got - ref) / np.abs(ref))) if n_seg else 0.0
             self.stats.max_summ_err = max(self.stats.max_summ_err, err)
             assert err <= SUMM_TOL, (b, g, err)
 
-    def check_step(self, i, t, q, out, sel, sc):
+    def check_step(self, i, lens, q, out, sel, sc):
         wl = self.wl
         G, c, d = wl.group, wl.seg_len, wl.head_dim
-        ws, n_cand = orc.window_split(t, c, wl.window)
-        k_eff = min(wl.top_k, n_cand)
         q64 = f64(q)
         out64 = f64(out)
         sel_np = sel.cpu().numpy()
         sc_np = sc.cpu().numpy()
         for (b, g) in self.groups:
+            t = lens[b]
+            ws, n_cand = orc.window_split(t, c, wl.window, self.n_sink)
+            k_eff = min(wl.top_k, n_cand)
             union = set()
+            own = {}
             for h in range(g * G, (g + 1) * G):
                 phi_q = orc.random_features(q64[b, h], self.omega64)
                 ora_sc = orc.segment_scores(phi_q, self.summ64[(b, g)][:n_cand])
                 self.stats.band_swaps += check_selection(sel_np[b, h], ora_sc,
                                                          k_eff, n_cand)
                 picks = [int(s) for s in sel_np[b, h, :k_eff]]
+                own[h] = picks
                 union.update(picks)
                 if k_eff:
                     ref = ora_sc[picks]
@@ -180,8 +210,9 @@ class Episode:
                     assert err <= SCORE_TOL, (i, b, h, err)
                     got_order = sc_np[b, h, :k_eff]
                     assert np.all(got_order[:-1] >= got_order[1:]), got_order
-            toks = orc.attended_tokens(sorted(union), c, ws, t)
             for h in range(g * G, (g + 1) * G):
+                segs = own[h] if self.per_head else sorted(union)
+                toks = orc.attended_tokens(segs, c, ws, t, self.n_sink)
                 ref = orc.attend(q64[b, h], self.keys[(b, g)],
                                  self.vals[(b, g)], toks)
                 e = rel_inf(out64[b, h], ref)

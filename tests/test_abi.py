@@ -39,7 +39,7 @@ def test_exports_every_declared_symbol(L):
 
 
 def test_version_and_strings(L):
-    assert L.radar_abi_version() == 1
+    assert L.radar_abi_version() == radar.ABI_VERSION == 2
     for st in range(6):
         assert L.radar_status_string(st).decode()
     assert L.radar_last_error() is not None
@@ -87,29 +87,32 @@ def test_validation_before_launch(L):
     assert L.radar_build_index(by(cfg), good, good, 0, good, None) == 2
     assert L.radar_build_index(by(cfg), good, good, 131585, good, None) == 2
     # append position outside [0, capacity)
-    assert L.radar_append(by(cfg), good, good, good, good, good, 131584, good,
-                          None) == 2
-    assert L.radar_append(by(cfg), good, good, good, good, good, -1, good,
-                          None) == 2
+    ap = [by(cfg), good, good, good, good, good]
+    assert L.radar_append(*ap, 131584, null, good, None) == 2
+    assert L.radar_append(*ap, -1, null, good, None) == 2
+    assert L.radar_append(*ap, 5, odd, good, None) == 1      # misaligned pos
     ws = L.radar_decode_workspace_bytes(by(cfg), 16)
     args = [by(cfg), good, good, good, good, good]
     # k out of range
-    assert L.radar_decode(*args, 1000, 0, good, None, None, good, ws, None) == 3
-    assert L.radar_decode(*args, 1000, 300, good, None, None, good, ws, None) == 3
+    assert L.radar_decode(*args, 1000, null, 0, good, None, None, good, ws, None) == 3
+    assert L.radar_decode(*args, 1000, null, 300, good, None, None, good, ws, None) == 3
     # t out of range
-    assert L.radar_decode(*args, 0, 16, good, None, None, good, ws, None) == 2
+    assert L.radar_decode(*args, 0, null, 16, good, None, None, good, ws, None) == 2
+    # misaligned lens
+    assert L.radar_decode(*args, 1000, odd, 16, good, None, None, good, ws, None) == 1
     # workspace missing / too small
-    assert L.radar_decode(*args, 1000, 16, good, None, None, None, ws, None) == 5
-    assert L.radar_decode(*args, 1000, 16, good, None, None, good, ws - 1,
+    assert L.radar_decode(*args, 1000, null, 16, good, None, None, None, ws, None) == 5
+    assert L.radar_decode(*args, 1000, null, 16, good, None, None, good, ws - 1,
                           None) == 5
     # too many candidate segments for the top-k stage
     big = _cfg(seg_len=16, window=16, capacity=1 << 20).c_struct()
     wsb = L.radar_decode_workspace_bytes(by(big), 16)
-    assert L.radar_decode(by(big), good, good, good, good, good, 40000, 16,
+    assert L.radar_decode(by(big), good, good, good, good, good, 40000, null, 16,
                           good, None, None, good, wsb, None) == 3
     # bad shapes
     for bad in (_cfg(batch=0), _cfg(n_q_heads=30), _cfg(seg_len=0),
-                _cfg(window=-1), _cfg(capacity=0)):
+                _cfg(window=-1), _cfg(capacity=0), _cfg(n_sink=-1),
+                _cfg(n_sink=131585), _cfg(gqa_mode=2)):
         assert L.radar_build_index(by(bad.c_struct()), good, good, 1, good,
                                    None) == 1
     for bad in (_cfg(head_dim=256), _cfg(n_features=1024),
@@ -119,21 +122,24 @@ def test_validation_before_launch(L):
                                    None) == 3
     # decode_exact: same checks as decode
     ex = [by(cfg), good, good, good]
-    assert L.radar_decode_exact(*ex, 1000, 0, good, None, None, good, ws,
+    assert L.radar_decode_exact(*ex, 1000, null, 0, good, None, None, good, ws,
                                 None) == 3
-    assert L.radar_decode_exact(*ex, 131585, 16, good, None, None, good, ws,
-                                None) == 2
-    assert L.radar_decode_exact(*ex, 1000, 16, null, None, None, good, ws,
+    assert L.radar_decode_exact(*ex, 131585, null, 16, good, None, None, good,
+                                ws, None) == 2
+    assert L.radar_decode_exact(*ex, 1000, null, 16, null, None, None, good, ws,
                                 None) == 1
-    assert L.radar_decode_exact(*ex, 1000, 16, good, None, None, good, ws - 1,
-                                None) == 5
-    assert L.radar_decode_exact(by(big), good, good, good, 40000, 16, good,
+    assert L.radar_decode_exact(*ex, 1000, null, 16, good, None, None, good,
+                                ws - 1, None) == 5
+    assert L.radar_decode_exact(by(big), good, good, good, 40000, null, 16, good,
                                 None, None, good, wsb, None) == 3
     # attend_selected
     assert L.radar_attend_selected(by(cfg), good, good, good, null, 4, 100,
-                                   good, good, ws, None) == 1
+                                   null, good, good, ws, None) == 1
     assert L.radar_attend_selected(by(cfg), good, good, good, good, 0, 100,
-                                   good, good, ws, None) == 3
+                                   null, good, good, ws, None) == 3
+    # sinks widen the scratch for the attention partials
+    assert radar.workspace_bytes(_cfg(n_sink=4096), 16) > \
+        radar.workspace_bytes(_cfg(), 16)
 
 
 def test_product_path_has_no_fallback(monkeypatch, tmp_path):
