@@ -1337,48 +1337,104 @@ __global__ __launch_bounds__(512) void k_decode_fused(
   const int64_t ws = sp.ws, t = sp.t;
 
   if (n_cand > 0) {                        // uniform
+    // Each wave's first batch of summary rows goes in flight before phi(q)
+    // is computed (the rows do not depend on it), so the projection's
+    // latency overlaps the stream of the scores.
+    constexpr int RB = FPL <= 4 ? 2 : 1;   // 16-row batches per pass
+    const float* base = summ + (bh * s_cap) * N + lane * FPL;
+    float x[RB][16][FPL];
+    auto load_rows = [&](int rb) {
+#pragma unroll
+      for (int bt = 0; bt < RB; ++bt)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int row = min(rb + bt * 16 + i, n_cand - 1);
+          const float* src = base + (int64_t)row * N;
+          if constexpr (FPL % 4 == 0) {
+#pragma unroll
+            for (int e = 0; e < FPL; e += 4) {
+              const float4 v = ld_stream_f4(src + e);
+              x[bt][i][e] = v.x; x[bt][i][e + 1] = v.y;
+              x[bt][i][e + 2] = v.z; x[bt][i][e + 3] = v.w;
+            }
+          } else if constexpr (FPL == 2) {
+            const float2 v = *reinterpret_cast<const float2*>(src);
+            x[bt][i][0] = v.x; x[bt][i][1] = v.y;
+          } else {
+            x[bt][i][0] = src[0];
+          }
+        }
+    };
+
     // ---- 1. phi(q) -----------------------------------------------------
+    // 16 lanes per Omega row, 4 rows per wave and pass, NP passes. All of a
+    // chunk's Omega loads are issued before any is used, then the summary
+    // rows (when they fit in registers next to them), then the dots.
+    const int rb0 = wave * 16 * RB;
     {
+      constexpr int NP = N / (4 * NW);       // passes
+      constexpr int PC = NP < 8 ? NP : 8;    // passes per load chunk
+      constexpr bool kPrefetch = NP <= 8;
       const int r = lane >> 4, jj = lane & 15;
       float qv[G][QPL], nrm[G];
 #pragma unroll
-      for (int g = 0; g < G; ++g) {
-        float sq = 0.f;
+      for (int g = 0; g < G; ++g)
 #pragma unroll
-        for (int e = 0; e < QPL; ++e) {
-          qv[g][e] = to_f32<T>(q0[g * D + jj * QPL + e]);
-          sq = fmaf(qv[g][e], qv[g][e], sq);
+        for (int e = 0; e < QPL; ++e) qv[g][e] = to_f32<T>(q0[g * D + jj * QPL + e]);
+      float ph[NP][G];
+#pragma unroll
+      for (int c0 = 0; c0 < NP; c0 += PC) {
+        float4 om[PC][QPL / 4];
+#pragma unroll
+        for (int p = 0; p < PC; ++p) {
+          const float* orow = omega + (int64_t)((c0 + p) * 4 * NW + wave * 4 + r) * D + jj * QPL;
+#pragma unroll
+          for (int e4 = 0; e4 < QPL / 4; ++e4)
+            om[p][e4] = *reinterpret_cast<const float4*>(orow + 4 * e4);
         }
-        nrm[g] = row_sum(sq);
-      }
-#pragma unroll
-      for (int row0 = 0; row0 < N; row0 += 4 * NW) {
-        const int row = row0 + wave * 4 + r;
-        const float* orow = omega + (int64_t)row * D + jj * QPL;
-        float a[G];
-#pragma unroll
-        for (int g = 0; g < G; ++g) a[g] = 0.f;
-#pragma unroll
-        for (int e4 = 0; e4 < QPL; e4 += 4) {
-          float4 o = *reinterpret_cast<const float4*>(orow + e4);
-          if constexpr (sizeof(T) == 2) {
-            o.x = round_bf16(o.x); o.y = round_bf16(o.y);
-            o.z = round_bf16(o.z); o.w = round_bf16(o.w);
-          }
+        // unconditional (rows clamp to the last candidate), so no branch
+        // makes the compiler wait for these loads before the dots
+        if (kPrefetch && c0 == 0) load_rows(rb0);
+        if (c0 == 0) {
 #pragma unroll
           for (int g = 0; g < G; ++g) {
-            a[g] = fmaf(o.x, qv[g][e4], a[g]);
-            a[g] = fmaf(o.y, qv[g][e4 + 1], a[g]);
-            a[g] = fmaf(o.z, qv[g][e4 + 2], a[g]);
-            a[g] = fmaf(o.w, qv[g][e4 + 3], a[g]);
+            float sq = 0.f;
+#pragma unroll
+            for (int e = 0; e < QPL; ++e) sq = fmaf(qv[g][e], qv[g][e], sq);
+            nrm[g] = row_sum(sq);
           }
         }
 #pragma unroll
-        for (int g = 0; g < G; ++g) {
-          const float dot = row_sum(a[g]);
-          if (jj == 0)
-            phq[g * N + row] = fast_exp2(fmaf(dot, s1, -nrm[g] * s2)) * inv_sqrt_n;
+        for (int p = 0; p < PC; ++p) {
+          float a[G];
+#pragma unroll
+          for (int g = 0; g < G; ++g) a[g] = 0.f;
+#pragma unroll
+          for (int e4 = 0; e4 < QPL / 4; ++e4) {
+            float4 o = om[p][e4];
+            if constexpr (sizeof(T) == 2) {
+              o.x = round_bf16(o.x); o.y = round_bf16(o.y);
+              o.z = round_bf16(o.z); o.w = round_bf16(o.w);
+            }
+#pragma unroll
+            for (int g = 0; g < G; ++g) {
+              a[g] = fmaf(o.x, qv[g][4 * e4], a[g]);
+              a[g] = fmaf(o.y, qv[g][4 * e4 + 1], a[g]);
+              a[g] = fmaf(o.z, qv[g][4 * e4 + 2], a[g]);
+              a[g] = fmaf(o.w, qv[g][4 * e4 + 3], a[g]);
+            }
+          }
+#pragma unroll
+          for (int g = 0; g < G; ++g)
+            ph[c0 + p][g] = fast_exp2(fmaf(row_sum(a[g]), s1, -nrm[g] * s2)) * inv_sqrt_n;
         }
+      }
+      if (!kPrefetch) load_rows(rb0);
+      if (jj == 0) {
+#pragma unroll
+        for (int p = 0; p < NP; ++p)
+#pragma unroll
+          for (int g = 0; g < G; ++g) phq[g * N + p * 4 * NW + wave * 4 + r] = ph[p][g];
       }
     }
     __syncthreads();
@@ -1390,30 +1446,8 @@ __global__ __launch_bounds__(512) void k_decode_fused(
       for (int g = 0; g < G; ++g)
 #pragma unroll
         for (int e = 0; e < FPL; ++e) pq[g][e] = phq[g * N + lane * FPL + e];
-      constexpr int RB = FPL <= 4 ? 2 : 1;   // 16-row batches per pass
-      const float* base = summ + (bh * s_cap) * N + lane * FPL;
-      for (int rb = wave * 16 * RB; rb < n_cand; rb += NW * 16 * RB) {
-        float x[RB][16][FPL];
-#pragma unroll
-        for (int bt = 0; bt < RB; ++bt)
-#pragma unroll
-          for (int i = 0; i < 16; ++i) {
-            const int row = min(rb + bt * 16 + i, n_cand - 1);
-            const float* src = base + (int64_t)row * N;
-            if constexpr (FPL % 4 == 0) {
-#pragma unroll
-              for (int e = 0; e < FPL; e += 4) {
-                const float4 v = ld_stream_f4(src + e);
-                x[bt][i][e] = v.x; x[bt][i][e + 1] = v.y;
-                x[bt][i][e + 2] = v.z; x[bt][i][e + 3] = v.w;
-              }
-            } else if constexpr (FPL == 2) {
-              const float2 v = *reinterpret_cast<const float2*>(src);
-              x[bt][i][0] = v.x; x[bt][i][1] = v.y;
-            } else {
-              x[bt][i][0] = src[0];
-            }
-          }
+      for (int rb = rb0; rb < n_cand; rb += NW * 16 * RB) {
+        if (rb != rb0) load_rows(rb);
 #pragma unroll
         for (int bt = 0; bt < RB; ++bt) {
           const int row = rb + bt * 16 + (lane & 15);
