@@ -278,9 +278,13 @@ def main():
                     choices=sorted(workloads.WORKLOADS))
     ap.add_argument("--cpu-baseline", type=int, default=1)
     ap.add_argument("--cpu-heads", type=int, default=8)
-    ap.add_argument("--calibrate-copy", type=int, default=0,
+    ap.add_argument("--calibrate-copy", type=int, default=1,
                     help="also run a plain 1 GiB read+write elementwise "
-                         "kernel (counter calibration for HBM traffic)")
+                         "kernel: the box's copy bandwidth (and the counter "
+                         "calibration for HBM traffic)")
+    ap.add_argument("--peaks", type=int, default=1,
+                    help="measure the sustained bf16 MFMA and exp2 rates "
+                         "(the index build's two resources)")
     ap.add_argument("--build-reps", type=int, default=3)
     ap.add_argument("--path", default="auto", choices=["auto", "split", "fused"],
                     help="decode path (auto: the library's choice)")
@@ -351,6 +355,7 @@ def main():
     n_keys = wl.batch * wl.n_kv_heads * (wl.t0 // wl.seg_len) * wl.seg_len
     build_flop = 2.0 * n_keys * wl.n_features * wl.head_dim
     build_tflops = build_flop / (build_ms * 1e-3) / 1e12
+    build_exps = n_keys * wl.n_features / (build_ms * 1e-3) / 1e12   # 10^12 / s
 
     # ---- decode steps ----------------------------------------------------
     stp = Stepper(cfg, inp, K, V, summ, ws, out, wl.top_k,
@@ -445,6 +450,8 @@ def main():
         log(f"[bench] copy kernel (1 GiB read + 1 GiB write): {copy_gbps:.1f} GB/s")
         del x, y
 
+    peaks = radar.peak_rates() if args.peaks else None
+
     line = {
         "metric": METRIC,
         "value": round(tokens_s, 1),
@@ -493,11 +500,17 @@ def main():
             "tflops": round(build_tflops, 1),
             "mfma_frac": round(build_tflops / BF16_MFMA_PEAK_TFLOPS, 4),
             "keys": n_keys,
+            "exp2_T_per_s": round(build_exps, 3),
+            "mfma_peak_measured_tflops": round(peaks["mfma_tflops"], 1) if peaks else None,
+            "mfma_frac_of_measured": round(build_tflops / peaks["mfma_tflops"], 4) if peaks else None,
+            "exp2_peak_measured_T_per_s": round(peaks["exp_T_per_s"], 3) if peaks else None,
+            "exp2_frac_of_measured": round(build_exps / peaks["exp_T_per_s"], 4) if peaks else None,
         },
         "cpu_baseline": cpu,
     }
     if copy_gbps is not None:
         line["copy_GBps"] = round(copy_gbps, 1)
+        line["roofline"]["frac_of_copy"] = round(dom_gbps / copy_gbps, 4)
     print(json.dumps(line), flush=True)
 
 

@@ -250,6 +250,19 @@ radar_status radar_profile_enable(int32_t on);
  * releases the records. */
 radar_status radar_profile_read(double* ms, int64_t* launches, int32_t n);
 
+/* Measurement microkernels (not part of the method), for reporting the
+ * index build against what this GPU sustains: radar_peak_mfma runs dense
+ * bf16 16x16x32 matrix-core chains, radar_peak_exp chains of exp2 on the
+ * vector ALUs, each over the whole chip for `iters` rounds on `stream`.
+ * *work (host) receives the launch's work: FLOP, or exp2 evaluations. The
+ * caller times the launch. sink: device buffer of at least
+ * radar_peak_sink_floats() floats, overwritten. */
+size_t radar_peak_sink_floats(void);
+radar_status radar_peak_mfma(int32_t iters, float* sink, double* work,
+                             hipStream_t stream);
+radar_status radar_peak_exp(int32_t iters, float* sink, double* work,
+                            hipStream_t stream);
+
 /* Static text for a status code. */
 const char* radar_status_string(radar_status status);
 

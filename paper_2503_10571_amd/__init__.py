@@ -115,6 +115,11 @@ def lib() -> ctypes.CDLL:
         L.radar_decode_path.restype = i32
         L.radar_profile_read.argtypes = [ctypes.POINTER(ctypes.c_double),
                                          ctypes.POINTER(ctypes.c_int64), i32]
+        L.radar_peak_sink_floats.restype = sz
+        L.radar_peak_mfma.argtypes = [i32, _P, ctypes.POINTER(ctypes.c_double), _P]
+        L.radar_peak_exp.argtypes = [i32, _P, ctypes.POINTER(ctypes.c_double), _P]
+        for fn in ("radar_peak_mfma", "radar_peak_exp"):
+            getattr(L, fn).restype = ctypes.c_int
         for fn in ("radar_build_index", "radar_append", "radar_decode",
                    "radar_decode_exact", "radar_attend_selected",
                    "radar_profile_enable", "radar_profile_read"):
@@ -294,6 +299,32 @@ def profile_read() -> dict:
     cnt = (ctypes.c_int64 * n)()
     _check("radar_profile_read", lib().radar_profile_read(ms, cnt, n))
     return {k: (ms[i], cnt[i]) for i, k in enumerate(KERNELS)}
+
+
+def peak_rates(device="cuda", iters=4096) -> dict:
+    """Measured sustained dense bf16 MFMA rate (TFLOP/s) and exp2 rate
+    (10^12 / s) of this GPU, from the library's measurement microkernels
+    (measurement only)."""
+    L = lib()
+    sink = torch.empty(int(L.radar_peak_sink_floats()), dtype=torch.float32,
+                       device=device)
+    st = ctypes.c_void_p(torch.cuda.current_stream(sink.device).cuda_stream)
+    out = {}
+    for name, fn, n in (("mfma_tflops", L.radar_peak_mfma, iters),
+                        ("exp_T_per_s", L.radar_peak_exp, iters * 4)):
+        work = ctypes.c_double()
+        _check(fn.__name__, fn(n, _ptr(sink), ctypes.byref(work), st))    # warm
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(3):
+            _check(fn.__name__, fn(n, _ptr(sink), ctypes.byref(work), st))
+        e1.record()
+        torch.cuda.synchronize()
+        sec = e0.elapsed_time(e1) / 3 * 1e-3
+        out[name] = work.value / sec / 1e12
+    return out
 
 
 class RadarLayer:

@@ -563,6 +563,51 @@ __global__ __launch_bounds__(256) void k_build(
 }
 
 // ---------------------------------------------------------------------------
+// measurement microkernels (not part of the method)
+// ---------------------------------------------------------------------------
+// The two resources the index build spends: dense bf16 matrix-core work
+// (8 independent 16x16x32 accumulation chains per wave) and exp2 on the
+// vector ALUs (8 independent chains per lane). The sink store, which the
+// compiler cannot prove dead, keeps the work alive.
+constexpr int kPeakWgPerCu = 2;
+
+__global__ __launch_bounds__(256) void k_peak_mfma(int iters, float* __restrict__ sink) {
+  const int lane = threadIdx.x & 63;
+  bf16x8_t a, b;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    a[i] = (short)(0x3f80 + ((lane + i) & 7));     // bf16 values near 1
+    b[i] = (short)(0x3f80 - i);
+  }
+  f32x4_t acc[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc[j], 0, 0, 0);
+  }
+  float v = 0.f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) v += acc[j][0] + acc[j][1] + acc[j][2] + acc[j][3];
+  sink[(int64_t)blockIdx.x * blockDim.x + threadIdx.x] = v;
+}
+
+__global__ __launch_bounds__(256) void k_peak_exp(int iters, float* __restrict__ sink) {
+  float x[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) x[j] = 1e-3f * (float)(threadIdx.x & 63) + 1e-2f * (float)j;
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) x[j] = fast_exp2(-x[j]);
+  }
+  float v = 0.f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) v += x[j];
+  sink[(int64_t)blockIdx.x * blockDim.x + threadIdx.x] = v;
+}
+
+// ---------------------------------------------------------------------------
 // k_append: K[b][h][t] = k_new[b][h], V likewise
 // ---------------------------------------------------------------------------
 // (row pos[b] of sequence b when pos is given; rows outside [0, cap) are
@@ -2090,6 +2135,28 @@ int32_t radar_decode_path(const radar_config* cfg, int64_t t, int32_t k) {
 radar_status radar_profile_enable(int32_t on) {
   g_prof.on = on != 0;
   return RADAR_OK;
+}
+
+size_t radar_peak_sink_floats(void) {
+  return (size_t)num_cu() * kPeakWgPerCu * 256;
+}
+
+radar_status radar_peak_mfma(int32_t iters, float* sink, double* work,
+                             hipStream_t stream) {
+  if (iters < 1 || !sink || !work || !aligned16(sink)) return RADAR_EINVAL;
+  const unsigned grid = (unsigned)(num_cu() * kPeakWgPerCu);
+  hipLaunchKernelGGL(k_peak_mfma, dim3(grid), dim3(256), 0, stream, iters, sink);
+  *work = (double)grid * 4 * iters * 8 * (2.0 * 16 * 16 * 32);
+  return launch_status();
+}
+
+radar_status radar_peak_exp(int32_t iters, float* sink, double* work,
+                            hipStream_t stream) {
+  if (iters < 1 || !sink || !work || !aligned16(sink)) return RADAR_EINVAL;
+  const unsigned grid = (unsigned)(num_cu() * kPeakWgPerCu);
+  hipLaunchKernelGGL(k_peak_exp, dim3(grid), dim3(256), 0, stream, iters, sink);
+  *work = (double)grid * 256 * iters * 8;
+  return launch_status();
 }
 
 radar_status radar_profile_read(double* ms, int64_t* launches, int32_t n) {

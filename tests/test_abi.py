@@ -137,6 +137,11 @@ def test_validation_before_launch(L):
                                    null, good, good, ws, None) == 1
     assert L.radar_attend_selected(by(cfg), good, good, good, good, 0, 100,
                                    null, good, good, ws, None) == 3
+    # measurement microkernels
+    work = ctypes.c_double()
+    assert L.radar_peak_mfma(0, good, by(work), None) == 1
+    assert L.radar_peak_exp(16, null, by(work), None) == 1
+    assert L.radar_peak_exp(16, odd, by(work), None) == 1
     # sinks widen the scratch for the attention partials
     assert radar.workspace_bytes(_cfg(n_sink=4096), 16) > \
         radar.workspace_bytes(_cfg(), 16)
