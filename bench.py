@@ -286,7 +286,8 @@ def main():
                     help="measure the sustained bf16 MFMA and exp2 rates "
                          "(the index build's two resources)")
     ap.add_argument("--build-reps", type=int, default=3)
-    ap.add_argument("--path", default="auto", choices=["auto", "split", "fused"],
+    ap.add_argument("--path", default="auto",
+                    choices=["auto", "split", "fused", "select"],
                     help="decode path (auto: the library's choice)")
     ap.add_argument("--selector", default="radar", choices=["radar", "exact"],
                     help="radar: Eq. 6 scores (the method); exact: the exact "
@@ -309,7 +310,8 @@ def main():
         sys.exit(2)
 
     radar.set_decode_path({"auto": radar.PATH_AUTO, "split": radar.PATH_SPLIT,
-                           "fused": radar.PATH_FUSED}[args.path])
+                           "fused": radar.PATH_FUSED,
+                           "select": radar.PATH_SELECT}[args.path])
     wl = workloads.WORKLOADS[args.workload]
     if args.recall:
         recall_sweep(wl)
@@ -474,8 +476,8 @@ def main():
             "batch": wl.batch, "context": wl.t0, "seg_len": wl.seg_len,
             "top_k": wl.top_k, "n_features": wl.n_features,
             "window": wl.window,
-            "decode_path": {radar.PATH_SPLIT: "split",
-                            radar.PATH_FUSED: "fused"}.get(path, "?"),
+            "decode_path": {radar.PATH_SPLIT: "split", radar.PATH_FUSED: "fused",
+                            radar.PATH_SELECT: "select"}.get(path, "?"),
             "schedule": args.schedule,
             "selector": args.selector,
             "restructures": restructures,

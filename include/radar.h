@@ -203,16 +203,22 @@ radar_status radar_schedule_sqrt(int64_t t, int32_t* seg_len, int32_t* window);
 /* Decode paths. The split path runs phi(q), scores, top-k, attention and
  * merge as separate kernels spread over the whole chip; the fused path runs
  * the whole step of one (b, kv head) in one workgroup, which suits shapes
- * with at least as many (b, kv head) pairs as compute units. Both compute the
- * same method; their fp32 summation orders differ. */
+ * with at least as many (b, kv head) pairs as compute units; the select path
+ * runs phi(q), scores, top-k and union of each pair in one workgroup and
+ * then the split path's attention and merge, which suits few pairs with few
+ * candidates. All compute the same method; their fp32 summation orders
+ * differ. */
 typedef enum {
   RADAR_PATH_AUTO = 0,   /* fused when the shape fits and either B * Hkv >=
-                            #CUs or one pair's step reads <= 256 KB; split
-                            otherwise                                       */
+                            #CUs or one pair's step reads <= 256 KB; else
+                            select when a pair's summary rows are <= 384 KB;
+                            split otherwise                                 */
   RADAR_PATH_SPLIT = 1,
-  RADAR_PATH_FUSED = 2   /* used when the shape fits (G <= 4, at most 1024
+  RADAR_PATH_FUSED = 2,  /* used when the shape fits (G <= 4, at most 1024
                             candidate segments, not fp32 with d = 128),
                             else split                                      */
+  RADAR_PATH_SELECT = 3  /* used when G <= 4 and at most 1024 candidate
+                            segments, else split                            */
 } radar_path;
 
 /* Choose the decode path for later calls from this host thread (default
@@ -220,8 +226,8 @@ typedef enum {
 radar_status radar_set_decode_path(int32_t path);
 
 /* The path radar_decode would take for this shape, t (the length, or the
- * bound of a ragged call's lengths) and k on this thread (RADAR_PATH_SPLIT or
- * RADAR_PATH_FUSED; -1 if the arguments are invalid). */
+ * bound of a ragged call's lengths) and k on this thread (RADAR_PATH_SPLIT,
+ * RADAR_PATH_FUSED or RADAR_PATH_SELECT; -1 if the arguments are invalid). */
 int32_t radar_decode_path(const radar_config* cfg, int64_t t, int32_t k);
 
 /* Kernel kinds reported by the measurement hook below. */
@@ -234,7 +240,8 @@ typedef enum {
   RADAR_K_ATTEND = 5,   /* gather-attention partials                       */
   RADAR_K_COMBINE = 6,  /* merge of the partials                           */
   RADAR_K_FUSED = 7,    /* the whole decode step, fused path               */
-  RADAR_K_COUNT = 8
+  RADAR_K_SELECT = 8,   /* phi(q) to union of one pair, select path        */
+  RADAR_K_COUNT = 9
 } radar_kernel;
 
 /* Measurement hook (not part of the method). While enabled on the calling

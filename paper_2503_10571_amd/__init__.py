@@ -261,7 +261,7 @@ def attend_selected(cfg: Config, q, K, V, selected, t: int, out=None,
 
 
 KERNELS = ("append", "build", "phi_q", "score", "topk", "attend", "combine",
-           "fused")
+           "fused", "select")
 
 
 def schedule_sqrt(t: int):
@@ -273,11 +273,12 @@ def schedule_sqrt(t: int):
     return c.value, w.value
 
 
-PATH_AUTO, PATH_SPLIT, PATH_FUSED = 0, 1, 2
+PATH_AUTO, PATH_SPLIT, PATH_FUSED, PATH_SELECT = 0, 1, 2, 3
 
 
 def set_decode_path(path: int) -> None:
-    """Force the split or fused decode path on this thread (0 = automatic)."""
+    """Force the split, fused or select decode path on this thread
+    (PATH_AUTO = automatic)."""
     _check("radar_set_decode_path", lib().radar_set_decode_path(path))
 
 

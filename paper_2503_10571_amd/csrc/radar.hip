@@ -1335,18 +1335,22 @@ __global__ __launch_bounds__(256) void k_attend(
 //   4. the group's union in LDS;
 //   5. every wave attends segment tiles (tile i to wave i mod 8);
 //   6. the waves' online-softmax states merge in LDS into the output.
+// With SEL set the kernel stops after phase 4 and writes the union to
+// uni_out / ucnt_out for the split path's attention (the select path: one
+// workgroup per pair replaces the phi(q), score and top-k kernels).
 constexpr int kFusedWaves = 8;
 constexpr int kFusedMaxG = 4;
 constexpr int kFusedMaxCand = 1024;
 
-template <typename T, int D, int G, int N>
+template <typename T, int D, int G, int N, bool SEL>
 __global__ __launch_bounds__(512) void k_decode_fused(
     const T* __restrict__ q, const T* __restrict__ K, const T* __restrict__ V,
     const float* __restrict__ omega, const float* __restrict__ summ,
     T* __restrict__ out, int32_t* __restrict__ selected,
     float* __restrict__ sel_scores, int Hq, int Hkv, int64_t cap,
     int64_t s_cap, int tiles_per_seg, SeqArgs sa, int per_head, float s1,
-    float s2, float inv_sqrt_n, float qscale) {
+    float s2, float inv_sqrt_n, float qscale, int* __restrict__ uni_out,
+    int* __restrict__ ucnt_out, int umax) {
   constexpr int NW = kFusedWaves;
   constexpr int QPL = D / 16;              // q elements per lane (phase 1)
   constexpr int FPL = N / 64;              // features per lane (phase 2)
@@ -1520,7 +1524,7 @@ __global__ __launch_bounds__(512) void k_decode_fused(
 
   // ---- 3. top-k (waves < G) | window and sink tiles (the other waves) ----
   TA ta;
-  ta.init(q0, qscale, lane);
+  if constexpr (!SEL) ta.init(q0, qscale, lane);
   const int win_tiles = (int)((t - ws + kTile - 1) / kTile);
   const int extra_tiles = win_tiles + (sp.sink + kTile - 1) / kTile;
   if (wave < G) {
@@ -1537,7 +1541,7 @@ __global__ __launch_bounds__(512) void k_decode_fused(
     else if (npl <= 4) head_topk<4>(src, n_cand, k, k_eff, row, so, sco, lane, hist, list);
     else if (npl <= 8) head_topk<8>(src, n_cand, k, k_eff, row, so, sco, lane, hist, list);
     else head_topk<16>(src, n_cand, k, k_eff, row, so, sco, lane, hist, list);
-  } else {
+  } else if constexpr (!SEL) {
     for (int i = wave - G; i < extra_tiles; i += NW - G) {
       int64_t start;
       int len;
@@ -1557,6 +1561,12 @@ __global__ __launch_bounds__(512) void k_decode_fused(
   // ---- 4. union -----------------------------------------------------------
   group_union(sel_lds, bits_lds, G, k_eff, per_head != 0, uni_lds, &ucnt_lds);
   __syncthreads();
+  if constexpr (SEL) {                     // hand the union to the split path
+    const int u = ucnt_lds;
+    for (int i = tid; i < u; i += NW * 64) uni_out[bh * umax + i] = uni_lds[i];
+    if (tid == 0) ucnt_out[bh] = u;
+    return;
+  }
   const int seg_tiles = ucnt_lds * tiles_per_seg;
 
   // ---- 5. segment tiles ---------------------------------------------------
@@ -1996,47 +2006,46 @@ void launch_segment_mass_d(const Shape& s, const void* q, const void* K, float* 
 // ---- fused path -------------------------------------------------------------
 thread_local int g_path_override = RADAR_PATH_AUTO;
 
-template <typename T, int D, int G, int N>
+// SEL: the select path (uni_out / ucnt_out / umax receive the union)
+template <typename T, int D, int G, int N, bool SEL>
 radar_status launch_fused_n(const Shape& s, const void* q, const void* K,
                             const void* V, const float* omega,
                             const float* summ, const SeqArgs& sa, void* out,
-                            int32_t* selected, float* sel_scores,
-                            hipStream_t st) {
+                            int32_t* selected, float* sel_scores, int* uni_out,
+                            int* ucnt_out, int umax, hipStream_t st) {
   const float s1 = kLog2e / std::pow((float)s.d, 0.25f);
   const float s2 = kLog2e / (2.f * std::sqrt((float)s.d));
-  launch(RADAR_K_FUSED, k_decode_fused<T, D, G, N>, dim3((unsigned)(s.B * s.Hkv)),
-         dim3(kFusedWaves * 64), 0, st, reinterpret_cast<const T*>(q),
-         reinterpret_cast<const T*>(K), reinterpret_cast<const T*>(V), omega, summ,
-         reinterpret_cast<T*>(out), selected, sel_scores, s.Hq, s.Hkv, s.cap,
-         s.s_cap, (int)ceil_div(s.c, kTile), sa, s.per_head, s1, s2,
-         1.f / std::sqrt((float)s.n), kLog2e / std::sqrt((float)s.d));
+  launch(SEL ? RADAR_K_SELECT : RADAR_K_FUSED, k_decode_fused<T, D, G, N, SEL>,
+         dim3((unsigned)(s.B * s.Hkv)), dim3(kFusedWaves * 64), 0, st,
+         reinterpret_cast<const T*>(q), reinterpret_cast<const T*>(K),
+         reinterpret_cast<const T*>(V), omega, summ, reinterpret_cast<T*>(out),
+         selected, sel_scores, s.Hq, s.Hkv, s.cap, s.s_cap, (int)ceil_div(s.c, kTile),
+         sa, s.per_head, s1, s2, 1.f / std::sqrt((float)s.n),
+         kLog2e / std::sqrt((float)s.d), uni_out, ucnt_out, umax);
   return launch_status();
 }
 
-template <typename T, int D, int G>
-radar_status launch_fused_g(const Shape& s, const void* q, const void* K,
-                            const void* V, const float* omega,
-                            const float* summ, const SeqArgs& sa, void* out,
-                            int32_t* selected, float* sel_scores,
-                            hipStream_t st) {
+#define RADAR_FUSED_ARGS s, q, K, V, omega, summ, sa, out, selected, sel_scores, uni_out, ucnt_out, umax, st
+#define RADAR_FUSED_PARAMS const Shape& s, const void* q, const void* K, const void* V, \
+    const float* omega, const float* summ, const SeqArgs& sa, void* out, int32_t* selected, \
+    float* sel_scores, int* uni_out, int* ucnt_out, int umax, hipStream_t st
+
+template <typename T, int D, int G, bool SEL>
+radar_status launch_fused_g(RADAR_FUSED_PARAMS) {
   switch (s.n) {
-    case 64: return launch_fused_n<T, D, G, 64>(s, q, K, V, omega, summ, sa, out, selected, sel_scores, st);
-    case 128: return launch_fused_n<T, D, G, 128>(s, q, K, V, omega, summ, sa, out, selected, sel_scores, st);
-    case 256: return launch_fused_n<T, D, G, 256>(s, q, K, V, omega, summ, sa, out, selected, sel_scores, st);
-    default: return launch_fused_n<T, D, G, 512>(s, q, K, V, omega, summ, sa, out, selected, sel_scores, st);
+    case 64: return launch_fused_n<T, D, G, 64, SEL>(RADAR_FUSED_ARGS);
+    case 128: return launch_fused_n<T, D, G, 128, SEL>(RADAR_FUSED_ARGS);
+    case 256: return launch_fused_n<T, D, G, 256, SEL>(RADAR_FUSED_ARGS);
+    default: return launch_fused_n<T, D, G, 512, SEL>(RADAR_FUSED_ARGS);
   }
 }
 
-template <typename T, int D>
-radar_status launch_fused_d(const Shape& s, const void* q, const void* K,
-                            const void* V, const float* omega,
-                            const float* summ, const SeqArgs& sa, void* out,
-                            int32_t* selected, float* sel_scores,
-                            hipStream_t st) {
+template <typename T, int D, bool SEL>
+radar_status launch_fused_d(RADAR_FUSED_PARAMS) {
   switch (s.G) {
-    case 1: return launch_fused_g<T, D, 1>(s, q, K, V, omega, summ, sa, out, selected, sel_scores, st);
-    case 2: return launch_fused_g<T, D, 2>(s, q, K, V, omega, summ, sa, out, selected, sel_scores, st);
-    default: return launch_fused_g<T, D, 4>(s, q, K, V, omega, summ, sa, out, selected, sel_scores, st);
+    case 1: return launch_fused_g<T, D, 1, SEL>(RADAR_FUSED_ARGS);
+    case 2: return launch_fused_g<T, D, 2, SEL>(RADAR_FUSED_ARGS);
+    default: return launch_fused_g<T, D, 4, SEL>(RADAR_FUSED_ARGS);
   }
 }
 
@@ -2045,15 +2054,38 @@ radar_status launch_fused(const Shape& s, const void* q, const void* K, const vo
                           const float* omega, const float* summ, const SeqArgs& sa,
                           void* out, int32_t* selected, float* sel_scores,
                           hipStream_t st) {
+  int* uni_out = nullptr;
+  int* ucnt_out = nullptr;
+  const int umax = 0;
   if (s.dt == RADAR_BF16)
-    return s.d == 64 ? launch_fused_d<bf16_t, 64>(s, q, K, V, omega, summ, sa, out, selected, sel_scores, st)
-                     : launch_fused_d<bf16_t, 128>(s, q, K, V, omega, summ, sa, out, selected, sel_scores, st);
+    return s.d == 64 ? launch_fused_d<bf16_t, 64, false>(RADAR_FUSED_ARGS)
+                     : launch_fused_d<bf16_t, 128, false>(RADAR_FUSED_ARGS);
   // fp32 caches with d = 128 keep the split path: their tiles need more
   // registers than the fused kernel has to spare
-  if (s.d == 64)
-    return launch_fused_d<float, 64>(s, q, K, V, omega, summ, sa, out, selected, sel_scores, st);
+  if (s.d == 64) return launch_fused_d<float, 64, false>(RADAR_FUSED_ARGS);
   return RADAR_EUNSUPPORTED;
 }
+
+// the select path's first kernel: phi(q), scores, top-k and union of each
+// pair in one workgroup, the union into the workspace
+radar_status launch_select(const Shape& s, const void* q, const float* omega,
+                           const float* summ, const SeqArgs& sa, int32_t* selected,
+                           float* sel_scores, unsigned char* w, const WsLayout& L,
+                           hipStream_t st) {
+  const void* K = nullptr;
+  const void* V = nullptr;
+  void* out = nullptr;
+  int* uni_out = reinterpret_cast<int*>(w + L.uni);
+  int* ucnt_out = reinterpret_cast<int*>(w + L.ucnt);
+  const int umax = L.umax;
+  if (s.dt == RADAR_BF16)
+    return s.d == 64 ? launch_fused_d<bf16_t, 64, true>(RADAR_FUSED_ARGS)
+                     : launch_fused_d<bf16_t, 128, true>(RADAR_FUSED_ARGS);
+  return s.d == 64 ? launch_fused_d<float, 64, true>(RADAR_FUSED_ARGS)
+                   : launch_fused_d<float, 128, true>(RADAR_FUSED_ARGS);
+}
+#undef RADAR_FUSED_ARGS
+#undef RADAR_FUSED_PARAMS
 
 // A pair's HBM bytes in one decode step at length t (summary rows plus the
 // K/V of the largest union, the window and the sinks), the quantity one
@@ -2066,18 +2098,31 @@ int64_t pair_bytes(const Shape& s, const SeqArgs& sa) {
          (u * s.c + (sp.t - sp.ws) + sp.sink) * 2 * s.d * skv;
 }
 
-// Which decode path a call takes. Fused when the shape fits its LDS plan and
-// either there are enough (b, kv head) pairs to occupy every CU, or each
-// pair's step is small enough (<= 256 KB) that one workgroup streams it in a
-// few microseconds, less than the split path's extra launches cost.
+// Which decode path a call takes.
+//  - fused: the shape fits its LDS plan and either there are enough (b, kv
+//    head) pairs to occupy every CU, or each pair's step is small enough
+//    (<= 256 KB) that one workgroup streams it in a few microseconds, less
+//    than the split path's extra launches cost;
+//  - select: otherwise, when a pair's summary rows fit one workgroup's
+//    stream (<= 384 KB, about 13 us at a CU's share of HBM): one workgroup per
+//    pair selects, then the split attention spreads the K/V gather over the
+//    chip (measured: the one select kernel beats the three it replaces up to
+//    about 500 KB per pair);
+//  - split: phi(q), scores and top-k as separate chip-wide kernels.
 int choose_path(const Shape& s, const SeqArgs& sa) {
   const int n_cand = make_span(sa.t_max, sa).n_cand;
-  const bool fits = s.G <= kFusedMaxG && n_cand <= kFusedMaxCand &&
-                    !(s.dt == RADAR_F32 && s.d == 128);
-  if (!fits || g_path_override == RADAR_PATH_SPLIT) return RADAR_PATH_SPLIT;
-  if (g_path_override == RADAR_PATH_FUSED) return RADAR_PATH_FUSED;
-  if ((int64_t)s.B * s.Hkv >= num_cu()) return RADAR_PATH_FUSED;
-  return pair_bytes(s, sa) <= (256 << 10) ? RADAR_PATH_FUSED : RADAR_PATH_SPLIT;
+  const bool fits_select = s.G <= kFusedMaxG && n_cand <= kFusedMaxCand;
+  const bool fits_fused = fits_select && !(s.dt == RADAR_F32 && s.d == 128);
+  switch (g_path_override) {
+    case RADAR_PATH_SPLIT: return RADAR_PATH_SPLIT;
+    case RADAR_PATH_FUSED: return fits_fused ? RADAR_PATH_FUSED : RADAR_PATH_SPLIT;
+    case RADAR_PATH_SELECT: return fits_select ? RADAR_PATH_SELECT : RADAR_PATH_SPLIT;
+    default: break;
+  }
+  if (fits_fused && ((int64_t)s.B * s.Hkv >= num_cu() || pair_bytes(s, sa) <= (256 << 10)))
+    return RADAR_PATH_FUSED;
+  if (fits_select && (int64_t)n_cand * s.n * 4 <= (384 << 10)) return RADAR_PATH_SELECT;
+  return RADAR_PATH_SPLIT;
 }
 
 // Argument checks shared by the decode-side calls: pointers, k, the length
@@ -2119,7 +2164,8 @@ radar_status radar_schedule_sqrt(int64_t t, int32_t* seg_len, int32_t* window) {
 }
 
 radar_status radar_set_decode_path(int32_t path) {
-  if (path != RADAR_PATH_AUTO && path != RADAR_PATH_SPLIT && path != RADAR_PATH_FUSED)
+  if (path != RADAR_PATH_AUTO && path != RADAR_PATH_SPLIT && path != RADAR_PATH_FUSED &&
+      path != RADAR_PATH_SELECT)
     return RADAR_EINVAL;
   g_path_override = path;
   return RADAR_OK;
@@ -2275,7 +2321,8 @@ radar_status radar_decode(const radar_config* cfg, const void* q, const void* K,
   const void* Kp = after_sinks(s, K);
   const void* Vp = after_sinks(s, V);
 
-  if (choose_path(s, sa) == RADAR_PATH_FUSED)
+  const int path = choose_path(s, sa);
+  if (path == RADAR_PATH_FUSED)
     return launch_fused(s, q, Kp, Vp, omega, summaries, sa, out, selected, scores,
                         stream);
 
@@ -2284,6 +2331,11 @@ radar_status radar_decode(const radar_config* cfg, const void* q, const void* K,
   if (ag.grid_x > kMaxWg) return RADAR_EUNSUPPORTED;
 
   unsigned char* w = reinterpret_cast<unsigned char*>(workspace);
+  if (path == RADAR_PATH_SELECT) {
+    r = launch_select(s, q, omega, summaries, sa, selected, scores, w, L, stream);
+    if (r != RADAR_OK) return r;
+    return launch_attend(s, q, Kp, Vp, ag, sa, out, w, L, stream);
+  }
   float* phiq = reinterpret_cast<float*>(w + L.phiq);
   float* sc = reinterpret_cast<float*>(w + L.scores);
   if (top.n_cand > 0) {

@@ -32,8 +32,9 @@ def _announce(name):
     print(f"[case] {name}", flush=True)
 
 
-PATHS = pytest.mark.parametrize("path", [radar.PATH_SPLIT, radar.PATH_FUSED],
-                                ids=["split", "fused"])
+PATHS = pytest.mark.parametrize("path", [radar.PATH_SPLIT, radar.PATH_FUSED,
+                                 radar.PATH_SELECT],
+                                ids=["split", "fused", "select"])
 
 
 def _run(wl, steps, groups=None, check_steps=None, path=radar.PATH_AUTO):
@@ -104,8 +105,8 @@ def test_full_size_sampled(name, steps, ngroups, path):
 
 def test_path_choice():
     """The fused path serves shapes with at least one (b, kv head) pair per
-    CU, or small steps; G > 4 or more than 1024 candidates take the split
-    path."""
+    CU, or small steps; the select path few pairs with few candidates; G > 4
+    or more than 1024 candidates take the split path."""
     def cfg(wl):
         return H.config_of(wl, wl.t0 + 1)
     n_cu = torch.cuda.get_device_properties(0).multi_processor_count
@@ -119,11 +120,18 @@ def test_path_choice():
     assert radar.decode_path(cfg(tiny), tiny.t0 + 1, tiny.top_k) == radar.PATH_FUSED
     g8 = mha.scaled(n_q_heads=32, n_kv_heads=4, batch=128)
     assert radar.decode_path(cfg(g8), g8.t0 + 1, 16) == radar.PATH_SPLIT
+    # few pairs whose summary rows fit one workgroup's stream: select
+    for name in ("llama2_16k", "gqa_64k"):
+        w = WORKLOADS[name]
+        assert radar.decode_path(cfg(w), w.t0 + 1, w.top_k) == radar.PATH_SELECT, name
     radar.set_decode_path(radar.PATH_FUSED)
     try:
         assert radar.decode_path(cfg(g5), g5.t0 + 1, g5.top_k) == radar.PATH_FUSED
         many = mha.scaled(seg_len=64, window=64)           # 2047 candidates
         assert radar.decode_path(cfg(many), many.t0 + 1, 16) == radar.PATH_SPLIT
+        radar.set_decode_path(radar.PATH_SELECT)
+        assert radar.decode_path(cfg(g5), g5.t0 + 1, g5.top_k) == radar.PATH_SELECT
+        assert radar.decode_path(cfg(g8), g8.t0 + 1, 16) == radar.PATH_SPLIT
     finally:
         radar.set_decode_path(radar.PATH_AUTO)
 

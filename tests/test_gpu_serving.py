@@ -27,8 +27,9 @@ from oracle import radar_oracle as orc  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 
-PATHS = pytest.mark.parametrize("path", [radar.PATH_SPLIT, radar.PATH_FUSED],
-                                ids=["split", "fused"])
+PATHS = pytest.mark.parametrize("path", [radar.PATH_SPLIT, radar.PATH_FUSED,
+                                 radar.PATH_SELECT],
+                                ids=["split", "fused", "select"])
 
 
 def _edge(name, **kw):
