@@ -171,6 +171,14 @@ EDGES = [
           dtype="f32", n_features=512),
     _edge("n512_b3", batch=3, t0=1200, seg_len=48, window=50, n_features=512,
           top_k=6, keys="clustered"),
+    # the largest k the library takes, with more candidates than k
+    _edge("k256", t0=1100, seg_len=4, window=16, top_k=256, n_features=64,
+          keys="clustered"),
+    # exactly the largest candidate count (2048 one-token segments)
+    _edge("cand2048", t0=2055, seg_len=1, window=8, top_k=17, n_features=64,
+          keys="clustered"),
+    # a context that starts at one token and grows into segments
+    _edge("t_one", t0=1, seg_len=4, window=4, top_k=2),
 ]
 
 
@@ -178,6 +186,8 @@ EDGES = [
 @pytest.mark.parametrize("wl", EDGES, ids=[w.name for w in EDGES])
 def test_edge(wl, path):
     steps = 70 if wl.seg_len <= 64 else 8
+    if wl.name == "cand2048":
+        steps = 1                          # one more step would pass 2048
     _run(wl, steps, path=path)
 
 
