@@ -282,6 +282,11 @@ def main():
                     help="also run a plain 1 GiB read+write elementwise "
                          "kernel: the box's copy bandwidth (and the counter "
                          "calibration for HBM traffic)")
+    ap.add_argument("--graph", type=int, default=0,
+                    help="1: capture the timed steps (the same library calls "
+                         "as the eager loop) into one HIP graph and time its "
+                         "replay, so host launch overhead is not timed; 0: "
+                         "time the eager launches")
     ap.add_argument("--peaks", type=int, default=1,
                     help="measure the sustained bf16 MFMA and exp2 rates "
                          "(the index build's two resources)")
@@ -371,11 +376,26 @@ def main():
     t_timed = wl.t0 + W
     seg_timed, win_timed = stp.cfg_c.seg_len, stp.cfg_c.window
     restr_before = stp.restructures
-    log(f"[bench] timing {Ksteps} steps")
-    e0.record()
-    for j in range(Ksteps):
-        stp.step(W + j, ctypes.c_void_p(sel_log[j].data_ptr()))
-    e1.record()
+    log(f"[bench] timing {Ksteps} steps" + (" (graph replay)" if args.graph else ""))
+    sel_ptrs = [ctypes.c_void_p(sel_log[j].data_ptr()) for j in range(Ksteps)]
+    if args.graph:
+        # capture records the launches without running them; the replay runs
+        # exactly the steps the eager loop would
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            stp.stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+            for j in range(Ksteps):
+                stp.step(W + j, sel_ptrs[j])
+        stp.stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+        e0.record()
+        graph.replay()
+        e1.record()
+    else:
+        e0.record()
+        for j in range(Ksteps):
+            stp.step(W + j, sel_ptrs[j])
+        e1.record()
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1)
     ms_step = ms / Ksteps
@@ -479,6 +499,7 @@ def main():
             "decode_path": {radar.PATH_SPLIT: "split", radar.PATH_FUSED: "fused",
                             radar.PATH_SELECT: "select"}.get(path, "?"),
             "schedule": args.schedule,
+            "launch": "hip graph replay" if args.graph else "eager",
             "selector": args.selector,
             "restructures": restructures,
         },
