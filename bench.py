@@ -1,9 +1,10 @@
 """Decode throughput of the Radar path on one MI355X.
 
-A step is one pass of the whole path for one token of every sequence:
-radar_append (k/v row write, plus the summary refresh when a segment fills)
-followed by radar_decode (phi(q), segment scores, top-k, union, gather
-attention, combine) for every (batch, query head). Inputs are seeded
+A step is one pass of the whole path for one token of every sequence: the
+append (k/v row write, plus the summary refresh when a segment fills) and the
+decode (phi(q), segment scores, top-k, union, gather attention, combine) for
+every (batch, query head), as one radar_append_decode call (or, with
+--merged 0, radar_append followed by radar_decode). Inputs are seeded
 synthetic tensors already resident in HBM; the default workload is the
 long-context MHA layer: batch 8, 32 heads, head_dim 128, 128K context,
 segment length 256, top-16 segments, 256 random features, recent window 256,
@@ -55,10 +56,11 @@ class Stepper:
     cost stays small next to the GPU time)."""
 
     def __init__(self, cfg, inp, K, V, summ, ws, out, k, sqrt_schedule=False,
-                 exact=False):
+                 exact=False, merged=True):
         self.L = radar.lib()
         self.sqrt = sqrt_schedule
         self.exact = exact
+        self.merged = merged
         self.restructures = 0
         self.cfg_c = cfg.c_struct()
         self.cfgp = ctypes.byref(self.cfg_c)
@@ -78,6 +80,18 @@ class Stepper:
 
     def step(self, i, sel=None):
         t = self.t0 + i
+        if self.merged and not self.exact:
+            c = math.isqrt(t + 1) if self.sqrt else self.cfg_c.seg_len
+            if c == self.cfg_c.seg_len:       # no restructure at this token
+                if self.sqrt:
+                    self.cfg_c.window = t + 1 - c * c
+                st = self.L.radar_append_decode(
+                    self.cfgp, self.q[i], self.K, self.V, self.kn[i], self.vn[i],
+                    self.om, self.summ, t + 1, None, self.k, self.out, sel, None,
+                    self.ws, self.ws_n, self.stream)
+                if st:
+                    raise radar.RadarError("radar_append_decode", st)
+                return
         st = self.L.radar_append(self.cfgp, self.K, self.V, self.kn[i],
                                  self.vn[i], self.om, t, None, self.summ,
                                  self.stream)
@@ -122,9 +136,9 @@ def union_sizes(sel, G):
 def step_bytes(wl, t, U, s_kv, sqrt_schedule=False, exact=False):
     """Algorithmic HBM bytes of one step whose decode runs at length t (the
     append wrote row t - 1). U: union size per (b, kv head).
-    Returns (whole step, decode call, K/V gather, candidate-key scan); with
-    exact=True the selection scans every candidate key instead of reading
-    phi(q)'s inputs and the summaries."""
+    Returns (whole step, decode call, K/V gather, candidate-key scan, row
+    append); with exact=True the selection scans every candidate key
+    instead of reading phi(q)'s inputs and the summaries."""
     d, n = wl.head_dim, wl.n_features
     if sqrt_schedule:
         c, w = radar.schedule_sqrt(t)
@@ -137,13 +151,13 @@ def step_bytes(wl, t, U, s_kv, sqrt_schedule=False, exact=False):
     kv = int(np.sum(U * c + W)) * d * 2 * s_kv
     qo = wl.batch * wl.n_q_heads * d * 2 * s_kv
     om = n * d * 4
-    app = BH * 2 * d * s_kv
+    app = BH * 4 * d * s_kv            # read k_new, v_new; write both rows
     close = BH * (c * d * s_kv + n * 4) if t % c == 0 else 0
     if sqrt_schedule and w == 0:       # restructure: all t keys re-summarised
         close += BH * (t * d * s_kv + (t // c) * n * 4)
     scan = BH * n_cand * c * d * s_kv
     decode = (scan if exact else summ + om) + kv + qo
-    return decode + app + close, decode, kv, scan
+    return decode + app + close, decode, kv, scan, app
 
 
 def measured_traffic(kernel, workload):
@@ -282,6 +296,10 @@ def main():
                     help="also run a plain 1 GiB read+write elementwise "
                          "kernel: the box's copy bandwidth (and the counter "
                          "calibration for HBM traffic)")
+    ap.add_argument("--merged", type=int, default=1,
+                    help="1: one radar_append_decode call per step (the row "
+                         "write runs inside the decode's first kernel); 0: "
+                         "radar_append then radar_decode")
     ap.add_argument("--graph", type=int, default=0,
                     help="1: capture the timed steps (the same library calls "
                          "as the eager loop) into one HIP graph and time its "
@@ -365,8 +383,10 @@ def main():
     build_exps = n_keys * wl.n_features / (build_ms * 1e-3) / 1e12   # 10^12 / s
 
     # ---- decode steps ----------------------------------------------------
+    merged = bool(args.merged) and not exact
     stp = Stepper(cfg, inp, K, V, summ, ws, out, wl.top_k,
-                  sqrt_schedule=args.schedule == "sqrt", exact=exact)
+                  sqrt_schedule=args.schedule == "sqrt", exact=exact,
+                  merged=merged)
     sel_log = torch.empty(Ksteps, wl.batch, wl.n_q_heads, wl.top_k,
                           dtype=torch.int32, device=K.device)
     log(f"[bench] warmup {W} steps")
@@ -421,10 +441,11 @@ def main():
     for j in range(Ksteps):
         t = wl.t0 + W + j + 1
         U = union_sizes(sel_np[j], wl.group)
-        b_all, b_dec, b_kv, b_scan = step_bytes(
+        b_all, b_dec, b_kv, b_scan, b_app = step_bytes(
             wl, t, U, s_kv, sqrt_schedule=args.schedule == "sqrt", exact=exact)
         tot_bytes += b_all
-        dec_bytes += b_dec
+        # with the merged call the fused kernel also does the row append
+        dec_bytes += b_dec + (b_app if merged else 0)
         kv_bytes += b_kv
         scan_bytes += b_scan
     step_gbps = tot_bytes / (ms * 1e-3) / 1e9
@@ -500,6 +521,8 @@ def main():
                             radar.PATH_SELECT: "select"}.get(path, "?"),
             "schedule": args.schedule,
             "launch": "hip graph replay" if args.graph else "eager",
+            "calls": ("radar_append_decode" if merged
+                      else "radar_append + radar_decode"),
             "selector": args.selector,
             "restructures": restructures,
         },

@@ -86,7 +86,7 @@
 extern "C" {
 #endif
 
-#define RADAR_ABI_VERSION 2
+#define RADAR_ABI_VERSION 3
 
 typedef enum {
   RADAR_OK = 0,
@@ -156,6 +156,31 @@ radar_status radar_decode(const radar_config* cfg, const void* q,
                           int32_t* selected, float* scores, void* workspace,
                           size_t workspace_bytes, hipStream_t stream);
 
+/* One decode step with its append (Algorithm 1: the new key joins W, then
+ * the query step), the same result as radar_append(..., t - 1, pos, ...)
+ * followed by radar_decode(..., t, lens = pos + 1, ...), in fewer kernels:
+ * the first per-(b, kv head) kernel of the decode writes the new rows
+ * k_new / v_new ([B][Hkv][d]) before the attention reads them, and the
+ * summary of a segment the rows complete is computed after the decode, with
+ * radar_append's code (that segment lies inside W at this step, so the
+ * decode does not read its summary; with w = 0 it would, and the call then
+ * runs append, refresh and decode in that order).
+ * t: the context length after the append, 1 <= t <= capacity. Without pos
+ * every sequence writes row t - 1 and attends t tokens. With pos (nullable,
+ * device int64 [B]) sequence b writes row pos[b] (skipped outside
+ * [0, capacity), as radar_append) and is decoded at length pos[b] + 1, with
+ * t their bound: a pos[b] outside [0, t) makes that sequence's outputs NaN
+ * and its ids -1 (see Ragged batches). Everything else as for radar_append
+ * and radar_decode; the workspace is radar_decode's. */
+radar_status radar_append_decode(const radar_config* cfg, const void* q,
+                                 void* K, void* V, const void* k_new,
+                                 const void* v_new, const float* omega,
+                                 float* summaries, int64_t t,
+                                 const int64_t* pos, int32_t k, void* out,
+                                 int32_t* selected, float* scores,
+                                 void* workspace, size_t workspace_bytes,
+                                 hipStream_t stream);
+
 /* Exact segment search (the exact-selection ablation of Section 3.3): like
  * radar_decode, but each query head selects the k candidate segments with
  * the largest exact attention mass beta_s = sum over the segment's keys of
@@ -171,8 +196,8 @@ radar_status radar_decode_exact(const radar_config* cfg, const void* q,
                                 void* workspace, size_t workspace_bytes,
                                 hipStream_t stream);
 
-/* Scratch bytes radar_decode, radar_decode_exact and radar_attend_selected
- * need for this shape and k (0 if cfg is invalid). */
+/* Scratch bytes radar_decode, radar_append_decode, radar_decode_exact and
+ * radar_attend_selected need for this shape and k (0 if cfg is invalid). */
 size_t radar_decode_workspace_bytes(const radar_config* cfg, int32_t k);
 
 /* Exact attention over caller-chosen segments (the last step of Algorithm 1

@@ -17,7 +17,7 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libradar.so")
 
-ABI_VERSION = 2
+ABI_VERSION = 3
 RADAR_F32, RADAR_BF16 = 0, 1
 GQA_UNION, GQA_PER_HEAD = 0, 1
 STATUS = {0: "ok", 1: "invalid argument", 2: "position outside the cache capacity",
@@ -98,6 +98,8 @@ def lib() -> ctypes.CDLL:
                                    _P, _P, _P, sz, _P]
         L.radar_decode_exact.argtypes = [cfgp, _P, _P, _P, i64, _P, i32, _P, _P,
                                          _P, _P, sz, _P]
+        L.radar_append_decode.argtypes = [cfgp, _P, _P, _P, _P, _P, _P, _P, i64,
+                                          _P, i32, _P, _P, _P, _P, sz, _P]
         L.radar_decode_workspace_bytes.argtypes = [cfgp, i32]
         L.radar_decode_workspace_bytes.restype = sz
         L.radar_attend_selected.argtypes = [cfgp, _P, _P, _P, _P, i32, i64, _P,
@@ -121,7 +123,8 @@ def lib() -> ctypes.CDLL:
         for fn in ("radar_peak_mfma", "radar_peak_exp"):
             getattr(L, fn).restype = ctypes.c_int
         for fn in ("radar_build_index", "radar_append", "radar_decode",
-                   "radar_decode_exact", "radar_attend_selected",
+                   "radar_append_decode", "radar_decode_exact",
+                   "radar_attend_selected",
                    "radar_profile_enable", "radar_profile_read"):
             getattr(L, fn).restype = ctypes.c_int
         _lib = L
@@ -142,13 +145,47 @@ def _check(fn, st):
         raise RadarError(fn, st, detail)
 
 
-def _need(x, dtype, name):
+def _need(x, dtype, name, numel=None, at_least=False):
+    """Device, dtype and layout checks; numel: the element count the kernels
+    address for this argument (exactly, or at least with at_least), so that
+    a tensor of the wrong size is refused before any kernel reads or writes
+    past its end."""
     if not x.is_cuda:
         raise ValueError(f"{name} must be a device tensor")
     if x.dtype != dtype:
         raise ValueError(f"{name} must be {dtype}, got {x.dtype}")
     if not x.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
+    if numel is not None and (x.numel() < numel if at_least else x.numel() != numel):
+        raise ValueError(f"{name} holds {x.numel()} elements, the config needs "
+                         f"{'at least ' if at_least else ''}{numel}")
+
+
+def _cache(cfg, K, V=None):
+    n = cfg.batch * cfg.n_kv_heads * cfg.capacity * cfg.head_dim
+    _need(K, cfg.dtype, "K", n)
+    if V is not None:
+        _need(V, cfg.dtype, "V", n)
+
+
+def _rows(cfg, k_new, v_new):
+    n = cfg.batch * cfg.n_kv_heads * cfg.head_dim
+    _need(k_new, cfg.dtype, "k_new", n)
+    _need(v_new, cfg.dtype, "v_new", n)
+
+
+def _query(cfg, q):
+    _need(q, cfg.dtype, "q", cfg.batch * cfg.n_q_heads * cfg.head_dim)
+
+
+def _omega(cfg, omega):
+    _need(omega, torch.float32, "omega", cfg.n_features * cfg.head_dim)
+
+
+def _summ(cfg, summaries):
+    rows = max(1, cfg.summary_rows)
+    _need(summaries, torch.float32, "summaries",
+          cfg.batch * cfg.n_kv_heads * rows * cfg.n_features, at_least=True)
 
 
 def workspace_bytes(cfg: Config, k: int) -> int:
@@ -169,8 +206,7 @@ def new_summaries(cfg: Config, device) -> torch.Tensor:
 
 def build_index(cfg: Config, K, omega, t: int, summaries) -> None:
     """radar_build_index: summaries of the floor(t / c) full segments."""
-    _need(K, cfg.dtype, "K"); _need(omega, torch.float32, "omega")
-    _need(summaries, torch.float32, "summaries")
+    _cache(cfg, K); _omega(cfg, omega); _summ(cfg, summaries)
     _check("radar_build_index", lib().radar_build_index(
         ctypes.byref(cfg.c_struct()), _ptr(K), _ptr(omega), t, _ptr(summaries),
         _stream(K)))
@@ -190,9 +226,8 @@ def append(cfg: Config, K, V, k_new, v_new, omega, t: int, summaries,
            pos=None) -> None:
     """radar_append: write row t (or row pos[b] of sequence b); refresh the
     summary of a segment the row completes."""
-    for x, nm in ((K, "K"), (V, "V"), (k_new, "k_new"), (v_new, "v_new")):
-        _need(x, cfg.dtype, nm)
-    _need(omega, torch.float32, "omega"); _need(summaries, torch.float32, "summaries")
+    _cache(cfg, K, V); _rows(cfg, k_new, v_new)
+    _omega(cfg, omega); _summ(cfg, summaries)
     pos = _lens(pos, cfg, "pos")
     _check("radar_append", lib().radar_append(
         ctypes.byref(cfg.c_struct()), _ptr(K), _ptr(V), _ptr(k_new), _ptr(v_new),
@@ -202,12 +237,15 @@ def append(cfg: Config, K, V, k_new, v_new, omega, t: int, summaries,
 def _outputs(cfg, q, k, out, selected, scores, workspace):
     if out is None:
         out = torch.empty_like(q)
+    _need(out, cfg.dtype, "out", cfg.batch * cfg.n_q_heads * cfg.head_dim)
     if workspace is None:
         workspace = new_workspace(cfg, k, q.device)
+    _need(workspace, torch.uint8, "workspace")
+    n_sel = cfg.batch * cfg.n_q_heads * k
     if selected is not None:
-        _need(selected, torch.int32, "selected")
+        _need(selected, torch.int32, "selected", n_sel, at_least=True)
     if scores is not None:
-        _need(scores, torch.float32, "scores")
+        _need(scores, torch.float32, "scores", n_sel, at_least=True)
     return out, workspace
 
 
@@ -216,9 +254,7 @@ def decode(cfg: Config, q, K, V, omega, summaries, t: int, k: int, out=None,
     """radar_decode: one query per (b, q head) at context length t (or at
     lens[b] <= t per sequence). Returns out (and writes the optional
     selected / scores tensors)."""
-    for x, nm in ((q, "q"), (K, "K"), (V, "V")):
-        _need(x, cfg.dtype, nm)
-    _need(omega, torch.float32, "omega"); _need(summaries, torch.float32, "summaries")
+    _query(cfg, q); _cache(cfg, K, V); _omega(cfg, omega); _summ(cfg, summaries)
     lens = _lens(lens, cfg, "lens")
     out, workspace = _outputs(cfg, q, k, out, selected, scores, workspace)
     _check("radar_decode", lib().radar_decode(
@@ -228,12 +264,30 @@ def decode(cfg: Config, q, K, V, omega, summaries, t: int, k: int, out=None,
     return out
 
 
+def append_decode(cfg: Config, q, K, V, k_new, v_new, omega, summaries,
+                  t: int, k: int, out=None, selected=None, scores=None,
+                  workspace=None, pos=None):
+    """radar_append_decode: append row t - 1 (row pos[b] of sequence b) and
+    decode at context length t (pos[b] + 1, bounded by t) in one call, the
+    same result as append(..., t - 1, pos=pos) then decode(..., t,
+    lens=pos + 1). Returns out."""
+    _query(cfg, q); _cache(cfg, K, V); _rows(cfg, k_new, v_new)
+    _omega(cfg, omega); _summ(cfg, summaries)
+    pos = _lens(pos, cfg, "pos")
+    out, workspace = _outputs(cfg, q, k, out, selected, scores, workspace)
+    _check("radar_append_decode", lib().radar_append_decode(
+        ctypes.byref(cfg.c_struct()), _ptr(q), _ptr(K), _ptr(V), _ptr(k_new),
+        _ptr(v_new), _ptr(omega), _ptr(summaries), t, _ptr(pos), k, _ptr(out),
+        _ptr(selected), _ptr(scores), _ptr(workspace), workspace.numel(),
+        _stream(q)))
+    return out
+
+
 def decode_exact(cfg: Config, q, K, V, t: int, k: int, out=None,
                  selected=None, scores=None, workspace=None, lens=None):
     """radar_decode_exact: top-k segments by exact attention mass, then the
     same attention as decode(). scores receives ln(beta) of the picks."""
-    for x, nm in ((q, "q"), (K, "K"), (V, "V")):
-        _need(x, cfg.dtype, nm)
+    _query(cfg, q); _cache(cfg, K, V)
     lens = _lens(lens, cfg, "lens")
     out, workspace = _outputs(cfg, q, k, out, selected, scores, workspace)
     _check("radar_decode_exact", lib().radar_decode_exact(
@@ -247,11 +301,10 @@ def attend_selected(cfg: Config, q, K, V, selected, t: int, out=None,
                     workspace=None, lens=None):
     """radar_attend_selected: exact attention over given segment ids plus
     the sinks and W."""
-    for x, nm in ((q, "q"), (K, "K"), (V, "V")):
-        _need(x, cfg.dtype, nm)
-    _need(selected, torch.int32, "selected")
-    lens = _lens(lens, cfg, "lens")
+    _query(cfg, q); _cache(cfg, K, V)
     k = selected.shape[-1]
+    _need(selected, torch.int32, "selected", cfg.batch * cfg.n_q_heads * k)
+    lens = _lens(lens, cfg, "lens")
     out, workspace = _outputs(cfg, q, k, out, None, None, workspace)
     _check("radar_attend_selected", lib().radar_attend_selected(
         ctypes.byref(cfg.c_struct()), _ptr(q), _ptr(K), _ptr(V), _ptr(selected),
@@ -330,7 +383,8 @@ def peak_rates(device="cuda", iters=4096) -> dict:
 
 class RadarLayer:
     """Device state of one Radar layer: K/V cache, summaries, Omega and a
-    decode workspace, driven through the C ABI (append, then decode).
+    decode workspace, driven through the C ABI (append, then decode, or
+    both in one step).
 
     schedule="fixed" keeps cfg.seg_len and cfg.window. schedule="sqrt"
     follows Algorithm 1's restructuring: at every perfect-square context
@@ -378,10 +432,28 @@ class RadarLayer:
                 self.restructures += 1
 
     def decode(self, q, out=None, selected=None, scores=None):
+        self._fit_workspace()
+        return decode(self.cfg, q, self.K, self.V, self.omega, self.summaries,
+                      self.t, self.k, out=out, selected=selected, scores=scores,
+                      workspace=self.workspace)
+
+    def step(self, q, k_new, v_new, out=None, selected=None, scores=None):
+        """append(k_new, v_new) then decode(q), as one radar_append_decode
+        call unless the sqrt schedule restructures at this token."""
+        if self.schedule == "sqrt" and self._cfg_at(self.t + 1).seg_len != self.cfg.seg_len:
+            self.append(k_new, v_new)
+            return self.decode(q, out=out, selected=selected, scores=scores)
+        if self.schedule == "sqrt":
+            self.cfg = self._cfg_at(self.t + 1)
+        self._fit_workspace()
+        self.t += 1
+        return append_decode(self.cfg, q, self.K, self.V, k_new, v_new,
+                             self.omega, self.summaries, self.t, self.k,
+                             out=out, selected=selected, scores=scores,
+                             workspace=self.workspace)
+
+    def _fit_workspace(self):
         # the scratch size follows the window, which grows between
         # restructures under the sqrt schedule
         if workspace_bytes(self.cfg, self.k) > self.workspace.numel():
             self.workspace = new_workspace(self.cfg, self.k, self.K.device)
-        return decode(self.cfg, q, self.K, self.V, self.omega, self.summaries,
-                      self.t, self.k, out=out, selected=selected, scores=scores,
-                      workspace=self.workspace)

@@ -68,6 +68,8 @@ struct SeqArgs {
   const int64_t* lens;  // [B] per-sequence lengths (device), or null: all t_max
   int64_t t_max;
   int c, w, n_sink, k;
+  int lens_add = 0;     // 1: lens holds append rows, a sequence's length is
+                        // its row + 1 (0, invalid, unless row < t_max)
 };
 
 // Lengths stay below 2^31 (the capacity limit), so the split is computed in
@@ -91,7 +93,35 @@ __host__ __device__ inline Span make_span(int64_t len, const SeqArgs& a) {
 }
 
 __device__ __forceinline__ Span seq_span(const SeqArgs& a, int64_t b) {
-  return make_span(a.lens ? a.lens[b] : a.t_max, a);
+  if (!a.lens) return make_span(a.t_max, a);
+  const int64_t v = a.lens[b];
+  if (!a.lens_add) return make_span(v, a);
+  return make_span(v >= 0 && v < a.t_max ? v + 1 : 0, a);
+}
+
+// The k / v row write of an append. radar_append runs it as its own kernel;
+// radar_append_decode runs it inside the per-(b, kv head) kernel that
+// precedes every read of the row, one wave per pair.
+struct AppendArgs {
+  uint4* K;                // cache base (row 0 of pair 0); null: no append
+  uint4* V;
+  const uint4* kn;         // [B][Hkv] rows of the new keys / values
+  const uint4* vn;
+  const int64_t* pos;      // [B] row of sequence b, or null: row t for all
+  int64_t t;
+  int chunks;              // 16-byte chunks per row
+};
+
+// rows outside [0, cap) are skipped
+__device__ __forceinline__ void append_row(const AppendArgs& ap, int64_t cap,
+                                           int64_t bh, int Hkv, int lane) {
+  const int64_t row = ap.pos ? ap.pos[bh / Hkv] : ap.t;
+  if (row < 0 || row >= cap) return;
+  const int64_t dst = (bh * cap + row) * ap.chunks, src = bh * ap.chunks;
+  for (int i = lane; i < ap.chunks; i += kWave) {
+    ap.K[dst + i] = ap.kn[src + i];
+    ap.V[dst + i] = ap.vn[src + i];
+  }
 }
 
 // union entries: segment id in the low 16 bits, the mask of the group's
@@ -608,30 +638,11 @@ __global__ __launch_bounds__(256) void k_peak_exp(int iters, float* __restrict__
 }
 
 // ---------------------------------------------------------------------------
-// k_append: K[b][h][t] = k_new[b][h], V likewise
+// k_append: K[b][h][t] = k_new[b][h], V likewise (row pos[b] of sequence b
+// when pos is given); one wave per (b, kv head)
 // ---------------------------------------------------------------------------
-// (row pos[b] of sequence b when pos is given; rows outside [0, cap) are
-// skipped)
-template <typename T, int D>
-__global__ __launch_bounds__(64) void k_append(T* __restrict__ K, T* __restrict__ V,
-                                               const T* __restrict__ kn,
-                                               const T* __restrict__ vn,
-                                               int64_t cap, int64_t t,
-                                               const int64_t* __restrict__ pos,
-                                               int Hkv) {
-  constexpr int CPR = D * (int)sizeof(T) / 16;
-  const int64_t bh = blockIdx.x;
-  const int i = threadIdx.x;
-  if (pos) t = pos[bh / Hkv];
-  if (t < 0 || t >= cap) return;
-  if (i < CPR) {
-    const uint4* sk = reinterpret_cast<const uint4*>(kn + bh * D) + i;
-    const uint4* sv = reinterpret_cast<const uint4*>(vn + bh * D) + i;
-    uint4* dk = reinterpret_cast<uint4*>(K + (bh * cap + t) * D) + i;
-    uint4* dv = reinterpret_cast<uint4*>(V + (bh * cap + t) * D) + i;
-    *dk = *sk;
-    *dv = *sv;
-  }
+__global__ __launch_bounds__(64) void k_append(AppendArgs ap, int64_t cap, int Hkv) {
+  append_row(ap, cap, blockIdx.x, Hkv, threadIdx.x);
 }
 
 // ---------------------------------------------------------------------------
@@ -959,7 +970,8 @@ __global__ __launch_bounds__(256) void k_score(const float* __restrict__ phiq,
 __global__ __launch_bounds__(256) void k_topk_union(
     const float* __restrict__ scores, int Hq, int Hkv, int G, SeqArgs sa,
     int nc_cap, int per_head, int* __restrict__ uni, int* __restrict__ ucnt,
-    int umax, int32_t* __restrict__ selected, float* __restrict__ sel_scores) {
+    int umax, int32_t* __restrict__ selected, float* __restrict__ sel_scores,
+    AppendArgs ap, int64_t cap) {
   __shared__ int sel_lds[kMaxG * kMaxK];
   __shared__ unsigned bits_lds[kMaxG * kBitmapWords];
   __shared__ unsigned hist_lds[4][256];
@@ -968,6 +980,9 @@ __global__ __launch_bounds__(256) void k_topk_union(
   const int wave = threadIdx.x >> 6;
   const int64_t bh = blockIdx.x;
   const int64_t b = bh / Hkv, hk = bh % Hkv;
+  // the append of radar_append_decode (the attention kernel that reads the
+  // row runs after this one)
+  if (ap.K && wave == 3) append_row(ap, cap, bh, Hkv, lane);
   const Span sp = seq_span(sa, b);
   const int n_cand = sp.n_cand, k_eff = sp.k_eff, k = sa.k;
   const int npl = (n_cand + 63) / 64;
@@ -1350,7 +1365,7 @@ __global__ __launch_bounds__(512) void k_decode_fused(
     float* __restrict__ sel_scores, int Hq, int Hkv, int64_t cap,
     int64_t s_cap, int tiles_per_seg, SeqArgs sa, int per_head, float s1,
     float s2, float inv_sqrt_n, float qscale, int* __restrict__ uni_out,
-    int* __restrict__ ucnt_out, int umax) {
+    int* __restrict__ ucnt_out, int umax, AppendArgs ap) {
   constexpr int NW = kFusedWaves;
   constexpr int QPL = D / 16;              // q elements per lane (phase 1)
   constexpr int FPL = N / 64;              // features per lane (phase 2)
@@ -1384,6 +1399,15 @@ __global__ __launch_bounds__(512) void k_decode_fused(
   const Span sp = seq_span(sa, b);
   const int c = sa.c, k = sa.k, n_cand = sp.n_cand, k_eff = sp.k_eff;
   const int64_t ws = sp.ws, t = sp.t;
+
+  // The append of radar_append_decode: the last wave writes the pair's new
+  // row before anything reads it. The row belongs to the window (never to a
+  // candidate segment), read from phase 3 on, after a barrier: those of
+  // phases 1 and 2, or this one when there are no candidates.
+  if (ap.K) {                              // uniform
+    if (wave == NW - 1) append_row(ap, cap, bh, Hkv, lane);
+    if (n_cand == 0) __syncthreads();
+  }
 
   if (n_cand > 0) {                        // uniform
     // Each wave's first batch of summary rows goes in flight before phi(q)
@@ -2012,7 +2036,8 @@ radar_status launch_fused_n(const Shape& s, const void* q, const void* K,
                             const void* V, const float* omega,
                             const float* summ, const SeqArgs& sa, void* out,
                             int32_t* selected, float* sel_scores, int* uni_out,
-                            int* ucnt_out, int umax, hipStream_t st) {
+                            int* ucnt_out, int umax, const AppendArgs& ap,
+                            hipStream_t st) {
   const float s1 = kLog2e / std::pow((float)s.d, 0.25f);
   const float s2 = kLog2e / (2.f * std::sqrt((float)s.d));
   launch(SEL ? RADAR_K_SELECT : RADAR_K_FUSED, k_decode_fused<T, D, G, N, SEL>,
@@ -2021,14 +2046,14 @@ radar_status launch_fused_n(const Shape& s, const void* q, const void* K,
          reinterpret_cast<const T*>(V), omega, summ, reinterpret_cast<T*>(out),
          selected, sel_scores, s.Hq, s.Hkv, s.cap, s.s_cap, (int)ceil_div(s.c, kTile),
          sa, s.per_head, s1, s2, 1.f / std::sqrt((float)s.n),
-         kLog2e / std::sqrt((float)s.d), uni_out, ucnt_out, umax);
+         kLog2e / std::sqrt((float)s.d), uni_out, ucnt_out, umax, ap);
   return launch_status();
 }
 
-#define RADAR_FUSED_ARGS s, q, K, V, omega, summ, sa, out, selected, sel_scores, uni_out, ucnt_out, umax, st
+#define RADAR_FUSED_ARGS s, q, K, V, omega, summ, sa, out, selected, sel_scores, uni_out, ucnt_out, umax, ap, st
 #define RADAR_FUSED_PARAMS const Shape& s, const void* q, const void* K, const void* V, \
     const float* omega, const float* summ, const SeqArgs& sa, void* out, int32_t* selected, \
-    float* sel_scores, int* uni_out, int* ucnt_out, int umax, hipStream_t st
+    float* sel_scores, int* uni_out, int* ucnt_out, int umax, const AppendArgs& ap, hipStream_t st
 
 template <typename T, int D, int G, bool SEL>
 radar_status launch_fused_g(RADAR_FUSED_PARAMS) {
@@ -2053,7 +2078,7 @@ radar_status launch_fused_d(RADAR_FUSED_PARAMS) {
 radar_status launch_fused(const Shape& s, const void* q, const void* K, const void* V,
                           const float* omega, const float* summ, const SeqArgs& sa,
                           void* out, int32_t* selected, float* sel_scores,
-                          hipStream_t st) {
+                          const AppendArgs& ap, hipStream_t st) {
   int* uni_out = nullptr;
   int* ucnt_out = nullptr;
   const int umax = 0;
@@ -2071,7 +2096,7 @@ radar_status launch_fused(const Shape& s, const void* q, const void* K, const vo
 radar_status launch_select(const Shape& s, const void* q, const float* omega,
                            const float* summ, const SeqArgs& sa, int32_t* selected,
                            float* sel_scores, unsigned char* w, const WsLayout& L,
-                           hipStream_t st) {
+                           const AppendArgs& ap, hipStream_t st) {
   const void* K = nullptr;
   const void* V = nullptr;
   void* out = nullptr;
@@ -2141,6 +2166,100 @@ radar_status check_decode(const radar_config* cfg, Shape* s, int64_t t,
   *sa = SeqArgs{lens, t, s->c, s->w, s->n_sink, k};
   if (make_span(t, *sa).n_cand > kMaxCand) return RADAR_EUNSUPPORTED;
   return RADAR_OK;
+}
+
+// Pointer checks shared by radar_append and radar_append_decode.
+radar_status check_append(const radar_config* cfg, Shape* s, const void* K,
+                          const void* V, const void* k_new, const void* v_new,
+                          const float* omega, const float* summaries,
+                          const int64_t* pos) {
+  radar_status r = check_cfg(cfg, s);
+  if (r != RADAR_OK) return r;
+  if (!K || !V || !k_new || !v_new || !omega || !summaries) return RADAR_EINVAL;
+  if (!aligned16(K) || !aligned16(V) || !aligned16(k_new) || !aligned16(v_new) ||
+      !aligned16(omega) || !aligned16(summaries) || (pos && !aligned16(pos)))
+    return RADAR_EINVAL;
+  return RADAR_OK;
+}
+
+AppendArgs append_args(const Shape& s, void* K, void* V, const void* k_new,
+                       const void* v_new, const int64_t* pos, int64_t t) {
+  const int esz = s.dt == RADAR_BF16 ? 2 : 4;
+  return AppendArgs{static_cast<uint4*>(K), static_cast<uint4*>(V),
+                    static_cast<const uint4*>(k_new), static_cast<const uint4*>(v_new),
+                    pos, t, s.d * esz / 16};
+}
+
+// The summary refresh of an append of row t (row pos[b] of sequence b): the
+// segment the row completes, if any, with the index build's own code.
+radar_status refresh_closed(const Shape& s, const void* K, const float* omega,
+                            float* summ, int64_t t, const int64_t* pos,
+                            hipStream_t st) {
+  const void* Kp = after_sinks(s, K);
+  if (pos) return launch_build(s, Kp, omega, summ, 0, 1, pos, st);
+  const int64_t row = t - s.n_sink;          // row after the sinks
+  if (row >= 0 && (row + 1) % s.c == 0)
+    return launch_build(s, Kp, omega, summ, (int)((row + 1) / s.c - 1), 1, nullptr,
+                        st);
+  return RADAR_OK;
+}
+
+// Which kernels a decode runs, decided (and checked) before any launch.
+struct DecodePlan {
+  int path;
+  AttendGrid ag;
+};
+
+radar_status plan_decode(const Shape& s, const WsLayout& L, const SeqArgs& sa,
+                         DecodePlan* p) {
+  const Span top = make_span(sa.t_max, sa);
+  p->path = choose_path(s, sa);
+  p->ag = AttendGrid{0, 1};
+  if (p->path == RADAR_PATH_FUSED) return RADAR_OK;
+  const int u_bound = std::min(s.G * top.k_eff, top.n_cand);
+  p->ag = attend_grid(s, L, u_bound, extra_tiles(s, sa));
+  return p->ag.grid_x > kMaxWg ? RADAR_EUNSUPPORTED : RADAR_OK;
+}
+
+// The decode launches. The first per-(b, kv head) kernel of the path (the
+// fused kernel, the select kernel or the top-k) also writes the new rows
+// that ap describes, before the attention reads them.
+radar_status run_decode(const Shape& s, const WsLayout& L, const SeqArgs& sa,
+                        const DecodePlan& plan, const void* q, const void* K,
+                        const void* V, const float* omega, const float* summaries,
+                        void* out, int32_t* selected, float* scores,
+                        unsigned char* w, const AppendArgs& ap, hipStream_t stream) {
+  const Span top = make_span(sa.t_max, sa);
+  const void* Kp = after_sinks(s, K);
+  const void* Vp = after_sinks(s, V);
+  if (plan.path == RADAR_PATH_FUSED)
+    return launch_fused(s, q, Kp, Vp, omega, summaries, sa, out, selected, scores, ap,
+                        stream);
+  if (plan.path == RADAR_PATH_SELECT) {
+    const radar_status r = launch_select(s, q, omega, summaries, sa, selected, scores,
+                                         w, L, ap, stream);
+    if (r != RADAR_OK) return r;
+    return launch_attend(s, q, Kp, Vp, plan.ag, sa, out, w, L, stream);
+  }
+  float* phiq = reinterpret_cast<float*>(w + L.phiq);
+  float* sc = reinterpret_cast<float*>(w + L.scores);
+  if (top.n_cand > 0) {
+    if (s.dt == RADAR_BF16) {
+      if (s.d == 64) launch_phi_q<bf16_t, 64>(s, q, omega, phiq, stream);
+      else launch_phi_q<bf16_t, 128>(s, q, omega, phiq, stream);
+    } else {
+      if (s.d == 64) launch_phi_q<float, 64>(s, q, omega, phiq, stream);
+      else launch_phi_q<float, 128>(s, q, omega, phiq, stream);
+    }
+    launch_score(s, phiq, summaries, sc, top.n_cand, sa, stream);
+  }
+  launch(RADAR_K_TOPK, k_topk_union, dim3((unsigned)(s.B * s.Hkv)), dim3(256), 0, stream,
+         sc, s.Hq, s.Hkv, s.G, sa, (int)std::max<int64_t>(1, s.s_cap), s.per_head,
+         reinterpret_cast<int*>(w + L.uni), reinterpret_cast<int*>(w + L.ucnt), L.umax,
+         selected, scores, ap, s.cap);
+  const radar_status r = launch_status();
+  if (r != RADAR_OK) return r;
+  return launch_attend(s, q, Kp, Vp, plan.ag, sa, out, w, L, stream);
 }
 
 }  // namespace
@@ -2267,38 +2386,15 @@ radar_status radar_append(const radar_config* cfg, void* K, void* V,
                           const float* omega, int64_t t, const int64_t* pos,
                           float* summaries, hipStream_t stream) {
   Shape s;
-  radar_status r = check_cfg(cfg, &s);
+  radar_status r = check_append(cfg, &s, K, V, k_new, v_new, omega, summaries, pos);
   if (r != RADAR_OK) return r;
-  if (!K || !V || !k_new || !v_new || !omega || !summaries) return RADAR_EINVAL;
-  if (!aligned16(K) || !aligned16(V) || !aligned16(k_new) || !aligned16(v_new) ||
-      !aligned16(omega) || !aligned16(summaries) || (pos && !aligned16(pos)))
-    return RADAR_EINVAL;
   if (!pos && (t < 0 || t >= s.cap)) return RADAR_ECAPACITY;
-  const unsigned grid = (unsigned)(s.B * s.Hkv);
-  if (s.dt == RADAR_BF16) {
-    if (s.d == 64)
-      launch(RADAR_K_APPEND, k_append<bf16_t, 64>, dim3(grid), dim3(64), 0, stream,
-             (bf16_t*)K, (bf16_t*)V, (const bf16_t*)k_new, (const bf16_t*)v_new, s.cap, t, pos, s.Hkv);
-    else
-      launch(RADAR_K_APPEND, k_append<bf16_t, 128>, dim3(grid), dim3(64), 0, stream,
-             (bf16_t*)K, (bf16_t*)V, (const bf16_t*)k_new, (const bf16_t*)v_new, s.cap, t, pos, s.Hkv);
-  } else {
-    if (s.d == 64)
-      launch(RADAR_K_APPEND, k_append<float, 64>, dim3(grid), dim3(64), 0, stream,
-             (float*)K, (float*)V, (const float*)k_new, (const float*)v_new, s.cap, t, pos, s.Hkv);
-    else
-      launch(RADAR_K_APPEND, k_append<float, 128>, dim3(grid), dim3(64), 0, stream,
-             (float*)K, (float*)V, (const float*)k_new, (const float*)v_new, s.cap, t, pos, s.Hkv);
-  }
+  const AppendArgs ap = append_args(s, K, V, k_new, v_new, pos, t);
+  launch(RADAR_K_APPEND, k_append, dim3((unsigned)(s.B * s.Hkv)), dim3(64), 0, stream,
+         ap, s.cap, s.Hkv);
   r = launch_status();
   if (r != RADAR_OK) return r;
-  const void* Kp = after_sinks(s, static_cast<const void*>(K));
-  if (pos) return launch_build(s, Kp, omega, summaries, 0, 1, pos, stream);
-  const int64_t row = t - s.n_sink;          // row after the sinks
-  if (row >= 0 && (row + 1) % s.c == 0)
-    return launch_build(s, Kp, omega, summaries, (int)((row + 1) / s.c - 1), 1,
-                        nullptr, stream);
-  return RADAR_OK;
+  return refresh_closed(s, K, omega, summaries, t, pos, stream);
 }
 
 radar_status radar_decode(const radar_config* cfg, const void* q, const void* K,
@@ -2317,44 +2413,54 @@ radar_status radar_decode(const radar_config* cfg, const void* q, const void* K,
   SeqArgs sa;
   radar_status r = check_decode(cfg, &s, t, lens, k, workspace, workspace_bytes, &L, &sa);
   if (r != RADAR_OK) return r;
-  const Span top = make_span(t, sa);
-  const void* Kp = after_sinks(s, K);
-  const void* Vp = after_sinks(s, V);
-
-  const int path = choose_path(s, sa);
-  if (path == RADAR_PATH_FUSED)
-    return launch_fused(s, q, Kp, Vp, omega, summaries, sa, out, selected, scores,
-                        stream);
-
-  const int u_bound = std::min(s.G * top.k_eff, top.n_cand);
-  const AttendGrid ag = attend_grid(s, L, u_bound, extra_tiles(s, sa));
-  if (ag.grid_x > kMaxWg) return RADAR_EUNSUPPORTED;
-
-  unsigned char* w = reinterpret_cast<unsigned char*>(workspace);
-  if (path == RADAR_PATH_SELECT) {
-    r = launch_select(s, q, omega, summaries, sa, selected, scores, w, L, stream);
-    if (r != RADAR_OK) return r;
-    return launch_attend(s, q, Kp, Vp, ag, sa, out, w, L, stream);
-  }
-  float* phiq = reinterpret_cast<float*>(w + L.phiq);
-  float* sc = reinterpret_cast<float*>(w + L.scores);
-  if (top.n_cand > 0) {
-    if (s.dt == RADAR_BF16) {
-      if (s.d == 64) launch_phi_q<bf16_t, 64>(s, q, omega, phiq, stream);
-      else launch_phi_q<bf16_t, 128>(s, q, omega, phiq, stream);
-    } else {
-      if (s.d == 64) launch_phi_q<float, 64>(s, q, omega, phiq, stream);
-      else launch_phi_q<float, 128>(s, q, omega, phiq, stream);
-    }
-    launch_score(s, phiq, summaries, sc, top.n_cand, sa, stream);
-  }
-  launch(RADAR_K_TOPK, k_topk_union, dim3((unsigned)(s.B * s.Hkv)), dim3(256), 0, stream,
-         sc, s.Hq, s.Hkv, s.G, sa, (int)std::max<int64_t>(1, s.s_cap), s.per_head,
-         reinterpret_cast<int*>(w + L.uni), reinterpret_cast<int*>(w + L.ucnt), L.umax,
-         selected, scores);
-  r = launch_status();
+  DecodePlan plan;
+  r = plan_decode(s, L, sa, &plan);
   if (r != RADAR_OK) return r;
-  return launch_attend(s, q, Kp, Vp, ag, sa, out, w, L, stream);
+  return run_decode(s, L, sa, plan, q, K, V, omega, summaries, out, selected, scores,
+                    static_cast<unsigned char*>(workspace), AppendArgs{}, stream);
+}
+
+radar_status radar_append_decode(const radar_config* cfg, const void* q, void* K,
+                                 void* V, const void* k_new, const void* v_new,
+                                 const float* omega, float* summaries, int64_t t,
+                                 const int64_t* pos, int32_t k, void* out,
+                                 int32_t* selected, float* scores, void* workspace,
+                                 size_t workspace_bytes, hipStream_t stream) {
+  Shape s;
+  radar_status r = check_append(cfg, &s, K, V, k_new, v_new, omega, summaries, pos);
+  if (r != RADAR_OK) return r;
+  if (!q || !out) return RADAR_EINVAL;
+  if (!aligned16(q) || !aligned16(out) || (selected && !aligned16(selected)) ||
+      (scores && !aligned16(scores)))
+    return RADAR_EINVAL;
+  WsLayout L;
+  SeqArgs sa;
+  r = check_decode(cfg, &s, t, pos, k, workspace, workspace_bytes, &L, &sa);
+  if (r != RADAR_OK) return r;
+  sa.lens_add = pos ? 1 : 0;
+  DecodePlan plan;
+  r = plan_decode(s, L, sa, &plan);
+  if (r != RADAR_OK) return r;
+  unsigned char* w = static_cast<unsigned char*>(workspace);
+  const AppendArgs ap = append_args(s, K, V, k_new, v_new, pos, t - 1);
+  if (s.w == 0) {
+    // Without a window the segment this row completes is already a
+    // candidate of the same step: write the row and refresh its summary
+    // first, then decode.
+    launch(RADAR_K_APPEND, k_append, dim3((unsigned)(s.B * s.Hkv)), dim3(64), 0,
+           stream, ap, s.cap, s.Hkv);
+    r = launch_status();
+    if (r == RADAR_OK) r = refresh_closed(s, K, omega, summaries, t - 1, pos, stream);
+    if (r != RADAR_OK) return r;
+    return run_decode(s, L, sa, plan, q, K, V, omega, summaries, out, selected, scores,
+                      w, AppendArgs{}, stream);
+  }
+  // With w >= 1 the completed segment ends inside the window, so the decode
+  // does not read its summary: the refresh runs after it.
+  r = run_decode(s, L, sa, plan, q, K, V, omega, summaries, out, selected, scores, w,
+                 ap, stream);
+  if (r != RADAR_OK) return r;
+  return refresh_closed(s, K, omega, summaries, t - 1, pos, stream);
 }
 
 radar_status radar_decode_exact(const radar_config* cfg, const void* q,
@@ -2393,7 +2499,7 @@ radar_status radar_decode_exact(const radar_config* cfg, const void* q,
   launch(RADAR_K_TOPK, k_topk_union, dim3((unsigned)(s.B * s.Hkv)), dim3(256), 0, stream,
          sc, s.Hq, s.Hkv, s.G, sa, (int)std::max<int64_t>(1, s.s_cap), s.per_head,
          reinterpret_cast<int*>(w + L.uni), reinterpret_cast<int*>(w + L.ucnt), L.umax,
-         selected, scores);
+         selected, scores, AppendArgs{}, s.cap);
   r = launch_status();
   if (r != RADAR_OK) return r;
   return launch_attend(s, q, Kp, Vp, ag, sa, out, w, L, stream);

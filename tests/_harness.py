@@ -93,13 +93,16 @@ class Episode:
     n_sink / per_head select the attention-sink and per-head GQA options.
     lens0 (one length <= t0 per sequence) makes the batch ragged: sequence b
     starts at length lens0[b] (its cache rows beyond are stale), appends at
-    its own position and decodes at its own length."""
+    its own position and decodes at its own length. merged runs each step as
+    one radar_append_decode call instead of radar_append + radar_decode."""
 
     def __init__(self, wl, steps, groups=None, device="cuda",
-                 path=radar.PATH_AUTO, n_sink=0, per_head=False, lens0=None):
+                 path=radar.PATH_AUTO, n_sink=0, per_head=False, lens0=None,
+                 merged=False):
         self.wl = wl
         self.steps = steps
         self.path = path
+        self.merged = merged
         self.n_sink, self.per_head = n_sink, per_head
         self.lens0 = list(lens0) if lens0 is not None else None
         self.inp = workloads.make_inputs(wl, device, steps=steps)
@@ -150,21 +153,24 @@ class Episode:
                          device=dev)
         out = torch.empty_like(inp.q[0])
         for i in range(self.steps):
-            if self.lens0 is None:
-                radar.append(cfg, K, V, inp.k_new[i].contiguous(),
-                             inp.v_new[i].contiguous(), inp.omega, lens[0], summ)
-            else:
-                pos = torch.tensor(lens, dtype=torch.int64, device=dev)
-                radar.append(cfg, K, V, inp.k_new[i].contiguous(),
-                             inp.v_new[i].contiguous(), inp.omega, 0, summ,
-                             pos=pos)
-            lens = [x + 1 for x in lens]
+            kn, vn = inp.k_new[i].contiguous(), inp.v_new[i].contiguous()
             q = inp.q[i].contiguous()
-            lens_dev = None if self.lens0 is None else \
+            pos = None if self.lens0 is None else \
                 torch.tensor(lens, dtype=torch.int64, device=dev)
-            radar.decode(cfg, q, K, V, inp.omega, summ, max(lens), wl.top_k,
-                         out=out, selected=sel, scores=sc, workspace=ws,
-                         lens=lens_dev)
+            if self.merged:
+                lens = [x + 1 for x in lens]
+                radar.append_decode(cfg, q, K, V, kn, vn, inp.omega, summ,
+                                    max(lens), wl.top_k, out=out, selected=sel,
+                                    scores=sc, workspace=ws, pos=pos)
+            else:
+                radar.append(cfg, K, V, kn, vn, inp.omega,
+                             lens[0] if pos is None else 0, summ, pos=pos)
+                lens = [x + 1 for x in lens]
+                lens_dev = None if self.lens0 is None else \
+                    torch.tensor(lens, dtype=torch.int64, device=dev)
+                radar.decode(cfg, q, K, V, inp.omega, summ, max(lens), wl.top_k,
+                             out=out, selected=sel, scores=sc, workspace=ws,
+                             lens=lens_dev)
             if check_steps is None or i in check_steps:
                 torch.cuda.synchronize()
                 self.check_step(i, lens, q, out, sel, sc)

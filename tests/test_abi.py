@@ -39,7 +39,7 @@ def test_exports_every_declared_symbol(L):
 
 
 def test_version_and_strings(L):
-    assert L.radar_abi_version() == radar.ABI_VERSION == 2
+    assert L.radar_abi_version() == radar.ABI_VERSION == 3
     for st in range(6):
         assert L.radar_status_string(st).decode()
     assert L.radar_last_error() is not None
@@ -137,6 +137,30 @@ def test_validation_before_launch(L):
                                    null, good, good, ws, None) == 1
     assert L.radar_attend_selected(by(cfg), good, good, good, good, 0, 100,
                                    null, good, good, ws, None) == 3
+    # append_decode: append's and decode's checks, t is the length after
+    # the append
+    ad = [by(cfg), good, good, good, good, good, good, good]
+    assert L.radar_append_decode(None, good, good, good, good, good, good, good,
+                                 1000, null, 16, good, None, None, good, ws,
+                                 None) == 1
+    assert L.radar_append_decode(by(cfg), null, good, good, good, good, good,
+                                 good, 1000, null, 16, good, None, None, good,
+                                 ws, None) == 1
+    assert L.radar_append_decode(by(cfg), good, good, good, null, good, good,
+                                 good, 1000, null, 16, good, None, None, good,
+                                 ws, None) == 1
+    assert L.radar_append_decode(*ad, 0, null, 16, good, None, None, good, ws,
+                                 None) == 2
+    assert L.radar_append_decode(*ad, 131585, null, 16, good, None, None, good,
+                                 ws, None) == 2
+    assert L.radar_append_decode(*ad, 1000, odd, 16, good, None, None, good, ws,
+                                 None) == 1
+    assert L.radar_append_decode(*ad, 1000, null, 0, good, None, None, good, ws,
+                                 None) == 3
+    assert L.radar_append_decode(*ad, 1000, null, 16, good, None, None, good,
+                                 ws - 1, None) == 5
+    assert L.radar_append_decode(*ad, 1000, null, 16, null, None, None, good,
+                                 ws, None) == 1
     # measurement microkernels
     work = ctypes.c_double()
     assert L.radar_peak_mfma(0, good, by(work), None) == 1

@@ -293,6 +293,36 @@ def test_errors_leave_outputs_untouched():
     assert bool((summ == 5.0).all()) and bool((out == 3.0).all())
 
 
+def test_binding_refuses_wrong_sizes():
+    """A tensor whose size does not match the config is refused before any
+    kernel could address past its end."""
+    wl = _edge("sizes")
+    cfg = H.config_of(wl, 64)
+    K = torch.zeros(1, 2, 64, 128, dtype=torch.bfloat16, device="cuda")
+    short = torch.zeros(1, 2, 63, 128, dtype=torch.bfloat16, device="cuda")
+    om = torch.zeros(128, 128, device="cuda")
+    summ = torch.zeros(1, 2, 4, 128, device="cuda")
+    q = torch.zeros(1, 2, 128, dtype=torch.bfloat16, device="cuda")
+    row = torch.zeros(1, 2, 128, dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(ValueError, match="K holds"):
+        radar.build_index(cfg, short, om, 10, summ)
+    with pytest.raises(ValueError, match="summaries holds"):
+        radar.build_index(cfg, K, om, 10, summ[:, :, :3].contiguous())
+    with pytest.raises(ValueError, match="omega holds"):
+        radar.build_index(cfg, K, om[:64].contiguous(), 10, summ)
+    with pytest.raises(ValueError, match="V holds"):
+        radar.decode(cfg, q, K, short, om, summ, 10, 2)
+    with pytest.raises(ValueError, match="k_new holds"):
+        radar.append(cfg, K, K, row[:, :1].contiguous(), row, om, 10, summ)
+    with pytest.raises(ValueError, match="selected holds"):
+        radar.decode(cfg, q, K, K, om, summ, 10, 4,
+                     selected=torch.zeros(1, 2, 3, dtype=torch.int32,
+                                          device="cuda"))
+    with pytest.raises(ValueError, match="out holds"):
+        radar.append_decode(cfg, q, K, K, row, row, om, summ, 10, 2,
+                            out=q[:, :1].contiguous())
+
+
 @PATHS
 @pytest.mark.parametrize("k", [3, 6, 13])
 def test_exact_ties_take_lower_index(path, k):
