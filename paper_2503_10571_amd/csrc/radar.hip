@@ -646,59 +646,72 @@ __global__ __launch_bounds__(64) void k_append(AppendArgs ap, int64_t cap, int H
 }
 
 // ---------------------------------------------------------------------------
-// k_phi_q: phi(q) for every (b, q head), Eq. 4
+// k_phi_q: phi(q) (Eq. 4) of the G query heads of one (b, kv head), one
+// block of 64 features per workgroup
 // ---------------------------------------------------------------------------
-// One workgroup per query head. 16 lanes share one Omega row (D/16 floats
-// each); a wave covers 4 rows per pass and the workgroup 16. The 16 passes of
-// a 256-feature chunk are transpose-reduced across the 16 lanes, so each lane
-// finishes one feature.
-template <typename T, int D>
+// Grid (n / 64, B * Hkv): each workgroup reads only its 64 rows of Omega.
+// 16 lanes share one Omega row (D/16 floats each); wave w covers rows
+// 16 w .. 16 w + 15 in 4 passes of 4 rows, and the 4 partial sums of each
+// lane are reduced across its 16 lanes (transpose-reduce over 4 lanes, then
+// two butterflies), so lane jj < 4 of row group r ends with feature
+// 16 w + 4 jj + r.
+template <typename T, int D, int G>
 __global__ __launch_bounds__(256) void k_phi_q(const T* __restrict__ q,
                                                const float* __restrict__ omega,
                                                float* __restrict__ phiq,
-                                               int n, float s1,
+                                               int n, int Hq, int Hkv, float s1,
                                                float s2, float inv_sqrt_n) {
   constexpr int QPL = D / 16;              // q elements per lane
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int r = lane >> 4, jj = lane & 15;
-  const int64_t bhq = blockIdx.x;
+  const int64_t bh = blockIdx.y;
+  const int64_t b = bh / Hkv, hk = bh % Hkv;
+  const int64_t hq0 = b * Hq + hk * G;     // the group's first (b, q head)
+  const int f0 = blockIdx.x * 64 + wave * 16;
 
-  float qv[QPL];
+  float4 om[4][QPL / 4];
 #pragma unroll
-  for (int e = 0; e < QPL; ++e) qv[e] = to_f32<T>(q[bhq * D + jj * QPL + e]);
-  float nrm = 0.f;
+  for (int p = 0; p < 4; ++p) {
+    const float* orow = omega + (int64_t)(f0 + p * 4 + r) * D + jj * QPL;
 #pragma unroll
-  for (int e = 0; e < QPL; ++e) nrm = fmaf(qv[e], qv[e], nrm);
-  nrm = row_sum(nrm);
-
-  for (int c0 = 0; c0 < n; c0 += 256) {
-    float part[16];
+    for (int e4 = 0; e4 < QPL / 4; ++e4)
+      om[p][e4] = *reinterpret_cast<const float4*>(orow + 4 * e4);
+  }
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      // rows past n re-read row n - 1; their sums land in lanes that
-      // write nothing
-      const int row = min(c0 + i * 16 + wave * 4 + r, n - 1);
+  for (int g = 0; g < G; ++g) {
+    float qv[QPL];
+#pragma unroll
+    for (int e = 0; e < QPL; ++e) qv[e] = to_f32<T>(q[(hq0 + g) * D + jj * QPL + e]);
+    float nrm = 0.f;
+#pragma unroll
+    for (int e = 0; e < QPL; ++e) nrm = fmaf(qv[e], qv[e], nrm);
+    nrm = row_sum(nrm);
+    float part[4];
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
       float a = 0.f;
-      const float* orow = omega + (int64_t)row * D + jj * QPL;
 #pragma unroll
-      for (int e4 = 0; e4 < QPL; e4 += 4) {
-        float4 o = *reinterpret_cast<const float4*>(orow + e4);
+      for (int e4 = 0; e4 < QPL / 4; ++e4) {
+        float4 o = om[p][e4];
         if constexpr (sizeof(T) == 2) {
           o.x = round_bf16(o.x); o.y = round_bf16(o.y);
           o.z = round_bf16(o.z); o.w = round_bf16(o.w);
         }
-        a = fmaf(o.x, qv[e4], a);
-        a = fmaf(o.y, qv[e4 + 1], a);
-        a = fmaf(o.z, qv[e4 + 2], a);
-        a = fmaf(o.w, qv[e4 + 3], a);
+        a = fmaf(o.x, qv[4 * e4], a);
+        a = fmaf(o.y, qv[4 * e4 + 1], a);
+        a = fmaf(o.z, qv[4 * e4 + 2], a);
+        a = fmaf(o.w, qv[4 * e4 + 3], a);
       }
-      part[i] = a;
+      part[p] = a;
     }
-    transpose_reduce<16>(part, lane);
-    const int row = c0 + jj * 16 + wave * 4 + r;
-    if (row < n)
-      phiq[bhq * n + row] = fast_exp2(fmaf(part[0], s1, -nrm * s2)) * inv_sqrt_n;
+    transpose_reduce<4>(part, lane);
+    float v = part[0];
+    v += __shfl_xor(v, 4);
+    v += __shfl_xor(v, 8);
+    if (jj < 4)
+      phiq[(hq0 + g) * n + f0 + jj * 4 + r] =
+          fast_exp2(fmaf(v, s1, -nrm * s2)) * inv_sqrt_n;
   }
 }
 
@@ -888,7 +901,9 @@ __device__ void group_union(const int* sel, unsigned* bits, int G, int per,
 // ---------------------------------------------------------------------------
 // k_score: a[h][s] = phi(q_h) . summ[s], Eq. 6
 // ---------------------------------------------------------------------------
-// Workgroup = 4 waves x (16 * RB) summary rows of one (b, kv head). Lane l
+// Workgroup = 1, 2 or 4 waves x (16 * RB) summary rows of one (b, kv head)
+// (fewer waves per workgroup when that spreads a small call over more CUs;
+// the waves are independent). Lane l
 // holds features [l*FPL, (l+1)*FPL) of phi(q) for the G heads of the group,
 // so each summary row is one contiguous n*4-byte wave load; all of a wave's
 // rows are loaded before any is reduced. A 16-row batch is transpose-reduced
@@ -906,7 +921,7 @@ __global__ __launch_bounds__(256) void k_score(const float* __restrict__ phiq,
   const int64_t bh = blockIdx.y;
   const int64_t b = bh / Hkv, hk = bh % Hkv;
   const int n_cand = seq_span(sa, b).n_cand;
-  const int wrow0 = blockIdx.x * (64 * RB) + wave * (16 * RB);
+  const int wrow0 = (blockIdx.x * (blockDim.x >> 6) + wave) * (16 * RB);
   if (wrow0 >= n_cand) return;             // wave-uniform; no barriers below
 
   float pq[G][FPL];
@@ -1638,25 +1653,29 @@ __global__ __launch_bounds__(512) void k_decode_fused(
 // ---------------------------------------------------------------------------
 // k_combine: log-sum-exp merge of the partials of each (b, q head)
 // ---------------------------------------------------------------------------
-// 1024 threads per query head: the partials' maxima and scale factors are
-// computed in parallel, then 1024 / D groups of threads sum disjoint subsets
-// of the partials' accumulators and LDS adds the groups.
-constexpr int kCombineThreads = 1024;
-
-template <typename T, int D>
-__global__ __launch_bounds__(kCombineThreads) void k_combine(
+// Grid (B * Hq, D / DS), NT threads: each workgroup produces DS output dims
+// of one query head. With many partials per head (DS = 32, NT = 256) a
+// head's partials are read by several CUs at once; with few (DS = D,
+// NT = 1024) one workgroup per head saves the launches. Every workgroup
+// takes the maximum and the scaled sum over all the head's partials (two
+// floats each, kept in registers between the passes), then NT / DS groups
+// of threads sum disjoint subsets of the partials' accumulators over its
+// dims, and LDS adds the groups.
+template <typename T, int D, int NT, int DS>
+__global__ __launch_bounds__(NT) void k_combine(
     const float* __restrict__ part, const int* __restrict__ ucnt,
     T* __restrict__ out, int Hq, int Hkv, int G, int tiles_per_seg,
     SeqArgs sa, int maxwg, int tpw) {
   constexpr int PSTRIDE = D + 4;
-  constexpr int NT = kCombineThreads;
   constexpr int NWAVE = NT / kWave;
-  constexpr int NGRP = NT / D;
+  constexpr int NGRP = NT / DS;
+  static_assert(D % DS == 0 && kMaxWg % NT == 0, "shape");
   __shared__ float f_lds[kMaxWg];
   __shared__ float red_lds[2 * NWAVE];
   __shared__ float acc_lds[NT];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t bhq = blockIdx.x;
+  const int e0 = blockIdx.y * DS;
   const int64_t b = bhq / Hq, hq = bhq % Hq;
   const int64_t hk = hq / G;
   const int g = (int)(hq % G);
@@ -1665,16 +1684,25 @@ __global__ __launch_bounds__(kCombineThreads) void k_combine(
   const int extra = (int)(((int64_t)sp.t - sp.ws + kTile - 1) / kTile) +
                     (sp.sink + kTile - 1) / kTile;
   const int nwg = (ucnt[bh] * tiles_per_seg + extra + 4 * tpw - 1) / (4 * tpw);
+  T* o = out + bhq * D + e0;
   if (!sp.ok || nwg == 0) {                // invalid length / nothing attended
-    if (tid < D)
-      out[bhq * D + tid] = from_f32<T>(sp.ok ? 0.f : __uint_as_float(0x7fc00000u));
+    if (tid < DS) o[tid] = from_f32<T>(sp.ok ? 0.f : __uint_as_float(0x7fc00000u));
     return;
   }
   const float* pb = part + ((bh * maxwg) * G + g) * (int64_t)PSTRIDE;
   const int64_t wstride = (int64_t)G * PSTRIDE;
 
+  // each thread's (max, sum) pairs stay in registers between the passes
+  constexpr int PPT = kMaxWg / NT;
+  float mw[PPT], lw[PPT];
   float mx = -INFINITY;
-  for (int w = tid; w < nwg; w += NT) mx = fmaxf(mx, pb[w * wstride]);
+#pragma unroll
+  for (int i = 0; i < PPT; ++i) {
+    const int w = tid + i * NT;
+    mw[i] = w < nwg ? pb[w * wstride] : -INFINITY;
+    lw[i] = w < nwg ? pb[w * wstride + 1] : 0.f;
+    mx = fmaxf(mx, mw[i]);
+  }
   mx = wave_max(mx);
   if (lane == 0) red_lds[wave] = mx;
   __syncthreads();
@@ -1682,14 +1710,18 @@ __global__ __launch_bounds__(kCombineThreads) void k_combine(
 #pragma unroll
   for (int i = 1; i < NWAVE; ++i) M = fmaxf(M, red_lds[i]);
   if (M == -INFINITY) {                    // this head attended nothing
-    if (tid < D) out[bhq * D + tid] = from_f32<T>(0.f);
+    if (tid < DS) o[tid] = from_f32<T>(0.f);
     return;
   }
   float ls = 0.f;
-  for (int w = tid; w < nwg; w += NT) {
-    const float f = fast_exp2(pb[w * wstride] - M);
-    f_lds[w] = f;
-    ls = fmaf(pb[w * wstride + 1], f, ls);
+#pragma unroll
+  for (int i = 0; i < PPT; ++i) {
+    const int w = tid + i * NT;
+    if (w < nwg) {
+      const float f = fast_exp2(mw[i] - M);
+      f_lds[w] = f;
+      ls = fmaf(lw[i], f, ls);
+    }
   }
   ls = wave_sum(ls);
   if (lane == 0) red_lds[NWAVE + wave] = ls;
@@ -1697,18 +1729,18 @@ __global__ __launch_bounds__(kCombineThreads) void k_combine(
   float L = 0.f;
 #pragma unroll
   for (int i = 0; i < NWAVE; ++i) L += red_lds[NWAVE + i];
-  const int e = tid % D, grp = tid / D;
+  const int e = tid % DS, grp = tid / DS;
+  const float* pe = pb + 4 + e0 + e;
   float a = 0.f;
-#pragma unroll 4
-  for (int w = grp; w < nwg; w += NGRP)
-    a = fmaf(pb[w * wstride + 4 + e], f_lds[w], a);
+#pragma unroll 8
+  for (int w = grp; w < nwg; w += NGRP) a = fmaf(pe[w * wstride], f_lds[w], a);
   acc_lds[tid] = a;
   __syncthreads();
-  if (tid < D) {
+  if (tid < DS) {
     float sum = 0.f;
 #pragma unroll
-    for (int i = 0; i < NGRP; ++i) sum += acc_lds[i * D + tid];
-    out[bhq * D + tid] = from_f32<T>(sum / L);
+    for (int i = 0; i < NGRP; ++i) sum += acc_lds[i * DS + tid];
+    o[tid] = from_f32<T>(sum / L);
   }
 }
 
@@ -1892,14 +1924,26 @@ P* after_sinks(const Shape& s, P* p) {
 }
 
 // ---- decode pieces -------------------------------------------------------
+template <typename T, int D, int G>
+void launch_phi_q_g(const Shape& s, const void* q, const float* omega, float* phiq,
+                    hipStream_t st) {
+  const float s1 = kLog2e / std::pow((float)s.d, 0.25f);
+  const float s2 = kLog2e / (2.f * std::sqrt((float)s.d));
+  launch(RADAR_K_PHI_Q, k_phi_q<T, D, G>,
+         dim3((unsigned)(s.n / 64), (unsigned)(s.B * s.Hkv)), dim3(256), 0, st,
+         reinterpret_cast<const T*>(q), omega, phiq, s.n, s.Hq, s.Hkv, s1, s2,
+         1.f / std::sqrt((float)s.n));
+}
+
 template <typename T, int D>
 void launch_phi_q(const Shape& s, const void* q, const float* omega, float* phiq,
                   hipStream_t st) {
-  const float s1 = kLog2e / std::pow((float)s.d, 0.25f);
-  const float s2 = kLog2e / (2.f * std::sqrt((float)s.d));
-  launch(RADAR_K_PHI_Q, k_phi_q<T, D>, dim3((unsigned)(s.B * s.Hq)), dim3(256), 0, st,
-         reinterpret_cast<const T*>(q), omega, phiq, s.n, s1, s2,
-         1.f / std::sqrt((float)s.n));
+  switch (s.G) {
+    case 1: launch_phi_q_g<T, D, 1>(s, q, omega, phiq, st); break;
+    case 2: launch_phi_q_g<T, D, 2>(s, q, omega, phiq, st); break;
+    case 4: launch_phi_q_g<T, D, 4>(s, q, omega, phiq, st); break;
+    default: launch_phi_q_g<T, D, 8>(s, q, omega, phiq, st); break;
+  }
 }
 
 // n_cand: the largest candidate count of the call (grid size); each
@@ -1907,10 +1951,15 @@ void launch_phi_q(const Shape& s, const void* q, const float* omega, float* phiq
 template <int N, int G>
 void launch_score_ng(const Shape& s, const float* phiq, const float* summ,
                      float* scores, int n_cand, const SeqArgs& sa, hipStream_t st) {
-  constexpr int rows_per_wg = 64 * (N <= 256 ? 2 : 1);
-  const dim3 grid((unsigned)ceil_div(n_cand, rows_per_wg), (unsigned)(s.B * s.Hkv));
+  constexpr int rows_per_wave = 16 * (N <= 256 ? 2 : 1);
+  // waves per workgroup: 4 when that still gives two workgroups per CU,
+  // else fewer, so that the rows spread over more CUs
+  int wpb = 4;
+  while (wpb > 1 && ceil_div(n_cand, rows_per_wave * wpb) * s.B * s.Hkv < 2 * num_cu())
+    wpb >>= 1;
+  const dim3 grid((unsigned)ceil_div(n_cand, rows_per_wave * wpb), (unsigned)(s.B * s.Hkv));
   const int nc_cap = (int)std::max<int64_t>(1, s.s_cap);
-  launch(RADAR_K_SCORE, k_score<N, G>, grid, dim3(256), 0, st, phiq, summ, scores,
+  launch(RADAR_K_SCORE, k_score<N, G>, grid, dim3(64 * wpb), 0, st, phiq, summ, scores,
          s.Hq, s.Hkv, sa, s.s_cap, nc_cap);
 }
 
@@ -1959,11 +2008,19 @@ void launch_attend_d(const Shape& s, const void* q, const void* K, const void* V
     case 4: launch_attend_g<T, D, 4>(s, q, K, V, w, L, grid_x, tpw, sa, st); break;
     default: launch_attend_g<T, D, 8>(s, q, K, V, w, L, grid_x, tpw, sa, st); break;
   }
-  launch(RADAR_K_COMBINE, k_combine<T, D>, dim3((unsigned)(s.B * s.Hq)),
-         dim3(kCombineThreads), 0,
-         st, reinterpret_cast<const float*>(w + L.part),
-         reinterpret_cast<const int*>(w + L.ucnt), reinterpret_cast<T*>(out), s.Hq,
-         s.Hkv, s.G, L.tiles_per_seg, sa, L.maxwg, tpw);
+  // partials per head above 128: split the dims over four workgroups
+  if (grid_x > 128)
+    launch(RADAR_K_COMBINE, k_combine<T, D, 256, 32>,
+           dim3((unsigned)(s.B * s.Hq), (unsigned)(D / 32)), dim3(256), 0,
+           st, reinterpret_cast<const float*>(w + L.part),
+           reinterpret_cast<const int*>(w + L.ucnt), reinterpret_cast<T*>(out), s.Hq,
+           s.Hkv, s.G, L.tiles_per_seg, sa, L.maxwg, tpw);
+  else
+    launch(RADAR_K_COMBINE, k_combine<T, D, 1024, D>, dim3((unsigned)(s.B * s.Hq)),
+           dim3(1024), 0,
+           st, reinterpret_cast<const float*>(w + L.part),
+           reinterpret_cast<const int*>(w + L.ucnt), reinterpret_cast<T*>(out), s.Hq,
+           s.Hkv, s.G, L.tiles_per_seg, sa, L.maxwg, tpw);
 }
 
 // Tiles beyond the union's segments per (b, kv head), the window's and the
