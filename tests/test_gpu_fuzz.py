@@ -1,11 +1,12 @@
 """Seeded random configurations vs the fp64 oracle.
 
 Each case draws a shape (dtype, head_dim, group size, kv heads, batch,
-features, segment length, window, k, sinks, GQA mode, ragged start lengths)
-and a decode path from its own seed, then runs 3 append + decode steps
-through the C ABI with the same acceptance as the core parity tests (tie band
-1e-5 on the Eq. 6 scores; outputs 2e-3 fp32 / 1e-2 bf16; summaries 1e-4), and
-one exact-selector decode checked against the oracle's ln(beta) (band 1e-4).
+features, segment length, window, k, sinks, GQA mode, ragged start lengths),
+a decode path and the call form (radar_append + radar_decode, or one
+radar_append_decode) from its own seed, then runs 3 decode steps through the
+C ABI with the same acceptance as the core parity tests (tie band 1e-5 on
+the Eq. 6 scores; outputs 2e-3 fp32 / 1e-2 bf16; summaries 1e-4), and one
+exact-selector decode checked against the oracle's ln(beta) (band 1e-4).
 Contexts stay small enough for the oracle to check every head.
 """
 import os
@@ -49,8 +50,11 @@ def draw(seed):
     if wl.batch > 1 and rng.random() < 0.5:
         lens0 = [int(x) for x in rng.integers(1, t0 + 1, size=wl.batch)]
         lens0[0] = t0
-    return wl, dict(n_sink=n_sink, per_head=bool(rng.random() < 0.3),
-                    lens0=lens0), int(rng.choice(PATHS))
+    opt = dict(n_sink=n_sink, per_head=bool(rng.random() < 0.3), lens0=lens0)
+    path = int(rng.choice(PATHS))
+    # drawn last, so the earlier draws of a seed stay what they were
+    opt["merged"] = bool(rng.random() < 0.5)
+    return wl, opt, path
 
 
 @pytest.mark.parametrize("seed", range(N_CASES))
