@@ -1,25 +1,37 @@
 // Radar decode path on MI355X (gfx950, CDNA4): kernels and the C ABI.
 //
 // Kernels (all on the caller's stream):
-//   k_build       segment summaries, Eq. 4 + Eq. 5: bf16/fp32 matrix-core
-//                 projection of the keys onto Omega, exp2 epilogue, mean over
-//                 the segment's tokens. Also serves the segment close of
-//                 radar_append, so appends and rebuilds agree bit for bit.
-//   k_append      writes one k/v row per (b, kv head).
-//   k_phi_q       phi(q) of every query head, Eq. 4.
-//   k_score       Eq. 6 scores of every candidate segment: HBM-bound GEMV
-//                 over the fp32 summaries, DPP transpose-reduce.
-//   k_topk_union  per query head top-k (score desc, index asc) by wavefront
-//                 arg-max rounds; per kv head sorted union of the group.
-//   k_union_given union of caller-given selections (test hook path).
-//   k_attend      exact attention (Eq. 1-2) over the union's segments plus
-//                 the window: coalesced 16-byte gathers of K/V, fp32 online
-//                 softmax, one partial (max, sum, acc[d]) per workgroup.
-//   k_combine     log-sum-exp merge of the partials into the output.
+//   k_build        segment summaries, Eq. 4 + Eq. 5: bf16/fp32 matrix-core
+//                  projection of the keys onto Omega, exp2 epilogue, mean
+//                  over the segment's tokens. Also serves the segment close
+//                  of an append, so appends and rebuilds agree bit for bit.
+//   k_append       writes one k/v row per (b, kv head) (radar_append; in
+//                  radar_append_decode the decode's first per-pair kernel
+//                  writes the rows instead).
+//   k_decode_fused the whole decode step of one (b, kv head) in one
+//                  workgroup: phi(q), Eq. 6 scores, top-k, union, attention
+//                  and merge. Its select-only instantiation (phases up to the
+//                  union) is the first kernel of the select path.
+//   k_phi_q        phi(q), Eq. 4, per block of 64 features of a kv head's
+//                  query group (split path).
+//   k_score        Eq. 6 scores of every candidate segment: HBM-bound GEMV
+//                  over the fp32 summaries, DPP transpose-reduce.
+//   k_topk_union   per query head top-k (score desc, index asc) by radix
+//                  selection; per kv head sorted union of the group.
+//   k_segment_mass ln(beta_s), the exact attention mass of every candidate
+//                  segment (the exact-selection ablation).
+//   k_union_given  union of caller-given selections.
+//   k_attend       exact attention (Eq. 1-2) over the union's segments plus
+//                  the window and sinks: coalesced 16-byte gathers of K/V,
+//                  fp32 online softmax, one partial (max, sum, acc[d]) per
+//                  workgroup.
+//   k_combine      log-sum-exp merge of the partials into the output.
+//   k_peak_mfma, k_peak_exp  measurement microkernels (matrix and exp2 rates).
 //
-// Stages hand data to each other only across kernel boundaries: the eight
-// L2 caches of the chip are not coherent with one another, and the fences a
-// same-kernel hand-off would need flush them.
+// Stages hand data to each other only inside a workgroup (LDS) or across
+// kernel boundaries: the eight L2 caches of the chip are not coherent with
+// one another, and the fences a cross-workgroup hand-off would need flush
+// them.
 //
 // All softmax / feature exponentials are base 2 with log2(e) folded into the
 // scale factors: exp(x) = exp2(x * log2(e)).
