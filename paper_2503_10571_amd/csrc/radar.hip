@@ -747,12 +747,13 @@ __device__ __forceinline__ float key_score(u64 key) {
 }
 
 // Top-k_eff of one query head by one wave, k-independent: radix selection of
-// the k_eff-th largest 32-bit score key in four 8-bit passes (a 256-bin LDS
-// histogram of the keys that still match the prefix found so far, a suffix
-// count over the bins by DPP row scans and readlanes, and a ballot for the
-// bin holding the k_eff-th key), then a ballot rank among keys equal to that
-// threshold (lower segment index first), compaction of the k_eff selected
-// keys into LDS and a rank sort by (score desc, index asc).
+// the k_eff-th largest 32-bit score key in up to four 8-bit passes (a
+// 256-bin LDS histogram of the keys that still match the prefix found so
+// far, a suffix count over the bins by DPP row scans and readlanes, and a
+// ballot for the bin holding the k_eff-th key; the passes stop early once
+// every key left in that bin is needed), then a ballot rank among keys equal
+// to that threshold (lower segment index first), compaction of the k_eff
+// selected keys into LDS and a rank sort by (score desc, index asc).
 // hist: 256 words and list: k words of LDS owned by this wave.
 __device__ __forceinline__ int row_incl_scan(int v, int lane) {
   // inclusive prefix sum over the 64 lanes
@@ -807,31 +808,40 @@ __device__ void head_topk(const float* __restrict__ src, int n_cand, int k,
 #pragma unroll
       for (int j = 0; j < 4; ++j) { c[j] = (int)hist[255 - lane * 4 - j]; tot += c[j]; }
       const int above = row_incl_scan(tot, lane) - tot;   // keys in larger digits
-      int cum = above, pick = -1, before = 0;
+      int cum = above, pick = -1, before = 0, in_bin = 0;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        if (pick < 0 && cum < need && need <= cum + c[j]) { pick = j; before = cum; }
+        if (pick < 0 && cum < need && need <= cum + c[j]) {
+          pick = j; before = cum; in_bin = c[j];
+        }
         cum += c[j];
       }
       const u64 who = __ballot(pick >= 0);
       const int wl = __ffsll((unsigned long long)who) - 1;
       const int pj = __builtin_amdgcn_readlane(pick, wl);
       const int pb = __builtin_amdgcn_readlane(before, wl);
+      const int pc = __builtin_amdgcn_readlane(in_bin, wl);
       const uint32_t digit = 255u - (uint32_t)(wl * 4 + pj);
       prefix |= digit << shift;
       mask |= 255u << shift;
       need -= pb;
+      // every key left in the chosen bin is taken: the digits found so far
+      // already separate the k_eff largest keys from the rest
+      if (need == pc) break;
     }
-    // prefix is the k_eff-th largest key; take every larger key and the
-    // `need` lowest-index keys equal to it
+    // (prefix, mask) hold the leading digits of the k_eff-th largest key;
+    // take every key whose leading digits are larger, and the `need`
+    // lowest-index keys whose leading digits equal them (all of them when
+    // the passes stopped early)
     int eq_before = 0;
     int n_sel = 0;
     const u64 lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
 #pragma unroll
     for (int m = 0; m < NPL; ++m) {
-      const bool eq = u[m] == prefix && u[m] != 0u;
+      const uint32_t um = u[m] & mask;
+      const bool eq = um == prefix && u[m] != 0u;
       const u64 be = __ballot(eq);
-      const bool take = (u[m] > prefix) ||
+      const bool take = (um > prefix) ||
                         (eq && eq_before + __popcll(be & lt_mask) < need);
       eq_before += __popcll(be);
       const u64 bt = __ballot(take);
@@ -849,6 +859,7 @@ __device__ void head_topk(const float* __restrict__ src, int n_cand, int k,
     for (int i = lane; i < k_eff; i += 64) {
       const u64 key = list[i];
       int rank = 0;
+#pragma unroll 8
       for (int j = 0; j < k_eff; ++j) rank += list[j] > key ? 1 : 0;
       const int idx = key_index(key);
       sel_row[rank] = idx;
