@@ -14,8 +14,10 @@
  * Conventions shared by every call
  * --------------------------------
  *  - Every tensor argument is a DEVICE pointer owned by the caller; `cfg` is a
- *    host pointer. The library allocates no device memory, keeps no state
- *    between calls, never synchronises, and launches only on `stream`.
+ *    host pointer. The library allocates no device memory, keeps no device
+ *    state between calls, never synchronises, and launches only on `stream`
+ *    (the path override and the profiling switch are host-side settings of
+ *    the calling thread).
  *  - Layouts are dense, row-major, element type `kv_dtype` for q / K / V /
  *    k_new / v_new / out, fp32 for Omega, summaries and scores, int32 for
  *    segment ids:
