@@ -239,15 +239,6 @@ __device__ __forceinline__ float dpp_f(float v) {
   return __int_as_float(__builtin_amdgcn_update_dpp(
       __float_as_int(v), __float_as_int(v), CTRL, 0xf, 0xf, false));
 }
-template <int CTRL>
-__device__ __forceinline__ u64 dpp_u64(u64 v) {
-  const int lo = __builtin_amdgcn_update_dpp((int)(uint32_t)v, (int)(uint32_t)v,
-                                             CTRL, 0xf, 0xf, false);
-  const int hi = __builtin_amdgcn_update_dpp((int)(uint32_t)(v >> 32),
-                                             (int)(uint32_t)(v >> 32), CTRL,
-                                             0xf, 0xf, false);
-  return ((u64)(uint32_t)hi << 32) | (u64)(uint32_t)lo;
-}
 
 // Value of the partner lane in a pairing that differs from this lane in bit
 // MASK. Within a 16-lane row the pairings are DPP moves (mirrors for bits 3
@@ -313,35 +304,6 @@ __device__ __forceinline__ float wave_max(float v) {
 __device__ __forceinline__ float wave_sum(float v) {
   v = row_sum(v);
   return (lane_read(v, 0) + lane_read(v, 16)) + (lane_read(v, 32) + lane_read(v, 48));
-}
-__device__ __forceinline__ u64 lane_read_u64(u64 v, int l) {
-  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
-  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), l);
-  return ((u64)hi << 32) | lo;
-}
-__device__ __forceinline__ u64 max_u64(u64 a, u64 b) { return a > b ? a : b; }
-template <int CTRL>
-__device__ __forceinline__ uint32_t dpp_u32(uint32_t v) {
-  return (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, CTRL, 0xf, 0xf, false);
-}
-__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
-  v = max(v, dpp_u32<kDppQuadSwap1>(v));
-  v = max(v, dpp_u32<kDppQuadSwap2>(v));
-  v = max(v, dpp_u32<kDppHalfMirror>(v));
-  v = max(v, dpp_u32<kDppMirror>(v));
-  const uint32_t a = (uint32_t)__builtin_amdgcn_readlane((int)v, 0);
-  const uint32_t b = (uint32_t)__builtin_amdgcn_readlane((int)v, 16);
-  const uint32_t c = (uint32_t)__builtin_amdgcn_readlane((int)v, 32);
-  const uint32_t d = (uint32_t)__builtin_amdgcn_readlane((int)v, 48);
-  return max(max(a, b), max(c, d));
-}
-__device__ __forceinline__ u64 wave_max_u64(u64 v) {
-  v = max_u64(v, dpp_u64<kDppQuadSwap1>(v));
-  v = max_u64(v, dpp_u64<kDppQuadSwap2>(v));
-  v = max_u64(v, dpp_u64<kDppHalfMirror>(v));
-  v = max_u64(v, dpp_u64<kDppMirror>(v));
-  return max_u64(max_u64(lane_read_u64(v, 0), lane_read_u64(v, 16)),
-                 max_u64(lane_read_u64(v, 32), lane_read_u64(v, 48)));
 }
 
 // ---------------------------------------------------------------------------
@@ -842,7 +804,7 @@ __device__ void head_topk(const float* __restrict__ src, int n_cand, int k,
       const bool eq = um == prefix && u[m] != 0u;
       const u64 be = __ballot(eq);
       const bool take = (um > prefix) ||
-                        (eq && eq_before + __popcll(be & lt_mask) < need);
+                        (eq && eq_before + (int)__popcll(be & lt_mask) < need);
       eq_before += __popcll(be);
       const u64 bt = __ballot(take);
       if (take) {
