@@ -325,8 +325,8 @@ def main():
                          "perfect squares, W = [c^2, t)), rebuilds timed")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: the decode path has no multi-GPU "
-              "mode in this build (run with --gpus 1)", file=sys.stderr)
+        print("bench.py measures one GPU: the decode path runs on a single "
+              "device (run with --gpus 1)", file=sys.stderr)
         sys.exit(2)
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)

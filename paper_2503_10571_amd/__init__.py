@@ -21,7 +21,7 @@ ABI_VERSION = 3
 RADAR_F32, RADAR_BF16 = 0, 1
 GQA_UNION, GQA_PER_HEAD = 0, 1
 STATUS = {0: "ok", 1: "invalid argument", 2: "position outside the cache capacity",
-          3: "shape not supported by this build", 4: "HIP launch failed",
+          3: "shape outside the instantiated kernels", 4: "HIP launch failed",
           5: "workspace missing or too small"}
 
 

@@ -2395,7 +2395,7 @@ const char* radar_status_string(radar_status st) {
     case RADAR_OK: return "ok";
     case RADAR_EINVAL: return "invalid argument";
     case RADAR_ECAPACITY: return "position outside the cache capacity";
-    case RADAR_EUNSUPPORTED: return "shape not supported by this build";
+    case RADAR_EUNSUPPORTED: return "shape outside the instantiated kernels";
     case RADAR_EHIP: return "HIP launch failed";
     case RADAR_EWORKSPACE: return "workspace missing or too small";
   }
