@@ -1583,21 +1583,30 @@ __global__ __launch_bounds__(512) void k_decode_fused(
   __syncthreads();
 
   // ---- 4. union -----------------------------------------------------------
-  group_union(sel_lds, bits_lds, G, k_eff, per_head != 0, uni_lds, &ucnt_lds);
-  __syncthreads();
+  // With one query head per group its selection is the set to attend (in
+  // score order; the online softmax does not depend on the order), so the
+  // bitmap union is skipped.
+  const int* segs = sel_lds;
+  int n_segs = k_eff;
+  if constexpr (G > 1 || SEL) {
+    group_union(sel_lds, bits_lds, G, k_eff, per_head != 0, uni_lds, &ucnt_lds);
+    __syncthreads();
+    segs = uni_lds;
+    n_segs = ucnt_lds;
+  }
   if constexpr (SEL) {                     // hand the union to the split path
-    const int u = ucnt_lds;
-    for (int i = tid; i < u; i += NW * 64) uni_out[bh * umax + i] = uni_lds[i];
-    if (tid == 0) ucnt_out[bh] = u;
+    for (int i = tid; i < n_segs; i += NW * 64) uni_out[bh * umax + i] = segs[i];
+    if (tid == 0) ucnt_out[bh] = n_segs;
     return;
   }
-  const int seg_tiles = ucnt_lds * tiles_per_seg;
+  const int seg_tiles = n_segs * tiles_per_seg;
 
   // ---- 5. segment tiles ---------------------------------------------------
   for (int i = wave; i < seg_tiles; i += NW) {
-    const int e = uni_lds[i / tiles_per_seg];
+    const int e = segs[i / tiles_per_seg];
     const int s = e & ((1 << kUniIdBits) - 1);
-    const unsigned hm = per_head ? (unsigned)e >> kUniIdBits : kAllHeads;
+    // (the plain selection of a one-head group carries no head mask)
+    const unsigned hm = (G > 1 && per_head) ? (unsigned)e >> kUniIdBits : kAllHeads;
     const int off = (i % tiles_per_seg) * kTile;
     ta.tile(K, V, bh * cap + (int64_t)s * c + off, min(kTile, c - off), lane, hm);
   }
