@@ -300,6 +300,14 @@ def main():
                     help="1: one radar_append_decode call per step (the row "
                          "write runs inside the decode's first kernel); 0: "
                          "radar_append then radar_decode")
+    ap.add_argument("--kernel-events", default="separate",
+                    choices=["inline", "separate"],
+                    help="per-kernel HIP event timing (the roofline's kernel "
+                         "duration): separate = on a second pass over the same "
+                         "steps, so the timed steps carry no event overhead; "
+                         "inline = on the timed steps themselves (the event "
+                         "pairs add host work per launch, which slows short "
+                         "steps)")
     ap.add_argument("--graph", type=int, default=0,
                     help="1: capture the timed steps (the same library calls "
                          "as the eager loop) into one HIP graph and time its "
@@ -412,6 +420,9 @@ def main():
         graph.replay()
         e1.record()
     else:
+        # with --kernel-events inline every launch of the timed steps is
+        # bracketed by HIP events (hipExtLaunchKernel) on its own stream
+        radar.profile_enable(args.kernel_events == "inline")
         e0.record()
         for j in range(Ksteps):
             stp.step(W + j, sel_ptrs[j])
@@ -419,6 +430,10 @@ def main():
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1)
     ms_step = ms / Ksteps
+    prof = None
+    if args.kernel_events == "inline" and not args.graph:
+        prof = radar.profile_read()
+        radar.profile_enable(False)
 
     restructures = stp.restructures - restr_before
     if args.schedule == "sqrt":
@@ -427,13 +442,14 @@ def main():
         radar.build_index(dataclasses.replace(cfg, seg_len=seg_timed,
                                               window=win_timed),
                           K, inp.omega, t_timed, summ)
-    # the same steps again with every kernel bracketed by HIP events
-    radar.profile_enable(True)
-    for j in range(Ksteps):
-        stp.step(W + j)
-    torch.cuda.synchronize()
-    prof = radar.profile_read()
-    radar.profile_enable(False)
+    if prof is None:
+        # the same steps again with every kernel bracketed by HIP events
+        radar.profile_enable(True)
+        for j in range(Ksteps):
+            stp.step(W + j)
+        torch.cuda.synchronize()
+        prof = radar.profile_read()
+        radar.profile_enable(False)
 
     # ---- algorithmic bytes ------------------------------------------------
     sel_np = sel_log.cpu().numpy()
@@ -521,6 +537,8 @@ def main():
                             radar.PATH_SELECT: "select"}.get(path, "?"),
             "schedule": args.schedule,
             "launch": "hip graph replay" if args.graph else "eager",
+            "kernel_events": ("inline" if args.kernel_events == "inline" and not args.graph
+                              else "separate pass"),
             "calls": ("radar_append_decode" if merged
                       else "radar_append + radar_decode"),
             "selector": args.selector,
