@@ -281,7 +281,9 @@ radar_status radar_profile_enable(int32_t on);
 /* Waits for the recorded kernels, adds their durations per radar_kernel kind
  * into ms[0 .. n) and their launch counts into launches[0 .. n) (n >=
  * RADAR_K_COUNT; both arrays are host memory, zeroed by this call), and
- * releases the records. */
+ * releases the records. Their events stay with the calling thread for the
+ * next profiled launches, so a profiled pass that follows another creates
+ * no events. */
 radar_status radar_profile_read(double* ms, int64_t* launches, int32_t n);
 
 /* Measurement microkernels (not part of the method), for reporting the

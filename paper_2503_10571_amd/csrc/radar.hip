@@ -1748,10 +1748,18 @@ thread_local char g_last_error[256] = "";
 // While profiling is enabled on a host thread, every launch goes through
 // hipExtLaunchKernelGGL with a start/stop event pair, so the recorded times
 // bracket exactly that kernel's execution on its stream.
+// Read records return their events to a pool, so a profiled pass that
+// follows another creates no events (event creation is host work that would
+// otherwise slow the launches being timed).
 struct Profiler {
   bool on = false;
   struct Rec { int kind; hipEvent_t a, b; };
   std::vector<Rec> recs;
+  std::vector<hipEvent_t> pool;
+  bool take(hipEvent_t* e) {
+    if (!pool.empty()) { *e = pool.back(); pool.pop_back(); return true; }
+    return hipEventCreate(e) == hipSuccess;
+  }
 };
 thread_local Profiler g_prof;
 
@@ -1760,10 +1768,13 @@ void launch(int kind, F kern, dim3 grid, dim3 block, size_t shm, hipStream_t st,
             Args... args) {
   if (g_prof.on) {
     hipEvent_t a = nullptr, b = nullptr;
-    if (hipEventCreate(&a) == hipSuccess && hipEventCreate(&b) == hipSuccess) {
-      hipExtLaunchKernelGGL(kern, grid, block, (uint32_t)shm, st, a, b, 0u, args...);
-      g_prof.recs.push_back({kind, a, b});
-      return;
+    if (g_prof.take(&a)) {
+      if (g_prof.take(&b)) {
+        hipExtLaunchKernelGGL(kern, grid, block, (uint32_t)shm, st, a, b, 0u, args...);
+        g_prof.recs.push_back({kind, a, b});
+        return;
+      }
+      g_prof.pool.push_back(a);
     }
   }
   hipLaunchKernelGGL(kern, grid, block, shm, st, args...);
@@ -2390,8 +2401,8 @@ radar_status radar_profile_read(double* ms, int64_t* launches, int32_t n) {
       ms[r.kind] += t;
       launches[r.kind] += 1;
     }
-    (void)hipEventDestroy(r.a);
-    (void)hipEventDestroy(r.b);
+    g_prof.pool.push_back(r.a);
+    g_prof.pool.push_back(r.b);
   }
   g_prof.recs.clear();
   return st;
