@@ -1334,13 +1334,17 @@ __global__ __launch_bounds__(256) void k_attend(
 }
 
 // ---------------------------------------------------------------------------
-// k_decode_fused: the whole decode step of one (b, kv head) in one workgroup
+// k_decode_fused: the whole decode step of one (b, kv head) in R workgroups
 // ---------------------------------------------------------------------------
-// Used when there are at least as many (b, kv head) pairs as compute units:
-// then one 512-thread workgroup per pair keeps every CU streaming, and no
-// stage hands data to another workgroup (the per-XCD L2s are not coherent,
-// so a cross-workgroup hand-off would need a kernel boundary or a cache
-// flush). Phases:
+// Every workgroup of a pair runs the whole selection itself (phases 1-4 give
+// the same result in each: the same inputs, the same order of operations),
+// so no stage hands data to another workgroup (the per-XCD L2s are not
+// coherent, so a cross-workgroup hand-off would need a kernel boundary or a
+// cache flush). With R = 1 (at least as many pairs as compute units) one
+// 512-thread workgroup per pair keeps every CU streaming and writes the
+// output; with fewer pairs R workgroups share a pair's attention tiles and
+// each writes a partial that k_combine merges (the repeated summary reads
+// mostly hit the caches). Phases:
 //   1. phi(q) of the group's G heads into LDS (16 lanes per Omega row);
 //   2. Eq. 6 scores of all candidates into LDS (32 summary rows per wave
 //      per pass, streaming loads);
@@ -1348,8 +1352,10 @@ __global__ __launch_bounds__(256) void k_attend(
 //      already attend the window tiles (the window never depends on the
 //      selection);
 //   4. the group's union in LDS;
-//   5. every wave attends segment tiles (tile i to wave i mod 8);
-//   6. the waves' online-softmax states merge in LDS into the output.
+//   5. every wave attends segment tiles (tile i to workgroup i mod R, and
+//      in it to wave (i / R) mod 8);
+//   6. the waves' online-softmax states merge in LDS into the output (or
+//      the workgroup's partial).
 // With SEL set the kernel stops after phase 4 and writes the union to
 // uni_out / ucnt_out for the split path's attention (the select path: one
 // workgroup per pair replaces the phi(q), score and top-k kernels).
@@ -1365,7 +1371,8 @@ __global__ __launch_bounds__(512) void k_decode_fused(
     float* __restrict__ sel_scores, int Hq, int Hkv, int64_t cap,
     int64_t s_cap, int tiles_per_seg, SeqArgs sa, int per_head, float s1,
     float s2, float inv_sqrt_n, float qscale, int* __restrict__ uni_out,
-    int* __restrict__ ucnt_out, int umax, AppendArgs ap) {
+    int* __restrict__ ucnt_out, int umax, AppendArgs ap, int R, int n_pairs,
+    float* __restrict__ part, int maxwg) {
   constexpr int NW = kFusedWaves;
   constexpr int QPL = D / 16;              // q elements per lane (phase 1)
   constexpr int FPL = N / 64;              // features per lane (phase 2)
@@ -1393,7 +1400,11 @@ __global__ __launch_bounds__(512) void k_decode_fused(
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int64_t bh = blockIdx.x;
+  // workgroup rj < R of pair bh: the workgroups of a pair differ by a
+  // multiple of n_pairs, so they share an XCD (and its L2) when n_pairs is a
+  // multiple of 8
+  const int64_t bh = blockIdx.x % n_pairs;
+  const int rj = (int)(blockIdx.x / n_pairs);
   const int64_t b = bh / Hkv, hk = bh % Hkv;
   const T* q0 = q + (b * Hq + hk * G) * D;
   const Span sp = seq_span(sa, b);
@@ -1553,8 +1564,10 @@ __global__ __launch_bounds__(512) void k_decode_fused(
   const int extra_tiles = win_tiles + (sp.sink + kTile - 1) / kTile;
   if (wave < G) {
     const int64_t hq = hk * G + wave;
-    int32_t* so = selected ? selected + (b * Hq + hq) * (int64_t)k : nullptr;
-    float* sco = sel_scores ? sel_scores + (b * Hq + hq) * (int64_t)k : nullptr;
+    // every workgroup of the pair selects the same segments; the first
+    // one reports them
+    int32_t* so = selected && rj == 0 ? selected + (b * Hq + hq) * (int64_t)k : nullptr;
+    float* sco = sel_scores && rj == 0 ? sel_scores + (b * Hq + hq) * (int64_t)k : nullptr;
     const float* src = sc + wave * kFusedMaxCand;
     int* row = sel_lds + wave * k_eff;
     unsigned* hist = hist_lds[wave];
@@ -1566,7 +1579,7 @@ __global__ __launch_bounds__(512) void k_decode_fused(
     else if (npl <= 8) head_topk<8>(src, n_cand, k, k_eff, row, so, sco, lane, hist, list);
     else head_topk<16>(src, n_cand, k, k_eff, row, so, sco, lane, hist, list);
   } else if constexpr (!SEL) {
-    for (int i = wave - G; i < extra_tiles; i += NW - G) {
+    for (int i = rj + (wave - G) * R; i < extra_tiles; i += (NW - G) * R) {
       int64_t start;
       int len;
       if (i < win_tiles) {
@@ -1602,7 +1615,7 @@ __global__ __launch_bounds__(512) void k_decode_fused(
   const int seg_tiles = n_segs * tiles_per_seg;
 
   // ---- 5. segment tiles ---------------------------------------------------
-  for (int i = wave; i < seg_tiles; i += NW) {
+  for (int i = rj + wave * R; i < seg_tiles; i += NW * R) {
     const int e = segs[i / tiles_per_seg];
     const int s = e & ((1 << kUniIdBits) - 1);
     // (the plain selection of a one-head group carries no head mask)
@@ -1639,8 +1652,14 @@ __global__ __launch_bounds__(512) void k_decode_fused(
       a = fmaf(wacc[(w * G + g) * D + e], f, a);
       L = fmaf(wl[w][g], f, L);
     }
-    const float o = !sp.ok ? __uint_as_float(0x7fc00000u) : (L > 0.f ? a / L : 0.f);
-    out[(b * Hq + hk * G + g) * D + e] = from_f32<T>(o);
+    if (R == 1) {
+      const float o = !sp.ok ? __uint_as_float(0x7fc00000u) : (L > 0.f ? a / L : 0.f);
+      out[(b * Hq + hk * G + g) * D + e] = from_f32<T>(o);
+    } else {                               // partial of this workgroup's tiles
+      float* pj = part + ((bh * maxwg + rj) * G + g) * (int64_t)(D + 4);
+      pj[4 + e] = a;
+      if (e == 0) { pj[0] = M; pj[1] = L; }
+    }
   }
 }
 
@@ -1659,7 +1678,7 @@ template <typename T, int D, int NT, int DS>
 __global__ __launch_bounds__(NT) void k_combine(
     const float* __restrict__ part, const int* __restrict__ ucnt,
     T* __restrict__ out, int Hq, int Hkv, int G, int tiles_per_seg,
-    SeqArgs sa, int maxwg, int tpw) {
+    SeqArgs sa, int maxwg, int tpw, int fixed_nwg) {
   constexpr int PSTRIDE = D + 4;
   constexpr int NWAVE = NT / kWave;
   constexpr int NGRP = NT / DS;
@@ -1675,9 +1694,14 @@ __global__ __launch_bounds__(NT) void k_combine(
   const int g = (int)(hq % G);
   const int64_t bh = b * Hkv + hk;
   const Span sp = seq_span(sa, b);
-  const int extra = (int)(((int64_t)sp.t - sp.ws + kTile - 1) / kTile) +
-                    (sp.sink + kTile - 1) / kTile;
-  const int nwg = (ucnt[bh] * tiles_per_seg + extra + 4 * tpw - 1) / (4 * tpw);
+  // partials of the pair: fixed_nwg (one per workgroup of the fused
+  // kernel), or one per 4 tpw tiles of the split attention
+  int nwg = fixed_nwg;
+  if (nwg == 0) {
+    const int extra = (int)(((int64_t)sp.t - sp.ws + kTile - 1) / kTile) +
+                      (sp.sink + kTile - 1) / kTile;
+    nwg = (ucnt[bh] * tiles_per_seg + extra + 4 * tpw - 1) / (4 * tpw);
+  }
   T* o = out + bhq * D + e0;
   if (!sp.ok || nwg == 0) {                // invalid length / nothing attended
     if (tid < DS) o[tid] = from_f32<T>(sp.ok ? 0.f : __uint_as_float(0x7fc00000u));
@@ -1989,6 +2013,25 @@ void launch_score(const Shape& s, const float* phiq, const float* summ,
   }
 }
 
+// The merge of the partials into the output: fixed_nwg partials per pair
+// (the fused kernel's workgroups), or those of the split attention (tpw);
+// partials_per_head bounds their count. Above 128 the dims are split over
+// four workgroups per head.
+template <typename T, int D>
+void launch_combine(const Shape& s, const float* part, const int* ucnt, void* out,
+                    const SeqArgs& sa, const WsLayout& L, int tpw, int fixed_nwg,
+                    int partials_per_head, hipStream_t st) {
+  if (partials_per_head > 128)
+    launch(RADAR_K_COMBINE, k_combine<T, D, 256, 32>,
+           dim3((unsigned)(s.B * s.Hq), (unsigned)(D / 32)), dim3(256), 0, st, part,
+           ucnt, reinterpret_cast<T*>(out), s.Hq, s.Hkv, s.G, L.tiles_per_seg, sa,
+           L.maxwg, tpw, fixed_nwg);
+  else
+    launch(RADAR_K_COMBINE, k_combine<T, D, 1024, D>, dim3((unsigned)(s.B * s.Hq)),
+           dim3(1024), 0, st, part, ucnt, reinterpret_cast<T*>(out), s.Hq, s.Hkv, s.G,
+           L.tiles_per_seg, sa, L.maxwg, tpw, fixed_nwg);
+}
+
 template <typename T, int D, int G>
 void launch_attend_g(const Shape& s, const void* q, const void* K, const void* V,
                      unsigned char* w, const WsLayout& L, int grid_x, int tpw,
@@ -2013,19 +2056,9 @@ void launch_attend_d(const Shape& s, const void* q, const void* K, const void* V
     case 4: launch_attend_g<T, D, 4>(s, q, K, V, w, L, grid_x, tpw, sa, st); break;
     default: launch_attend_g<T, D, 8>(s, q, K, V, w, L, grid_x, tpw, sa, st); break;
   }
-  // partials per head above 128: split the dims over four workgroups
-  if (grid_x > 128)
-    launch(RADAR_K_COMBINE, k_combine<T, D, 256, 32>,
-           dim3((unsigned)(s.B * s.Hq), (unsigned)(D / 32)), dim3(256), 0,
-           st, reinterpret_cast<const float*>(w + L.part),
-           reinterpret_cast<const int*>(w + L.ucnt), reinterpret_cast<T*>(out), s.Hq,
-           s.Hkv, s.G, L.tiles_per_seg, sa, L.maxwg, tpw);
-  else
-    launch(RADAR_K_COMBINE, k_combine<T, D, 1024, D>, dim3((unsigned)(s.B * s.Hq)),
-           dim3(1024), 0,
-           st, reinterpret_cast<const float*>(w + L.part),
-           reinterpret_cast<const int*>(w + L.ucnt), reinterpret_cast<T*>(out), s.Hq,
-           s.Hkv, s.G, L.tiles_per_seg, sa, L.maxwg, tpw);
+  launch_combine<T, D>(s, reinterpret_cast<const float*>(w + L.part),
+                       reinterpret_cast<const int*>(w + L.ucnt), out, sa, L, tpw, 0,
+                       grid_x, st);
 }
 
 // Tiles beyond the union's segments per (b, kv head), the window's and the
@@ -2099,23 +2132,26 @@ radar_status launch_fused_n(const Shape& s, const void* q, const void* K,
                             const float* summ, const SeqArgs& sa, void* out,
                             int32_t* selected, float* sel_scores, int* uni_out,
                             int* ucnt_out, int umax, const AppendArgs& ap,
-                            hipStream_t st) {
+                            int R, float* part, int maxwg, hipStream_t st) {
   const float s1 = kLog2e / std::pow((float)s.d, 0.25f);
   const float s2 = kLog2e / (2.f * std::sqrt((float)s.d));
+  const int n_pairs = s.B * s.Hkv;
   launch(SEL ? RADAR_K_SELECT : RADAR_K_FUSED, k_decode_fused<T, D, G, N, SEL>,
-         dim3((unsigned)(s.B * s.Hkv)), dim3(kFusedWaves * 64), 0, st,
+         dim3((unsigned)(n_pairs * R)), dim3(kFusedWaves * 64), 0, st,
          reinterpret_cast<const T*>(q), reinterpret_cast<const T*>(K),
          reinterpret_cast<const T*>(V), omega, summ, reinterpret_cast<T*>(out),
          selected, sel_scores, s.Hq, s.Hkv, s.cap, s.s_cap, (int)ceil_div(s.c, kTile),
          sa, s.per_head, s1, s2, 1.f / std::sqrt((float)s.n),
-         kLog2e / std::sqrt((float)s.d), uni_out, ucnt_out, umax, ap);
+         kLog2e / std::sqrt((float)s.d), uni_out, ucnt_out, umax, ap, R, n_pairs,
+         part, maxwg);
   return launch_status();
 }
 
-#define RADAR_FUSED_ARGS s, q, K, V, omega, summ, sa, out, selected, sel_scores, uni_out, ucnt_out, umax, ap, st
+#define RADAR_FUSED_ARGS s, q, K, V, omega, summ, sa, out, selected, sel_scores, uni_out, ucnt_out, umax, ap, R, part, maxwg, st
 #define RADAR_FUSED_PARAMS const Shape& s, const void* q, const void* K, const void* V, \
     const float* omega, const float* summ, const SeqArgs& sa, void* out, int32_t* selected, \
-    float* sel_scores, int* uni_out, int* ucnt_out, int umax, const AppendArgs& ap, hipStream_t st
+    float* sel_scores, int* uni_out, int* ucnt_out, int umax, const AppendArgs& ap, int R, \
+    float* part, int maxwg, hipStream_t st
 
 template <typename T, int D, int G, bool SEL>
 radar_status launch_fused_g(RADAR_FUSED_PARAMS) {
@@ -2136,21 +2172,34 @@ radar_status launch_fused_d(RADAR_FUSED_PARAMS) {
   }
 }
 
-// K and V start after the sinks
+// K and V start after the sinks. R workgroups per pair; with R > 1 their
+// partials go to the workspace and k_combine merges them.
 radar_status launch_fused(const Shape& s, const void* q, const void* K, const void* V,
                           const float* omega, const float* summ, const SeqArgs& sa,
                           void* out, int32_t* selected, float* sel_scores,
-                          const AppendArgs& ap, hipStream_t st) {
+                          const AppendArgs& ap, int R, unsigned char* w,
+                          const WsLayout& L, hipStream_t st) {
   int* uni_out = nullptr;
   int* ucnt_out = nullptr;
   const int umax = 0;
+  float* part = R > 1 ? reinterpret_cast<float*>(w + L.part) : nullptr;
+  const int maxwg = L.maxwg;
+  radar_status r;
   if (s.dt == RADAR_BF16)
-    return s.d == 64 ? launch_fused_d<bf16_t, 64, false>(RADAR_FUSED_ARGS)
-                     : launch_fused_d<bf16_t, 128, false>(RADAR_FUSED_ARGS);
+    r = s.d == 64 ? launch_fused_d<bf16_t, 64, false>(RADAR_FUSED_ARGS)
+                  : launch_fused_d<bf16_t, 128, false>(RADAR_FUSED_ARGS);
   // fp32 caches with d = 128 keep the split path: their tiles need more
   // registers than the fused kernel has to spare
-  if (s.d == 64) return launch_fused_d<float, 64, false>(RADAR_FUSED_ARGS);
-  return RADAR_EUNSUPPORTED;
+  else if (s.d == 64) r = launch_fused_d<float, 64, false>(RADAR_FUSED_ARGS);
+  else return RADAR_EUNSUPPORTED;
+  if (r != RADAR_OK || R == 1) return r;
+  if (s.dt == RADAR_BF16) {
+    if (s.d == 64) launch_combine<bf16_t, 64>(s, part, nullptr, out, sa, L, 1, R, R, st);
+    else launch_combine<bf16_t, 128>(s, part, nullptr, out, sa, L, 1, R, R, st);
+  } else {
+    launch_combine<float, 64>(s, part, nullptr, out, sa, L, 1, R, R, st);
+  }
+  return launch_status();
 }
 
 // the select path's first kernel: phi(q), scores, top-k and union of each
@@ -2165,6 +2214,8 @@ radar_status launch_select(const Shape& s, const void* q, const float* omega,
   int* uni_out = reinterpret_cast<int*>(w + L.uni);
   int* ucnt_out = reinterpret_cast<int*>(w + L.ucnt);
   const int umax = L.umax;
+  const int R = 1, maxwg = 0;
+  float* part = nullptr;
   if (s.dt == RADAR_BF16)
     return s.d == 64 ? launch_fused_d<bf16_t, 64, true>(RADAR_FUSED_ARGS)
                      : launch_fused_d<bf16_t, 128, true>(RADAR_FUSED_ARGS);
@@ -2187,14 +2238,16 @@ int64_t pair_bytes(const Shape& s, const SeqArgs& sa) {
 
 // Which decode path a call takes.
 //  - fused: the shape fits its LDS plan and either there are enough (b, kv
-//    head) pairs to occupy every CU, or each pair's step is small enough
-//    (<= 256 KB) that one workgroup streams it in a few microseconds, less
-//    than the split path's extra launches cost;
-//  - select: otherwise, when a pair's summary rows fit one workgroup's
-//    stream (<= 384 KB, about 13 us at a CU's share of HBM): one workgroup per
-//    pair selects, then the split attention spreads the K/V gather over the
-//    chip (measured: the one select kernel beats the three it replaces up to
-//    about 500 KB per pair);
+//    head) pairs to occupy every CU (one workgroup per pair), or each pair's
+//    step is small enough (<= 256 KB) that one workgroup streams it in a few
+//    microseconds, or a pair's summary rows are few (<= 384 KB): then R
+//    workgroups per pair each repeat the selection (the repeated rows mostly
+//    hit the caches) and share the attention (measured: 47k vs 36k tokens/s
+//    for the select path at 16K, 87k vs 86k at 64K GQA; with the 1.5 MB of
+//    rows per pair at 512K the repetition costs more than it saves);
+//  - select: fp32 caches with d = 128 (outside the fused kernel's register
+//    plan) and summary rows <= 384 KB: one workgroup per pair selects, then
+//    the split attention spreads the K/V gather over the chip;
 //  - split: phi(q), scores and top-k as separate chip-wide kernels.
 int choose_path(const Shape& s, const SeqArgs& sa) {
   const int n_cand = make_span(sa.t_max, sa).n_cand;
@@ -2206,9 +2259,11 @@ int choose_path(const Shape& s, const SeqArgs& sa) {
     case RADAR_PATH_SELECT: return fits_select ? RADAR_PATH_SELECT : RADAR_PATH_SPLIT;
     default: break;
   }
-  if (fits_fused && ((int64_t)s.B * s.Hkv >= num_cu() || pair_bytes(s, sa) <= (256 << 10)))
+  const bool few_rows = (int64_t)n_cand * s.n * 4 <= (384 << 10);
+  if (fits_fused && ((int64_t)s.B * s.Hkv >= num_cu() ||
+                     pair_bytes(s, sa) <= (256 << 10) || few_rows))
     return RADAR_PATH_FUSED;
-  if (fits_select && (int64_t)n_cand * s.n * 4 <= (384 << 10)) return RADAR_PATH_SELECT;
+  if (fits_select && few_rows) return RADAR_PATH_SELECT;
   return RADAR_PATH_SPLIT;
 }
 
@@ -2270,14 +2325,33 @@ radar_status refresh_closed(const Shape& s, const void* K, const float* omega,
 struct DecodePlan {
   int path;
   AttendGrid ag;
+  int R;               // fused kernel: workgroups per pair
 };
+
+#ifndef RADAR_FUSED_WAYS_MAX
+#define RADAR_FUSED_WAYS_MAX 1024
+#endif
+
+// Workgroups per pair for the fused kernel: one 512-thread workgroup per
+// CU overall, at most one per partial slot of the workspace, and 1 when the
+// pairs alone fill the chip or a pair's step is small.
+int fused_ways(const Shape& s, const WsLayout& L, const SeqArgs& sa) {
+  const int64_t P = (int64_t)s.B * s.Hkv;
+  if (P >= num_cu() || pair_bytes(s, sa) <= (256 << 10)) return 1;
+  return (int)std::max<int64_t>(
+      1, std::min<int64_t>({num_cu() / P, (int64_t)L.maxwg, RADAR_FUSED_WAYS_MAX}));
+}
 
 radar_status plan_decode(const Shape& s, const WsLayout& L, const SeqArgs& sa,
                          DecodePlan* p) {
   const Span top = make_span(sa.t_max, sa);
   p->path = choose_path(s, sa);
   p->ag = AttendGrid{0, 1};
-  if (p->path == RADAR_PATH_FUSED) return RADAR_OK;
+  p->R = 1;
+  if (p->path == RADAR_PATH_FUSED) {
+    p->R = fused_ways(s, L, sa);
+    return RADAR_OK;
+  }
   const int u_bound = std::min(s.G * top.k_eff, top.n_cand);
   p->ag = attend_grid(s, L, u_bound, extra_tiles(s, sa));
   return p->ag.grid_x > kMaxWg ? RADAR_EUNSUPPORTED : RADAR_OK;
@@ -2296,7 +2370,7 @@ radar_status run_decode(const Shape& s, const WsLayout& L, const SeqArgs& sa,
   const void* Vp = after_sinks(s, V);
   if (plan.path == RADAR_PATH_FUSED)
     return launch_fused(s, q, Kp, Vp, omega, summaries, sa, out, selected, scores, ap,
-                        stream);
+                        plan.R, w, L, stream);
   if (plan.path == RADAR_PATH_SELECT) {
     const radar_status r = launch_select(s, q, omega, summaries, sa, selected, scores,
                                          w, L, ap, stream);

@@ -105,8 +105,9 @@ def test_full_size_sampled(name, steps, ngroups, path):
 
 def test_path_choice():
     """The fused path serves shapes with at least one (b, kv head) pair per
-    CU, or small steps; the select path few pairs with few candidates; G > 4
-    or more than 1024 candidates take the split path."""
+    CU, small steps, or few summary rows per pair (several workgroups per
+    pair); the select path fp32 d = 128 caches with few rows; G > 4, more
+    than 1024 candidates or many rows per pair take the split path."""
     def cfg(wl):
         return H.config_of(wl, wl.t0 + 1)
     n_cu = torch.cuda.get_device_properties(0).multi_processor_count
@@ -120,10 +121,13 @@ def test_path_choice():
     assert radar.decode_path(cfg(tiny), tiny.t0 + 1, tiny.top_k) == radar.PATH_FUSED
     g8 = mha.scaled(n_q_heads=32, n_kv_heads=4, batch=128)
     assert radar.decode_path(cfg(g8), g8.t0 + 1, 16) == radar.PATH_SPLIT
-    # few pairs whose summary rows fit one workgroup's stream: select
+    # few pairs with few summary rows each: fused, several workgroups a pair
     for name in ("llama2_16k", "gqa_64k"):
         w = WORKLOADS[name]
-        assert radar.decode_path(cfg(w), w.t0 + 1, w.top_k) == radar.PATH_SELECT, name
+        assert radar.decode_path(cfg(w), w.t0 + 1, w.top_k) == radar.PATH_FUSED, name
+    # the same with an fp32 cache at d = 128: select
+    f32 = WORKLOADS["llama2_16k"].scaled(dtype="f32")
+    assert radar.decode_path(cfg(f32), f32.t0 + 1, f32.top_k) == radar.PATH_SELECT
     radar.set_decode_path(radar.PATH_FUSED)
     try:
         assert radar.decode_path(cfg(g5), g5.t0 + 1, g5.top_k) == radar.PATH_FUSED
