@@ -229,17 +229,17 @@ radar_status radar_schedule_sqrt(int64_t t, int32_t* seg_len, int32_t* window);
 
 /* Decode paths. The split path runs phi(q), scores, top-k, attention and
  * merge as separate kernels spread over the whole chip; the fused path runs
- * the whole step of one (b, kv head) in one workgroup, which suits shapes
- * with at least as many (b, kv head) pairs as compute units; the select path
- * runs phi(q), scores, top-k and union of each pair in one workgroup and
- * then the split path's attention and merge, which suits few pairs with few
- * candidates. All compute the same method; their fp32 summation orders
- * differ. */
+ * the whole step of one (b, kv head) in R workgroups that each repeat the
+ * pair's selection and share its attention (R = 1 when the pairs fill the
+ * chip or a step is small; with R > 1 a merge kernel follows); the select
+ * path runs phi(q), scores, top-k and union of each pair in one workgroup
+ * and then the split path's attention and merge. All compute the same
+ * method; their fp32 summation orders differ. */
 typedef enum {
   RADAR_PATH_AUTO = 0,   /* fused when the shape fits and either B * Hkv >=
-                            #CUs or one pair's step reads <= 256 KB; else
-                            select when a pair's summary rows are <= 384 KB;
-                            split otherwise                                 */
+                            #CUs, one pair's step reads <= 256 KB, or a
+                            pair's summary rows are <= 384 KB; else select
+                            when the rows are <= 384 KB; split otherwise    */
   RADAR_PATH_SPLIT = 1,
   RADAR_PATH_FUSED = 2,  /* used when the shape fits (G <= 4, at most 1024
                             candidate segments, not fp32 with d = 128),
