@@ -25,7 +25,7 @@ from oracle import radar_oracle as orc  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 
-N_CASES = 100
+N_CASES = 300
 PATHS = (radar.PATH_SPLIT, radar.PATH_FUSED, radar.PATH_SELECT, radar.PATH_AUTO)
 
 
@@ -38,7 +38,8 @@ def draw(seed):
     w = int(rng.choice([0, 5, 64, 150, 300]))
     # keep the candidates within the top-k stage's limit
     t0 = min(t0, 2000 * c + w)
-    n_sink = int(rng.choice([0, 0, 1, 4, 70]))
+    # at most the cache's capacity (t0 + 3 rows), as the config requires
+    n_sink = min(int(rng.choice([0, 0, 1, 4, 70])), t0 + 3)
     wl = Workload(
         f"fuzz{seed}", batch=int(rng.integers(1, 4)), n_q_heads=G * Hkv,
         n_kv_heads=Hkv, head_dim=int(rng.choice([64, 128])), t0=t0, seg_len=c,

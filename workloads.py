@@ -202,7 +202,8 @@ def make_inputs(wl: Workload, device="cpu", steps: int | None = None,
         npl = min(wl.planted, n_cand0)
         segs = torch.rand(S, B, Hq, n_cand0, generator=gp,
                           device=device).argsort(-1)[..., :npl]
-        offs = torch.randint(0, c, (S, B, Hq, npl), generator=gp,
+        # (a context shorter than one segment plants on its own tokens)
+        offs = torch.randint(0, min(c, t0), (S, B, Hq, npl), generator=gp,
                              device=device)
         pos = segs * c + offs                                  # < t0
         bidx = torch.arange(B, device=device)[None, :, None, None]
