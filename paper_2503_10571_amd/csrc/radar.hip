@@ -1667,23 +1667,27 @@ __global__ __launch_bounds__(512) void k_decode_fused(
 // k_combine: log-sum-exp merge of the partials of each (b, q head)
 // ---------------------------------------------------------------------------
 // Grid (B * Hq, D / DS), NT threads: each workgroup produces DS output dims
-// of one query head. With many partials per head (DS = 32, NT = 256) a
-// head's partials are read by several CUs at once; with few (DS = D,
-// NT = 1024) one workgroup per head saves the launches. Every workgroup
-// takes the maximum and the scaled sum over all the head's partials (two
-// floats each, kept in registers between the passes), then NT / DS groups
+// of one query head from at most MAXP partials. Every workgroup takes the
+// maximum and the scaled sum over all the head's partials (a (max, sum)
+// pair each, kept in registers between the passes); then the NT / DS groups
 // of threads sum disjoint subsets of the partials' accumulators over its
 // dims, and LDS adds the groups.
-template <typename T, int D, int NT, int DS>
+// With many partials per head (DS = 32, MAXP = kMaxWg) a head's partials are
+// read by several CUs at once, and each thread issues its first PF
+// accumulator loads before the first reduction, so most of the merge waits
+// on memory once. With few (DS = D, PF = 0) one workgroup per head saves the
+// launches, and the accumulators are read after the reductions.
+template <typename T, int D, int NT, int DS, int MAXP, int PF>
 __global__ __launch_bounds__(NT) void k_combine(
     const float* __restrict__ part, const int* __restrict__ ucnt,
     T* __restrict__ out, int Hq, int Hkv, int G, int tiles_per_seg,
     SeqArgs sa, int maxwg, int tpw, int fixed_nwg) {
   constexpr int PSTRIDE = D + 4;
   constexpr int NWAVE = NT / kWave;
-  constexpr int NGRP = NT / DS;
-  static_assert(D % DS == 0 && kMaxWg % NT == 0, "shape");
-  __shared__ float f_lds[kMaxWg];
+  constexpr int NGRP = NT / DS;            // thread groups over the partials
+  constexpr int PPT = (MAXP + NT - 1) / NT;  // (max, sum) pairs per thread
+  static_assert(D % DS == 0 && MAXP <= kMaxWg && PF * NGRP <= MAXP, "shape");
+  __shared__ float f_lds[MAXP];
   __shared__ float red_lds[2 * NWAVE];
   __shared__ float acc_lds[NT];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -1695,13 +1699,15 @@ __global__ __launch_bounds__(NT) void k_combine(
   const int64_t bh = b * Hkv + hk;
   const Span sp = seq_span(sa, b);
   // partials of the pair: fixed_nwg (one per workgroup of the fused
-  // kernel), or one per 4 tpw tiles of the split attention
+  // kernel), or one per 4 tpw tiles of the split attention; the host sizes
+  // MAXP from the same bound
   int nwg = fixed_nwg;
   if (nwg == 0) {
     const int extra = (int)(((int64_t)sp.t - sp.ws + kTile - 1) / kTile) +
                       (sp.sink + kTile - 1) / kTile;
     nwg = (ucnt[bh] * tiles_per_seg + extra + 4 * tpw - 1) / (4 * tpw);
   }
+  nwg = min(nwg, MAXP);
   T* o = out + bhq * D + e0;
   if (!sp.ok || nwg == 0) {                // invalid length / nothing attended
     if (tid < DS) o[tid] = from_f32<T>(sp.ok ? 0.f : __uint_as_float(0x7fc00000u));
@@ -1710,17 +1716,25 @@ __global__ __launch_bounds__(NT) void k_combine(
   const float* pb = part + ((bh * maxwg) * G + g) * (int64_t)PSTRIDE;
   const int64_t wstride = (int64_t)G * PSTRIDE;
 
-  // each thread's (max, sum) pairs stay in registers between the passes
-  constexpr int PPT = kMaxWg / NT;
   float mw[PPT], lw[PPT];
-  float mx = -INFINITY;
 #pragma unroll
   for (int i = 0; i < PPT; ++i) {
     const int w = tid + i * NT;
     mw[i] = w < nwg ? pb[w * wstride] : -INFINITY;
     lw[i] = w < nwg ? pb[w * wstride + 1] : 0.f;
-    mx = fmaxf(mx, mw[i]);
   }
+  const int e = tid % DS, grp = tid / DS;
+  const float* pe = pb + 4 + e0 + e;
+  float av[PF > 0 ? PF : 1];
+#pragma unroll
+  for (int j = 0; j < PF; ++j) {
+    const int w = grp + j * NGRP;
+    av[j] = w < nwg ? pe[w * wstride] : 0.f;
+  }
+
+  float mx = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < PPT; ++i) mx = fmaxf(mx, mw[i]);
   mx = wave_max(mx);
   if (lane == 0) red_lds[wave] = mx;
   __syncthreads();
@@ -1747,11 +1761,14 @@ __global__ __launch_bounds__(NT) void k_combine(
   float L = 0.f;
 #pragma unroll
   for (int i = 0; i < NWAVE; ++i) L += red_lds[NWAVE + i];
-  const int e = tid % DS, grp = tid / DS;
-  const float* pe = pb + 4 + e0 + e;
   float a = 0.f;
+#pragma unroll
+  for (int j = 0; j < PF; ++j) {
+    const int w = grp + j * NGRP;
+    if (w < nwg) a = fmaf(av[j], f_lds[w], a);
+  }
 #pragma unroll 8
-  for (int w = grp; w < nwg; w += NGRP) a = fmaf(pe[w * wstride], f_lds[w], a);
+  for (int w = grp + PF * NGRP; w < nwg; w += NGRP) a = fmaf(pe[w * wstride], f_lds[w], a);
   acc_lds[tid] = a;
   __syncthreads();
   if (tid < DS) {
@@ -2015,19 +2032,19 @@ void launch_score(const Shape& s, const float* phiq, const float* summ,
 
 // The merge of the partials into the output: fixed_nwg partials per pair
 // (the fused kernel's workgroups), or those of the split attention (tpw);
-// partials_per_head bounds their count. Above 128 the dims are split over
-// four workgroups per head.
+// partials_per_head bounds their count (at most kMaxWg). Above 128 the dims
+// are split over D / 32 workgroups per head.
 template <typename T, int D>
 void launch_combine(const Shape& s, const float* part, const int* ucnt, void* out,
                     const SeqArgs& sa, const WsLayout& L, int tpw, int fixed_nwg,
                     int partials_per_head, hipStream_t st) {
   if (partials_per_head > 128)
-    launch(RADAR_K_COMBINE, k_combine<T, D, 256, 32>,
-           dim3((unsigned)(s.B * s.Hq), (unsigned)(D / 32)), dim3(256), 0, st, part,
+    launch(RADAR_K_COMBINE, k_combine<T, D, 1024, 32, kMaxWg, 16>,
+           dim3((unsigned)(s.B * s.Hq), (unsigned)(D / 32)), dim3(1024), 0, st, part,
            ucnt, reinterpret_cast<T*>(out), s.Hq, s.Hkv, s.G, L.tiles_per_seg, sa,
            L.maxwg, tpw, fixed_nwg);
   else
-    launch(RADAR_K_COMBINE, k_combine<T, D, 1024, D>, dim3((unsigned)(s.B * s.Hq)),
+    launch(RADAR_K_COMBINE, k_combine<T, D, 1024, D, 128, 0>, dim3((unsigned)(s.B * s.Hq)),
            dim3(1024), 0, st, part, ucnt, reinterpret_cast<T*>(out), s.Hq, s.Hkv, s.G,
            L.tiles_per_seg, sa, L.maxwg, tpw, fixed_nwg);
 }
