@@ -160,11 +160,22 @@ def step_bytes(wl, t, U, s_kv, sqrt_schedule=False, exact=False):
     return decode + app + close, decode, kv, scan, app
 
 
-def measured_traffic(kernel, workload):
+def run_signature(line):
+    """What fixes the bytes per launch of a run besides the workload: the
+    step range (the context grows by one row a step) and the call form."""
+    cfg = line["config"]
+    return {"steps": line["steps"], "warmup": line["warmup"],
+            "decode_path": cfg["decode_path"], "schedule": cfg["schedule"],
+            "calls": cfg["calls"], "selector": cfg["selector"]}
+
+
+def measured_traffic(kernel, workload, line):
     """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
     record (FETCH_SIZE and WRITE_SIZE KiB per dispatch, each divided by the
-    scale a 1 GiB copy kernel shows), or None when there is no record or the
-    kernel source has changed since it was taken."""
+    scale a 1 GiB copy kernel shows), or None when there is no record, the
+    kernel source has changed since it was taken, or the record's run had
+    another step range or call form than this one (its launches then move
+    other bytes)."""
     import hashlib
     path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.json")
     if not os.path.exists(path):
@@ -172,6 +183,8 @@ def measured_traffic(kernel, workload):
     rec = json.load(open(path))
     src = os.path.join(ROOT, rec["source"])
     if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["source_sha256"]:
+        return None
+    if rec.get("run") != run_signature(line):
         return None
     return int(rec["fetch_size_kib"] * 1024 / rec["fetch_scale"] +
                rec["write_size_kib"] * 1024 / rec["write_scale"])
@@ -570,7 +583,7 @@ def main():
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": round(dom_gbps / HBM_PEAK_GBPS, 4),
-            "traffic": measured_traffic(dom_name, wl.name),
+            "traffic": None,              # filled in below
             "bytes_per_launch": int(dom_bytes // Ksteps),
             "avg_us": round(dom_avg_ms * 1e3, 2),
         },
@@ -588,6 +601,7 @@ def main():
         },
         "cpu_baseline": cpu,
     }
+    line["roofline"]["traffic"] = measured_traffic(dom_name, wl.name, line)
     if copy_gbps is not None:
         line["copy_GBps"] = round(copy_gbps, 1)
         line["roofline"]["frac_of_copy"] = round(dom_gbps / copy_gbps, 4)
