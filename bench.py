@@ -55,7 +55,7 @@ class Stepper:
     """Direct C-ABI calls with pre-marshalled arguments (the per-step host
     cost stays small next to the GPU time)."""
 
-    def __init__(self, cfg, inp, K, V, summ, ws, out, k, sqrt_schedule=False,
+    def __init__(self, cfg, inp, K, V, summ, ws, out, k, omega, sqrt_schedule=False,
                  exact=False, merged=True):
         self.L = radar.lib()
         self.sqrt = sqrt_schedule
@@ -67,7 +67,7 @@ class Stepper:
         self.inp = inp
         P = ctypes.c_void_p
         self.K, self.V = P(K.data_ptr()), P(V.data_ptr())
-        self.om = P(inp.omega.data_ptr())
+        self.om = P(omega.data_ptr())
         self.summ = P(summ.data_ptr())
         self.ws, self.ws_n = P(ws.data_ptr()), ws.numel()
         self.out = P(out.data_ptr())
@@ -133,12 +133,13 @@ def union_sizes(sel, G):
     return out
 
 
-def step_bytes(wl, t, U, s_kv, sqrt_schedule=False, exact=False):
+def step_bytes(wl, t, U, s_kv, sqrt_schedule=False, exact=False, s_om=4):
     """Algorithmic HBM bytes of one step whose decode runs at length t (the
     append wrote row t - 1). U: union size per (b, kv head).
     Returns (whole step, decode call, K/V gather, candidate-key scan, row
     append); with exact=True the selection scans every candidate key
-    instead of reading phi(q)'s inputs and the summaries."""
+    instead of reading phi(q)'s inputs and the summaries. s_om: bytes per
+    Omega entry."""
     d, n = wl.head_dim, wl.n_features
     if sqrt_schedule:
         c, w = radar.schedule_sqrt(t)
@@ -150,7 +151,7 @@ def step_bytes(wl, t, U, s_kv, sqrt_schedule=False, exact=False):
     summ = BH * n_cand * n * 4
     kv = int(np.sum(U * c + W)) * d * 2 * s_kv
     qo = wl.batch * wl.n_q_heads * d * 2 * s_kv
-    om = n * d * 4
+    om = n * d * s_om
     app = BH * 4 * d * s_kv            # read k_new, v_new; write both rows
     close = BH * (c * d * s_kv + n * 4) if t % c == 0 else 0
     if sqrt_schedule and w == 0:       # restructure: all t keys re-summarised
@@ -166,7 +167,8 @@ def run_signature(line):
     cfg = line["config"]
     return {"steps": line["steps"], "warmup": line["warmup"],
             "decode_path": cfg["decode_path"], "schedule": cfg["schedule"],
-            "calls": cfg["calls"], "selector": cfg["selector"]}
+            "calls": cfg["calls"], "selector": cfg["selector"],
+            "omega": cfg["omega"]}
 
 
 def measured_traffic(kernel, workload, line):
@@ -340,6 +342,11 @@ def main():
                     help="instead of timing: recall of Radar's selection "
                          "against the exact search over n and k, one JSON "
                          "line per (n, k)")
+    ap.add_argument("--omega", default="auto", choices=["auto", "f32"],
+                    help="auto: Omega passed as bf16 for bf16 caches (their "
+                         "projection rounds it to bf16 anyway; same results, "
+                         "half the Omega bytes), fp32 otherwise; f32: always "
+                         "fp32")
     ap.add_argument("--schedule", default="fixed", choices=["fixed", "sqrt"],
                     help="fixed: the workload's segment length and window; "
                          "sqrt: Algorithm 1's restructuring (c = sqrt(t) at "
@@ -369,10 +376,15 @@ def main():
     if args.schedule == "sqrt":
         c0, w0 = radar.schedule_sqrt(wl.t0)
         wl = wl.scaled(seg_len=c0, window=w0)
+    omega = inp.omega
+    if args.omega == "auto" and wl.dtype == "bf16":
+        omega = inp.omega.to(torch.bfloat16)    # exact: the values are bf16
+        assert torch.equal(omega.float(), inp.omega)
     cfg = radar.Config(wl.batch, wl.n_q_heads, wl.n_kv_heads, wl.head_dim,
                        wl.n_features, wl.seg_len, wl.window, wl.t0 + total,
-                       wl.torch_dtype())
+                       wl.torch_dtype(), omega_dtype=omega.dtype)
     s_kv = 2 if wl.dtype == "bf16" else 4
+    s_om = omega.element_size()
     K, V = inp.K, inp.V
     summ = radar.new_summaries(cfg, K.device)
     if args.schedule == "sqrt":
@@ -389,12 +401,12 @@ def main():
 
     # ---- index build (Eq. 4-5 over the whole prefix) --------------------
     log("[bench] index build")
-    radar.build_index(cfg, K, inp.omega, wl.t0, summ)
+    radar.build_index(cfg, K, omega, wl.t0, summ)
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
     for _ in range(args.build_reps):
-        radar.build_index(cfg, K, inp.omega, wl.t0, summ)
+        radar.build_index(cfg, K, omega, wl.t0, summ)
     e1.record()
     torch.cuda.synchronize()
     build_ms = e0.elapsed_time(e1) / args.build_reps
@@ -405,7 +417,7 @@ def main():
 
     # ---- decode steps ----------------------------------------------------
     merged = bool(args.merged) and not exact
-    stp = Stepper(cfg, inp, K, V, summ, ws, out, wl.top_k,
+    stp = Stepper(cfg, inp, K, V, summ, ws, out, wl.top_k, omega,
                   sqrt_schedule=args.schedule == "sqrt", exact=exact,
                   merged=merged)
     sel_log = torch.empty(Ksteps, wl.batch, wl.n_q_heads, wl.top_k,
@@ -426,7 +438,7 @@ def main():
             stp.cfg_c.seg_len, stp.cfg_c.window = seg_timed, win_timed
             radar.build_index(dataclasses.replace(cfg, seg_len=seg_timed,
                                                   window=win_timed),
-                              K, inp.omega, t_timed, summ)
+                              K, omega, t_timed, summ)
         torch.cuda.synchronize()
 
     def profiled_pass():
@@ -487,7 +499,8 @@ def main():
         t = wl.t0 + W + j + 1
         U = union_sizes(sel_np[j], wl.group)
         b_all, b_dec, b_kv, b_scan, b_app = step_bytes(
-            wl, t, U, s_kv, sqrt_schedule=args.schedule == "sqrt", exact=exact)
+            wl, t, U, s_kv, sqrt_schedule=args.schedule == "sqrt", exact=exact,
+            s_om=s_om)
         tot_bytes += b_all
         # with the merged call the fused kernel also does the row append
         dec_bytes += b_dec + (b_app if merged else 0)
@@ -571,6 +584,7 @@ def main():
             "calls": ("radar_append_decode" if merged
                       else "radar_append + radar_decode"),
             "selector": args.selector,
+            "omega": "bf16" if s_om == 2 else "f32",
             "restructures": restructures,
         },
         "hbm_GBps": round(step_gbps, 1),

@@ -19,8 +19,8 @@
  *    (the path override and the profiling switch are host-side settings of
  *    the calling thread).
  *  - Layouts are dense, row-major, element type `kv_dtype` for q / K / V /
- *    k_new / v_new / out, fp32 for Omega, summaries and scores, int32 for
- *    segment ids:
+ *    k_new / v_new / out, `omega_dtype` for Omega, fp32 for summaries and
+ *    scores, int32 for segment ids:
  *        q, out          [B][Hq][d]
  *        K, V            [B][Hkv][capacity][d]     (token-major per head)
  *        k_new, v_new    [B][Hkv][d]
@@ -88,7 +88,7 @@
 extern "C" {
 #endif
 
-#define RADAR_ABI_VERSION 3
+#define RADAR_ABI_VERSION 4
 
 typedef enum {
   RADAR_OK = 0,
@@ -118,6 +118,12 @@ typedef struct {
   radar_dtype kv_dtype;
   int32_t n_sink;      /* attention-sink tokens, 0 .. capacity (0: none)    */
   radar_gqa gqa_mode;  /* which segments a grouped query head attends       */
+  radar_dtype omega_dtype;  /* element type of Omega: RADAR_F32, or
+                          RADAR_BF16 with a bf16 cache only (its projection
+                          rounds Omega to bf16 anyway, so a bf16 copy gives
+                          the same results and halves the Omega bytes every
+                          decode reads); a zero-initialised config means
+                          fp32                                             */
 } radar_config;
 
 /* Index build (Eq. 4 and Eq. 5; Algorithm 1's restructuring step that
@@ -125,7 +131,7 @@ typedef struct {
  * 0 .. floor((t - n_sink) / c) - 1 of every (b, kv head) from the rows of K
  * before t. Rows beyond are not touched. Requires 1 <= t <= capacity. */
 radar_status radar_build_index(const radar_config* cfg, const void* K,
-                               const float* omega, int64_t t,
+                               const void* omega, int64_t t,
                                float* summaries, hipStream_t stream);
 
 /* Append one token (Algorithm 1: the new key joins the buffer W). Writes
@@ -139,7 +145,7 @@ radar_status radar_build_index(const radar_config* cfg, const void* K,
  * skipped (no write, no summary). */
 radar_status radar_append(const radar_config* cfg, void* K, void* V,
                           const void* k_new, const void* v_new,
-                          const float* omega, int64_t t, const int64_t* pos,
+                          const void* omega, int64_t t, const int64_t* pos,
                           float* summaries, hipStream_t stream);
 
 /* Decode one query per (b, q head) (Algorithm 1, querying step): phi(q)
@@ -152,7 +158,7 @@ radar_status radar_append(const radar_config* cfg, void* K, void* V,
  * least radar_decode_workspace_bytes(cfg, k) bytes; its contents on entry do
  * not matter and it must not be used by another call at the same time. */
 radar_status radar_decode(const radar_config* cfg, const void* q,
-                          const void* K, const void* V, const float* omega,
+                          const void* K, const void* V, const void* omega,
                           const float* summaries, int64_t t,
                           const int64_t* lens, int32_t k, void* out,
                           int32_t* selected, float* scores, void* workspace,
@@ -176,7 +182,7 @@ radar_status radar_decode(const radar_config* cfg, const void* q,
  * and radar_decode; the workspace is radar_decode's. */
 radar_status radar_append_decode(const radar_config* cfg, const void* q,
                                  void* K, void* V, const void* k_new,
-                                 const void* v_new, const float* omega,
+                                 const void* v_new, const void* omega,
                                  float* summaries, int64_t t,
                                  const int64_t* pos, int32_t k, void* out,
                                  int32_t* selected, float* scores,

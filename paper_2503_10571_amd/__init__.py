@@ -17,7 +17,7 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libradar.so")
 
-ABI_VERSION = 3
+ABI_VERSION = 4
 RADAR_F32, RADAR_BF16 = 0, 1
 GQA_UNION, GQA_PER_HEAD = 0, 1
 STATUS = {0: "ok", 1: "invalid argument", 2: "position outside the cache capacity",
@@ -40,7 +40,7 @@ class _Config(ctypes.Structure):
                 ("n_features", ctypes.c_int32), ("seg_len", ctypes.c_int32),
                 ("window", ctypes.c_int32), ("capacity", ctypes.c_int64),
                 ("kv_dtype", ctypes.c_int32), ("n_sink", ctypes.c_int32),
-                ("gqa_mode", ctypes.c_int32)]
+                ("gqa_mode", ctypes.c_int32), ("omega_dtype", ctypes.c_int32)]
 
 
 @dataclasses.dataclass(frozen=True)
@@ -48,7 +48,10 @@ class Config:
     """Shape of one Radar layer (mirrors radar_config). n_sink: leading
     attention-sink tokens (always attended, in no segment); gqa_mode:
     GQA_UNION (each query head attends its group's union) or GQA_PER_HEAD
-    (its own selection)."""
+    (its own selection); omega_dtype: the element type of the Omega tensor
+    passed to every call (torch.bfloat16 only with a bf16 cache, whose
+    projection rounds Omega to bf16 anyway: the same results from half the
+    Omega bytes)."""
     batch: int
     n_q_heads: int
     n_kv_heads: int
@@ -60,13 +63,14 @@ class Config:
     dtype: torch.dtype = torch.bfloat16
     n_sink: int = 0
     gqa_mode: int = GQA_UNION
+    omega_dtype: torch.dtype = torch.float32
 
     def c_struct(self) -> _Config:
-        dt = {torch.float32: RADAR_F32, torch.bfloat16: RADAR_BF16}[self.dtype]
+        codes = {torch.float32: RADAR_F32, torch.bfloat16: RADAR_BF16}
         return _Config(self.batch, self.n_q_heads, self.n_kv_heads,
                        self.head_dim, self.n_features, self.seg_len,
-                       self.window, self.capacity, dt, self.n_sink,
-                       self.gqa_mode)
+                       self.window, self.capacity, codes[self.dtype], self.n_sink,
+                       self.gqa_mode, codes[self.omega_dtype])
 
     @property
     def summary_rows(self) -> int:
@@ -179,7 +183,7 @@ def _query(cfg, q):
 
 
 def _omega(cfg, omega):
-    _need(omega, torch.float32, "omega", cfg.n_features * cfg.head_dim)
+    _need(omega, cfg.omega_dtype, "omega", cfg.n_features * cfg.head_dim)
 
 
 def _summ(cfg, summaries):

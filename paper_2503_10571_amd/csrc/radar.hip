@@ -212,6 +212,54 @@ __device__ __forceinline__ float4 ld_stream_f4(const float* p) {
   return make_float4(t.x, t.y, t.z, t.w);
 }
 
+// Omega is fp32 [n][d], or bf16 [n][d] for bf16 caches (whose projection
+// rounds Omega to bf16 anyway, so both give the same products); four
+// consecutive entries from element idx, widened to fp32 (exact for bf16).
+// fp32 caches always pass fp32 Omega.
+template <bool BF>
+__device__ __forceinline__ float4 load_omega4(const void* omega, int64_t idx) {
+  if constexpr (BF) {
+    const uint2 u = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(omega) + idx);
+    return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
+                       __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u));
+  } else {
+    return *reinterpret_cast<const float4*>(static_cast<const float*>(omega) + idx);
+  }
+}
+
+// NR rows of QPL Omega entries (row_idx(p): element index of row p's first
+// entry), stored as bf16 (BF) or fp32, all loads issued together and kept
+// as raw words (fp32: four floats; bf16: four values in .x and .y);
+// omega_f4 widens a word where it is used. Callers choose BF at compile
+// time, so no branch or conversion sits between these loads and the loads
+// issued after them.
+template <bool BF, int NR, int QPL, typename F>
+__device__ __forceinline__ void load_omega_rows(uint4 (&raw)[NR][QPL / 4], const void* omega,
+                                                F&& row_idx) {
+#pragma unroll
+  for (int p = 0; p < NR; ++p)
+#pragma unroll
+    for (int e4 = 0; e4 < QPL / 4; ++e4) {
+      if constexpr (BF) {
+        const uint2 u = *reinterpret_cast<const uint2*>(
+            static_cast<const uint16_t*>(omega) + row_idx(p) + 4 * e4);
+        raw[p][e4] = make_uint4(u.x, u.y, 0u, 0u);
+      } else {
+        raw[p][e4] = *reinterpret_cast<const uint4*>(
+            static_cast<const float*>(omega) + row_idx(p) + 4 * e4);
+      }
+    }
+}
+template <bool BF>
+__device__ __forceinline__ float4 omega_f4(uint4 w) {
+  if constexpr (BF)
+    return make_float4(__uint_as_float(w.x << 16), __uint_as_float(w.x & 0xffff0000u),
+                       __uint_as_float(w.y << 16), __uint_as_float(w.y & 0xffff0000u));
+  else
+    return make_float4(__uint_as_float(w.x), __uint_as_float(w.y), __uint_as_float(w.z),
+                       __uint_as_float(w.w));
+}
+
 // ---------------------------------------------------------------------------
 // cross-lane exchanges
 // ---------------------------------------------------------------------------
@@ -346,7 +394,7 @@ struct BuildTile {
 
 template <typename T, int D, int FT>
 __global__ __launch_bounds__(256) void k_build(
-    const T* __restrict__ K, const float* __restrict__ omega,
+    const T* __restrict__ K, const void* __restrict__ omega, bool obf,
     float* __restrict__ summ, int n, int c, int64_t cap, int64_t s_cap,
     int seg_first, int seg_count, int64_t n_items, float s1, float s2,
     float out_scale, int64_t kv_head_stride_rows,
@@ -372,12 +420,13 @@ __global__ __launch_bounds__(256) void k_build(
   typename MC::frag_t bfrag[FT][KB];
 #pragma unroll
   for (int f = 0; f < FT; ++f) {
-    const float* orow = omega + (int64_t)(fbase + f * 16 + col) * D;
+    const int64_t orow = (int64_t)(fbase + f * 16 + col) * D;
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb) {
       if constexpr (sizeof(T) == 2) {
-        const float4 a = *reinterpret_cast<const float4*>(orow + kb * 32 + grp * 8);
-        const float4 b = *reinterpret_cast<const float4*>(orow + kb * 32 + grp * 8 + 4);
+        const int64_t i0 = orow + kb * 32 + grp * 8;
+        const float4 a = obf ? load_omega4<true>(omega, i0) : load_omega4<false>(omega, i0);
+        const float4 b = obf ? load_omega4<true>(omega, i0 + 4) : load_omega4<false>(omega, i0 + 4);
         bf16x8_t v;
         v[0] = (short)f32_to_bf16(a.x); v[1] = (short)f32_to_bf16(a.y);
         v[2] = (short)f32_to_bf16(a.z); v[3] = (short)f32_to_bf16(a.w);
@@ -385,7 +434,7 @@ __global__ __launch_bounds__(256) void k_build(
         v[6] = (short)f32_to_bf16(b.z); v[7] = (short)f32_to_bf16(b.w);
         bfrag[f][kb] = v;
       } else {
-        bfrag[f][kb] = orow[kb * 4 + grp];
+        bfrag[f][kb] = static_cast<const float*>(omega)[orow + kb * 4 + grp];
       }
     }
   }
@@ -629,9 +678,9 @@ __global__ __launch_bounds__(64) void k_append(AppendArgs ap, int64_t cap, int H
 // lane are reduced across its 16 lanes (transpose-reduce over 4 lanes, then
 // two butterflies), so lane jj < 4 of row group r ends with feature
 // 16 w + 4 jj + r.
-template <typename T, int D, int G>
+template <typename T, int D, int G, bool BF>
 __global__ __launch_bounds__(256) void k_phi_q(const T* __restrict__ q,
-                                               const float* __restrict__ omega,
+                                               const void* __restrict__ omega,
                                                float* __restrict__ phiq,
                                                int n, int Hq, int Hkv, float s1,
                                                float s2, float inv_sqrt_n) {
@@ -644,14 +693,10 @@ __global__ __launch_bounds__(256) void k_phi_q(const T* __restrict__ q,
   const int64_t hq0 = b * Hq + hk * G;     // the group's first (b, q head)
   const int f0 = blockIdx.x * 64 + wave * 16;
 
-  float4 om[4][QPL / 4];
-#pragma unroll
-  for (int p = 0; p < 4; ++p) {
-    const float* orow = omega + (int64_t)(f0 + p * 4 + r) * D + jj * QPL;
-#pragma unroll
-    for (int e4 = 0; e4 < QPL / 4; ++e4)
-      om[p][e4] = *reinterpret_cast<const float4*>(orow + 4 * e4);
-  }
+  uint4 om[4][QPL / 4];
+  load_omega_rows<BF, 4, QPL>(om, omega, [&](int p) {
+    return (int64_t)(f0 + p * 4 + r) * D + jj * QPL;
+  });
 #pragma unroll
   for (int g = 0; g < G; ++g) {
     float qv[QPL];
@@ -667,8 +712,8 @@ __global__ __launch_bounds__(256) void k_phi_q(const T* __restrict__ q,
       float a = 0.f;
 #pragma unroll
       for (int e4 = 0; e4 < QPL / 4; ++e4) {
-        float4 o = om[p][e4];
-        if constexpr (sizeof(T) == 2) {
+        float4 o = omega_f4<BF>(om[p][e4]);
+        if constexpr (sizeof(T) == 2 && !BF) {
           o.x = round_bf16(o.x); o.y = round_bf16(o.y);
           o.z = round_bf16(o.z); o.w = round_bf16(o.w);
         }
@@ -1366,7 +1411,7 @@ constexpr int kFusedMaxCand = 1024;
 template <typename T, int D, int G, int N, bool SEL>
 __global__ __launch_bounds__(512) void k_decode_fused(
     const T* __restrict__ q, const T* __restrict__ K, const T* __restrict__ V,
-    const float* __restrict__ omega, const float* __restrict__ summ,
+    const void* __restrict__ omega, bool obf, const float* __restrict__ summ,
     T* __restrict__ out, int32_t* __restrict__ selected,
     float* __restrict__ sel_scores, int Hq, int Hkv, int64_t cap,
     int64_t s_cap, int tiles_per_seg, SeqArgs sa, int per_head, float s1,
@@ -1453,32 +1498,37 @@ __global__ __launch_bounds__(512) void k_decode_fused(
     // ---- 1. phi(q) -----------------------------------------------------
     // 16 lanes per Omega row, 4 rows per wave and pass, NP passes. All of a
     // chunk's Omega loads are issued before any is used, then the summary
-    // rows (when they fit in registers next to them), then the dots.
+    // rows (when they fit in registers next to them), then the dots. The
+    // phase is compiled once per Omega storage type (BF: bf16) and one copy
+    // runs, so both kinds of load stay in flight together.
     const int rb0 = wave * 16 * RB;
-    {
+    auto phase1 = [&](auto bf_tag) {
+      constexpr bool BF = decltype(bf_tag)::value;
       constexpr int NP = N / (4 * NW);       // passes
       constexpr int PC = NP < 8 ? NP : 8;    // passes per load chunk
       constexpr bool kPrefetch = NP <= 8;
       const int r = lane >> 4, jj = lane & 15;
       float qv[G][QPL], nrm[G];
-#pragma unroll
-      for (int g = 0; g < G; ++g)
-#pragma unroll
-        for (int e = 0; e < QPL; ++e) qv[g][e] = to_f32<T>(q0[g * D + jj * QPL + e]);
       float ph[NP][G];
 #pragma unroll
       for (int c0 = 0; c0 < NP; c0 += PC) {
-        float4 om[PC][QPL / 4];
+        // the Omega loads come first in each copy of the phase, so the
+        // compiler cannot hoist the q loads and their conversion (code the
+        // two copies share) above the choice of copy, where they would
+        // have to be waited for
+        uint4 om[PC][QPL / 4];
+        load_omega_rows<BF, PC, QPL>(om, omega, [&](int p) {
+          return (int64_t)((c0 + p) * 4 * NW + wave * 4 + r) * D + jj * QPL;
+        });
+        if (c0 == 0) {
 #pragma unroll
-        for (int p = 0; p < PC; ++p) {
-          const float* orow = omega + (int64_t)((c0 + p) * 4 * NW + wave * 4 + r) * D + jj * QPL;
+          for (int g = 0; g < G; ++g)
 #pragma unroll
-          for (int e4 = 0; e4 < QPL / 4; ++e4)
-            om[p][e4] = *reinterpret_cast<const float4*>(orow + 4 * e4);
+            for (int e = 0; e < QPL; ++e) qv[g][e] = to_f32<T>(q0[g * D + jj * QPL + e]);
         }
-        // unconditional (rows clamp to the last candidate), so no branch
-        // makes the compiler wait for these loads before the dots
-        if (kPrefetch && c0 == 0) load_rows(rb0);
+        // rows clamp to the last candidate; a wave whose first row is past
+        // it has no rows (the candidate count is uniform)
+        if (kPrefetch && c0 == 0 && rb0 < n_cand) load_rows(rb0);
         if (c0 == 0) {
 #pragma unroll
           for (int g = 0; g < G; ++g) {
@@ -1495,8 +1545,8 @@ __global__ __launch_bounds__(512) void k_decode_fused(
           for (int g = 0; g < G; ++g) a[g] = 0.f;
 #pragma unroll
           for (int e4 = 0; e4 < QPL / 4; ++e4) {
-            float4 o = om[p][e4];
-            if constexpr (sizeof(T) == 2) {
+            float4 o = omega_f4<BF>(om[p][e4]);
+            if constexpr (sizeof(T) == 2 && !BF) {
               o.x = round_bf16(o.x); o.y = round_bf16(o.y);
               o.z = round_bf16(o.z); o.w = round_bf16(o.w);
             }
@@ -1513,13 +1563,19 @@ __global__ __launch_bounds__(512) void k_decode_fused(
             ph[c0 + p][g] = fast_exp2(fmaf(row_sum(a[g]), s1, -nrm[g] * s2)) * inv_sqrt_n;
         }
       }
-      if (!kPrefetch) load_rows(rb0);
+      if (!kPrefetch && rb0 < n_cand) load_rows(rb0);
       if (jj == 0) {
 #pragma unroll
         for (int p = 0; p < NP; ++p)
 #pragma unroll
           for (int g = 0; g < G; ++g) phq[g * N + p * 4 * NW + wave * 4 + r] = ph[p][g];
       }
+    };
+    if constexpr (sizeof(T) == 2) {
+      if (obf) phase1(std::true_type{});
+      else phase1(std::false_type{});
+    } else {
+      phase1(std::false_type{});
     }
     __syncthreads();
 
@@ -1825,6 +1881,7 @@ struct Shape {
   int B, Hq, Hkv, G, d, n, c, w, n_sink, per_head;
   int64_t cap, s_cap;
   radar_dtype dt;
+  bool obf;                                // Omega stored as bf16
 };
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -1836,6 +1893,9 @@ radar_status check_cfg(const radar_config* cfg, Shape* s) {
       cfg->n_q_heads % cfg->n_kv_heads != 0)
     return RADAR_EINVAL;
   if (cfg->kv_dtype != RADAR_F32 && cfg->kv_dtype != RADAR_BF16) return RADAR_EINVAL;
+  if (cfg->omega_dtype != RADAR_F32 && cfg->omega_dtype != RADAR_BF16) return RADAR_EINVAL;
+  // a bf16 Omega only where the projection rounds Omega to bf16
+  if (cfg->omega_dtype == RADAR_BF16 && cfg->kv_dtype != RADAR_BF16) return RADAR_EINVAL;
   if (cfg->n_sink < 0 || cfg->n_sink > cfg->capacity) return RADAR_EINVAL;
   if (cfg->gqa_mode != RADAR_GQA_UNION && cfg->gqa_mode != RADAR_GQA_PER_HEAD)
     return RADAR_EINVAL;
@@ -1851,6 +1911,7 @@ radar_status check_cfg(const radar_config* cfg, Shape* s) {
   s->d = cfg->head_dim; s->n = n; s->c = cfg->seg_len; s->w = cfg->window;
   s->cap = cfg->capacity; s->s_cap = cfg->capacity / cfg->seg_len;
   s->dt = cfg->kv_dtype; s->n_sink = cfg->n_sink;
+  s->obf = cfg->omega_dtype == RADAR_BF16;
   s->per_head = cfg->gqa_mode == RADAR_GQA_PER_HEAD;
   return RADAR_OK;
 }
@@ -1904,7 +1965,7 @@ int num_cu() {
 }
 
 template <typename T, int D, int FT>
-radar_status launch_build_t(const Shape& s, const void* K, const float* omega,
+radar_status launch_build_t(const Shape& s, const void* K, const void* omega,
                             float* summ, int seg_first, int seg_count,
                             const int64_t* pos, hipStream_t st) {
   const int slices = s.n / (64 * FT);
@@ -1922,14 +1983,14 @@ radar_status launch_build_t(const Shape& s, const void* K, const float* omega,
   const float s2 = kLog2e / (2.f * std::sqrt((float)s.d));
   const float out_scale = 1.f / ((float)s.c * std::sqrt((float)s.n));
   launch(RADAR_K_BUILD, kern, dim3((unsigned)gx, (unsigned)slices), dim3(256), 0, st,
-                     reinterpret_cast<const T*>(K), omega, summ, s.n, s.c, s.cap,
+                     reinterpret_cast<const T*>(K), omega, s.obf, summ, s.n, s.c, s.cap,
                      s.s_cap, seg_first, seg_count, items, s1, s2, out_scale, s.cap,
                      pos, s.Hkv, s.n_sink);
   return launch_status();
 }
 
 template <typename T, int D>
-radar_status launch_build_d(const Shape& s, const void* K, const float* omega,
+radar_status launch_build_d(const Shape& s, const void* K, const void* omega,
                             float* summ, int seg_first, int seg_count,
                             const int64_t* pos, hipStream_t st) {
   // features per workgroup = 64 * FT; FT capped so the resident Omega slice
@@ -1949,7 +2010,7 @@ radar_status launch_build_d(const Shape& s, const void* K, const float* omega,
 
 // K: the first row after the sinks (after_sinks); pos: per-sequence segment
 // closes (seg_first / seg_count then 0 / 1)
-radar_status launch_build(const Shape& s, const void* K, const float* omega,
+radar_status launch_build(const Shape& s, const void* K, const void* omega,
                           float* summ, int seg_first, int seg_count,
                           const int64_t* pos, hipStream_t st) {
   if (s.dt == RADAR_BF16)
@@ -1971,18 +2032,26 @@ P* after_sinks(const Shape& s, P* p) {
 
 // ---- decode pieces -------------------------------------------------------
 template <typename T, int D, int G>
-void launch_phi_q_g(const Shape& s, const void* q, const float* omega, float* phiq,
+void launch_phi_q_g(const Shape& s, const void* q, const void* omega, float* phiq,
                     hipStream_t st) {
   const float s1 = kLog2e / std::pow((float)s.d, 0.25f);
   const float s2 = kLog2e / (2.f * std::sqrt((float)s.d));
-  launch(RADAR_K_PHI_Q, k_phi_q<T, D, G>,
-         dim3((unsigned)(s.n / 64), (unsigned)(s.B * s.Hkv)), dim3(256), 0, st,
+  const dim3 grid((unsigned)(s.n / 64), (unsigned)(s.B * s.Hkv));
+  if constexpr (sizeof(T) == 2) {
+    if (s.obf) {
+      launch(RADAR_K_PHI_Q, k_phi_q<T, D, G, true>, grid, dim3(256), 0, st,
+             reinterpret_cast<const T*>(q), omega, phiq, s.n, s.Hq, s.Hkv, s1, s2,
+             1.f / std::sqrt((float)s.n));
+      return;
+    }
+  }
+  launch(RADAR_K_PHI_Q, k_phi_q<T, D, G, false>, grid, dim3(256), 0, st,
          reinterpret_cast<const T*>(q), omega, phiq, s.n, s.Hq, s.Hkv, s1, s2,
          1.f / std::sqrt((float)s.n));
 }
 
 template <typename T, int D>
-void launch_phi_q(const Shape& s, const void* q, const float* omega, float* phiq,
+void launch_phi_q(const Shape& s, const void* q, const void* omega, float* phiq,
                   hipStream_t st) {
   switch (s.G) {
     case 1: launch_phi_q_g<T, D, 1>(s, q, omega, phiq, st); break;
@@ -2145,7 +2214,7 @@ thread_local int g_path_override = RADAR_PATH_AUTO;
 // SEL: the select path (uni_out / ucnt_out / umax receive the union)
 template <typename T, int D, int G, int N, bool SEL>
 radar_status launch_fused_n(const Shape& s, const void* q, const void* K,
-                            const void* V, const float* omega,
+                            const void* V, const void* omega,
                             const float* summ, const SeqArgs& sa, void* out,
                             int32_t* selected, float* sel_scores, int* uni_out,
                             int* ucnt_out, int umax, const AppendArgs& ap,
@@ -2156,7 +2225,7 @@ radar_status launch_fused_n(const Shape& s, const void* q, const void* K,
   launch(SEL ? RADAR_K_SELECT : RADAR_K_FUSED, k_decode_fused<T, D, G, N, SEL>,
          dim3((unsigned)(n_pairs * R)), dim3(kFusedWaves * 64), 0, st,
          reinterpret_cast<const T*>(q), reinterpret_cast<const T*>(K),
-         reinterpret_cast<const T*>(V), omega, summ, reinterpret_cast<T*>(out),
+         reinterpret_cast<const T*>(V), omega, s.obf, summ, reinterpret_cast<T*>(out),
          selected, sel_scores, s.Hq, s.Hkv, s.cap, s.s_cap, (int)ceil_div(s.c, kTile),
          sa, s.per_head, s1, s2, 1.f / std::sqrt((float)s.n),
          kLog2e / std::sqrt((float)s.d), uni_out, ucnt_out, umax, ap, R, n_pairs,
@@ -2166,7 +2235,7 @@ radar_status launch_fused_n(const Shape& s, const void* q, const void* K,
 
 #define RADAR_FUSED_ARGS s, q, K, V, omega, summ, sa, out, selected, sel_scores, uni_out, ucnt_out, umax, ap, R, part, maxwg, st
 #define RADAR_FUSED_PARAMS const Shape& s, const void* q, const void* K, const void* V, \
-    const float* omega, const float* summ, const SeqArgs& sa, void* out, int32_t* selected, \
+    const void* omega, const float* summ, const SeqArgs& sa, void* out, int32_t* selected, \
     float* sel_scores, int* uni_out, int* ucnt_out, int umax, const AppendArgs& ap, int R, \
     float* part, int maxwg, hipStream_t st
 
@@ -2192,7 +2261,7 @@ radar_status launch_fused_d(RADAR_FUSED_PARAMS) {
 // K and V start after the sinks. R workgroups per pair; with R > 1 their
 // partials go to the workspace and k_combine merges them.
 radar_status launch_fused(const Shape& s, const void* q, const void* K, const void* V,
-                          const float* omega, const float* summ, const SeqArgs& sa,
+                          const void* omega, const float* summ, const SeqArgs& sa,
                           void* out, int32_t* selected, float* sel_scores,
                           const AppendArgs& ap, int R, unsigned char* w,
                           const WsLayout& L, hipStream_t st) {
@@ -2221,7 +2290,7 @@ radar_status launch_fused(const Shape& s, const void* q, const void* K, const vo
 
 // the select path's first kernel: phi(q), scores, top-k and union of each
 // pair in one workgroup, the union into the workspace
-radar_status launch_select(const Shape& s, const void* q, const float* omega,
+radar_status launch_select(const Shape& s, const void* q, const void* omega,
                            const float* summ, const SeqArgs& sa, int32_t* selected,
                            float* sel_scores, unsigned char* w, const WsLayout& L,
                            const AppendArgs& ap, hipStream_t st) {
@@ -2305,7 +2374,7 @@ radar_status check_decode(const radar_config* cfg, Shape* s, int64_t t,
 // Pointer checks shared by radar_append and radar_append_decode.
 radar_status check_append(const radar_config* cfg, Shape* s, const void* K,
                           const void* V, const void* k_new, const void* v_new,
-                          const float* omega, const float* summaries,
+                          const void* omega, const float* summaries,
                           const int64_t* pos) {
   radar_status r = check_cfg(cfg, s);
   if (r != RADAR_OK) return r;
@@ -2326,7 +2395,7 @@ AppendArgs append_args(const Shape& s, void* K, void* V, const void* k_new,
 
 // The summary refresh of an append of row t (row pos[b] of sequence b): the
 // segment the row completes, if any, with the index build's own code.
-radar_status refresh_closed(const Shape& s, const void* K, const float* omega,
+radar_status refresh_closed(const Shape& s, const void* K, const void* omega,
                             float* summ, int64_t t, const int64_t* pos,
                             hipStream_t st) {
   const void* Kp = after_sinks(s, K);
@@ -2379,7 +2448,7 @@ radar_status plan_decode(const Shape& s, const WsLayout& L, const SeqArgs& sa,
 // that ap describes, before the attention reads them.
 radar_status run_decode(const Shape& s, const WsLayout& L, const SeqArgs& sa,
                         const DecodePlan& plan, const void* q, const void* K,
-                        const void* V, const float* omega, const float* summaries,
+                        const void* V, const void* omega, const float* summaries,
                         void* out, int32_t* selected, float* scores,
                         unsigned char* w, const AppendArgs& ap, hipStream_t stream) {
   const Span top = make_span(sa.t_max, sa);
@@ -2520,7 +2589,7 @@ size_t radar_decode_workspace_bytes(const radar_config* cfg, int32_t k) {
 }
 
 radar_status radar_build_index(const radar_config* cfg, const void* K,
-                               const float* omega, int64_t t, float* summaries,
+                               const void* omega, int64_t t, float* summaries,
                                hipStream_t stream) {
   Shape s;
   radar_status r = check_cfg(cfg, &s);
@@ -2536,7 +2605,7 @@ radar_status radar_build_index(const radar_config* cfg, const void* K,
 
 radar_status radar_append(const radar_config* cfg, void* K, void* V,
                           const void* k_new, const void* v_new,
-                          const float* omega, int64_t t, const int64_t* pos,
+                          const void* omega, int64_t t, const int64_t* pos,
                           float* summaries, hipStream_t stream) {
   Shape s;
   radar_status r = check_append(cfg, &s, K, V, k_new, v_new, omega, summaries, pos);
@@ -2551,7 +2620,7 @@ radar_status radar_append(const radar_config* cfg, void* K, void* V,
 }
 
 radar_status radar_decode(const radar_config* cfg, const void* q, const void* K,
-                          const void* V, const float* omega,
+                          const void* V, const void* omega,
                           const float* summaries, int64_t t, const int64_t* lens,
                           int32_t k, void* out, int32_t* selected, float* scores,
                           void* workspace, size_t workspace_bytes,
@@ -2575,7 +2644,7 @@ radar_status radar_decode(const radar_config* cfg, const void* q, const void* K,
 
 radar_status radar_append_decode(const radar_config* cfg, const void* q, void* K,
                                  void* V, const void* k_new, const void* v_new,
-                                 const float* omega, float* summaries, int64_t t,
+                                 const void* omega, float* summaries, int64_t t,
                                  const int64_t* pos, int32_t k, void* out,
                                  int32_t* selected, float* scores, void* workspace,
                                  size_t workspace_bytes, hipStream_t stream) {

@@ -94,11 +94,13 @@ class Episode:
     lens0 (one length <= t0 per sequence) makes the batch ragged: sequence b
     starts at length lens0[b] (its cache rows beyond are stale), appends at
     its own position and decodes at its own length. merged runs each step as
-    one radar_append_decode call instead of radar_append + radar_decode."""
+    one radar_append_decode call instead of radar_append + radar_decode.
+    omega_bf16 passes Omega to the library as bf16 (bf16 workloads, whose
+    Omega values are bf16 already; the oracle reads the same values)."""
 
     def __init__(self, wl, steps, groups=None, device="cuda",
                  path=radar.PATH_AUTO, n_sink=0, per_head=False, lens0=None,
-                 merged=False):
+                 merged=False, omega_bf16=False):
         self.wl = wl
         self.steps = steps
         self.path = path
@@ -107,6 +109,12 @@ class Episode:
         self.lens0 = list(lens0) if lens0 is not None else None
         self.inp = workloads.make_inputs(wl, device, steps=steps)
         self.cfg = config_of(wl, wl.t0 + steps, n_sink, per_head)
+        self.omega_dev = self.inp.omega
+        if omega_bf16:
+            assert wl.dtype == "bf16"
+            self.omega_dev = self.inp.omega.to(torch.bfloat16)
+            assert torch.equal(self.omega_dev.float(), self.inp.omega)
+            self.cfg = dataclasses.replace(self.cfg, omega_dtype=torch.bfloat16)
         B, Hkv = wl.batch, wl.n_kv_heads
         self.groups = groups if groups is not None else \
             [(b, g) for b in range(B) for g in range(Hkv)]
@@ -143,7 +151,7 @@ class Episode:
         dev = inp.K.device
         K, V = inp.K.clone(), inp.V.clone()
         summ = radar.new_summaries(cfg, dev)
-        radar.build_index(cfg, K, inp.omega, wl.t0, summ)
+        radar.build_index(cfg, K, self.omega_dev, wl.t0, summ)
         lens = [wl.t0] * wl.batch if self.lens0 is None else list(self.lens0)
         self.check_summaries(summ, lens)
         ws = radar.new_workspace(cfg, wl.top_k, dev)
@@ -159,16 +167,16 @@ class Episode:
                 torch.tensor(lens, dtype=torch.int64, device=dev)
             if self.merged:
                 lens = [x + 1 for x in lens]
-                radar.append_decode(cfg, q, K, V, kn, vn, inp.omega, summ,
+                radar.append_decode(cfg, q, K, V, kn, vn, self.omega_dev, summ,
                                     max(lens), wl.top_k, out=out, selected=sel,
                                     scores=sc, workspace=ws, pos=pos)
             else:
-                radar.append(cfg, K, V, kn, vn, inp.omega,
+                radar.append(cfg, K, V, kn, vn, self.omega_dev,
                              lens[0] if pos is None else 0, summ, pos=pos)
                 lens = [x + 1 for x in lens]
                 lens_dev = None if self.lens0 is None else \
                     torch.tensor(lens, dtype=torch.int64, device=dev)
-                radar.decode(cfg, q, K, V, inp.omega, summ, max(lens), wl.top_k,
+                radar.decode(cfg, q, K, V, self.omega_dev, summ, max(lens), wl.top_k,
                              out=out, selected=sel, scores=sc, workspace=ws,
                              lens=lens_dev)
             if check_steps is None or i in check_steps:

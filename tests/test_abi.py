@@ -39,10 +39,40 @@ def test_exports_every_declared_symbol(L):
 
 
 def test_version_and_strings(L):
-    assert L.radar_abi_version() == radar.ABI_VERSION == 3
+    assert L.radar_abi_version() == radar.ABI_VERSION == 4
     for st in range(6):
         assert L.radar_status_string(st).decode()
     assert L.radar_last_error() is not None
+
+
+def test_config_layout_matches_the_header(tmp_path):
+    """The binding's ctypes mirror of radar_config has the C compiler's size
+    and field offsets (a C program built from the header prints them)."""
+    import shutil
+    import subprocess
+    gcc = shutil.which("gcc")
+    if gcc is None:
+        pytest.skip("no C compiler")
+    src = tmp_path / "layout.c"
+    src.write_text(
+        "#include <stddef.h>\n#include <stdio.h>\n#include \"radar.h\"\n"
+        "int main(void) {\n"
+        "  printf(\"%zu\", sizeof(radar_config));\n"
+        + "".join(f"  printf(\" %zu\", offsetof(radar_config, {f}));\n"
+                  for f, _ in radar._Config._fields_)
+        + "  return 0;\n}\n")
+    exe = tmp_path / "layout"
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    r = subprocess.run([gcc, "-D__HIP_PLATFORM_AMD__", "-I", os.path.join(ROOT, "include"),
+                        "-I", os.path.join(rocm, "include"), str(src), "-o", str(exe)],
+                       capture_output=True, text=True)
+    if r.returncode != 0:
+        pytest.skip("header does not compile here: " + r.stderr[-300:])
+    got = [int(v) for v in subprocess.run([str(exe)], capture_output=True,
+                                          text=True, check=True).stdout.split()]
+    want = [ctypes.sizeof(radar._Config)] + [getattr(radar._Config, f).offset
+                                             for f, _ in radar._Config._fields_]
+    assert got == want
 
 
 def _cfg(**kw):
@@ -66,6 +96,10 @@ def test_workspace_bytes(L):
     assert radar.workspace_bytes(_cfg(head_dim=96), 16) == 0
     assert radar.workspace_bytes(_cfg(n_features=100), 16) == 0
     assert radar.workspace_bytes(_cfg(dtype=torch.float32), 16) > 0
+    # a bf16 Omega with a bf16 cache; refused with an fp32 cache
+    assert radar.workspace_bytes(_cfg(omega_dtype=torch.bfloat16), 16) == n16
+    assert radar.workspace_bytes(_cfg(dtype=torch.float32,
+                                      omega_dtype=torch.bfloat16), 16) == 0
 
 
 def _P(v):
@@ -115,6 +149,17 @@ def test_validation_before_launch(L):
                 _cfg(n_sink=131585), _cfg(gqa_mode=2)):
         assert L.radar_build_index(by(bad.c_struct()), good, good, 1, good,
                                    None) == 1
+    # Omega element type: fp32 or bf16, bf16 only with a bf16 cache
+    import torch
+    for bad_omega in (2, -1):
+        c = _cfg().c_struct()
+        c.omega_dtype = bad_omega
+        assert L.radar_build_index(by(c), good, good, 1, good, None) == 1
+        assert L.radar_decode_workspace_bytes(by(c), 16) == 0
+    c = _cfg(dtype=torch.float32, omega_dtype=torch.bfloat16).c_struct()
+    assert L.radar_build_index(by(c), good, good, 1, good, None) == 1
+    assert L.radar_append(by(c), good, good, good, good, good, 5, null, good,
+                          None) == 1
     for bad in (_cfg(head_dim=256), _cfg(n_features=1024),
                 _cfg(n_q_heads=96, n_kv_heads=32), _cfg(capacity=1 << 31),
                 _cfg(batch=2048, n_q_heads=32, n_kv_heads=32)):

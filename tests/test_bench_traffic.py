@@ -17,7 +17,7 @@ import workloads  # noqa: E402
 def _line(rec, **over):
     run = dict(rec["run"], **over)
     return {"steps": run["steps"], "warmup": run["warmup"],
-            "config": {k: run[k] for k in ("decode_path", "schedule", "calls", "selector")}}
+            "config": {k: v for k, v in run.items() if k not in ("steps", "warmup")}}
 
 
 def _records():
@@ -36,6 +36,7 @@ def test_records_are_for_the_default_runs():
         assert run["steps"] == wl.steps and run["warmup"] == 16, rec["workload"]
         assert run["schedule"] == "fixed" and run["selector"] == "radar"
         assert run["calls"] == "radar_append_decode"
+        assert run["omega"] == ("bf16" if wl.dtype == "bf16" else "f32")
 
 
 def test_traffic_only_for_the_same_run():
@@ -53,5 +54,6 @@ def test_traffic_only_for_the_same_run():
         assert bench.measured_traffic(k, w, _line(rec, warmup=0)) is None
         assert bench.measured_traffic(k, w, _line(rec, calls="radar_append + radar_decode")) is None
         assert bench.measured_traffic(k, w, _line(rec, schedule="sqrt")) is None
+        assert bench.measured_traffic(k, w, _line(rec, omega="other")) is None
     assert bench.measured_traffic("k_decode_fused", "no_such_workload",
                                   {"steps": 1, "warmup": 0, "config": {}}) is None
