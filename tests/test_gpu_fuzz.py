@@ -55,6 +55,7 @@ def draw(seed):
     path = int(rng.choice(PATHS))
     # drawn last, so the earlier draws of a seed stay what they were
     opt["merged"] = bool(rng.random() < 0.5)
+    opt["omega_bf16"] = bool(wl.dtype == "bf16" and rng.random() < 0.5)
     return wl, opt, path
 
 

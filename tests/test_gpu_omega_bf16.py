@@ -106,6 +106,19 @@ def test_oracle_parity_bf16_omega(path):
     assert st.heads > 0
 
 
+@PATHS
+def test_oracle_parity_bf16_omega_with_options(path):
+    """bf16 Omega together with attention sinks, per-head GQA masks and a
+    ragged batch (each sequence at its own length, appending at its own
+    position)."""
+    wl = _workloads()["g4"].scaled(name="ob_opts", batch=3)
+    print(f"[case] omega bf16 + sinks + per-head + ragged: {wl.name} path={path}",
+          flush=True)
+    st = H.Episode(wl, 24, path=path, omega_bf16=True, n_sink=3, per_head=True,
+                   lens0=[wl.t0, 1200, 40]).run()
+    assert st.heads > 0
+
+
 def test_binding_refuses_mismatched_omega():
     wl = _workloads()["g1"]
     cfg = H.config_of(wl, wl.t0 + 1)
