@@ -309,7 +309,7 @@ def main():
     ap.add_argument("--cpu-heads", type=int, default=8)
     ap.add_argument("--calibrate-copy", type=int, default=1,
                     help="also run a plain 1 GiB read+write elementwise "
-                         "kernel: the box's copy bandwidth (and the counter "
+                         "kernel: this GPU's copy bandwidth (and the counter "
                          "calibration for HBM traffic)")
     ap.add_argument("--merged", type=int, default=1,
                     help="1: one radar_append_decode call per step (the row "
