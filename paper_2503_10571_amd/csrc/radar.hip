@@ -1390,9 +1390,12 @@ __global__ __launch_bounds__(256) void k_attend(
 // output; with fewer pairs R workgroups share a pair's attention tiles and
 // each writes a partial that k_combine merges (the repeated summary reads
 // mostly hit the caches). Phases:
-//   1. phi(q) of the group's G heads into LDS (16 lanes per Omega row);
-//   2. Eq. 6 scores of all candidates into LDS (32 summary rows per wave
-//      per pass, streaming loads);
+//   1. phi(q) of the group's G heads into LDS (16 lanes per Omega row;
+//      Omega in fp32 or bf16, obf), with each wave's first summary rows
+//      already in flight (waves whose first row is past the candidates
+//      load none);
+//   2. Eq. 6 scores of all candidates into LDS (16 or 32 summary rows per
+//      wave per pass, streaming loads);
 //   3. waves < G take the top-k of one head each, while the other waves
 //      already attend the window tiles (the window never depends on the
 //      selection);
