@@ -38,6 +38,7 @@ import workloads  # noqa: E402
 
 METRIC = ("decode attention tokens/sec (all heads) + achieved HBM GB/s at "
           "128K context")
+HOST_LINK_PEAK_GBPS = 63.0      # PCIe 5.0 x16, one direction
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
 BF16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak
 
@@ -165,10 +166,13 @@ def run_signature(line):
     """What fixes the bytes per launch of a run besides the workload: the
     step range (the context grows by one row a step) and the call form."""
     cfg = line["config"]
-    return {"steps": line["steps"], "warmup": line["warmup"],
-            "decode_path": cfg["decode_path"], "schedule": cfg["schedule"],
-            "calls": cfg["calls"], "selector": cfg["selector"],
-            "omega": cfg["omega"]}
+    sig = {"steps": line["steps"], "warmup": line["warmup"],
+           "decode_path": cfg["decode_path"], "schedule": cfg["schedule"],
+           "calls": cfg["calls"], "selector": cfg["selector"],
+           "omega": cfg["omega"]}
+    if cfg.get("kv", "device") != "device":
+        sig["kv"] = cfg["kv"]
+    return sig
 
 
 def measured_traffic(kernel, workload, line):
@@ -344,6 +348,10 @@ def main():
                     help="instead of timing: recall of Radar's selection "
                          "against the exact search over n and k, one JSON "
                          "line per (n, k)")
+    ap.add_argument("--kv-host", type=int, default=0,
+                    help="1: the K/V cache in pinned host memory mapped for "
+                         "the GPU; the decode gathers the selected segments "
+                         "over the host link (reported as host_link)")
     ap.add_argument("--omega", default="auto", choices=["auto", "f32"],
                     help="auto: Omega passed as bf16 for bf16 caches (their "
                          "projection rounds it to bf16 anyway; same results, "
@@ -388,16 +396,26 @@ def main():
     s_kv = 2 if wl.dtype == "bf16" else 4
     s_om = omega.element_size()
     K, V = inp.K, inp.V
-    summ = radar.new_summaries(cfg, K.device)
+    gpu = inp.K.device
+    if args.kv_host:
+        # the K/V cache in pinned host memory mapped for the GPU: the decode
+        # reads only the selected segments, the window and the sinks over
+        # the host link (the summaries, Omega and the workspace stay on the
+        # GPU)
+        K = torch.empty(inp.K.shape, dtype=inp.K.dtype, pin_memory=True)
+        V = torch.empty(inp.V.shape, dtype=inp.V.dtype, pin_memory=True)
+        K.copy_(inp.K)
+        V.copy_(inp.V)
+    summ = radar.new_summaries(cfg, gpu)
     if args.schedule == "sqrt":
         # the largest scratch any step of the run needs (window up to 2c)
         need = max(radar.workspace_bytes(
             dataclasses.replace(cfg, seg_len=radar.schedule_sqrt(t)[0],
                                 window=radar.schedule_sqrt(t)[1]), wl.top_k)
             for t in range(wl.t0, wl.t0 + total + 1))
-        ws = torch.empty(need, dtype=torch.uint8, device=K.device)
+        ws = torch.empty(need, dtype=torch.uint8, device=gpu)
     else:
-        ws = radar.new_workspace(cfg, wl.top_k, K.device)
+        ws = radar.new_workspace(cfg, wl.top_k, gpu)
     out = torch.empty_like(inp.q[0])
     torch.cuda.synchronize()
 
@@ -426,7 +444,7 @@ def main():
                   sqrt_schedule=args.schedule == "sqrt", exact=exact,
                   merged=merged)
     sel_log = torch.empty(Ksteps, wl.batch, wl.n_q_heads, wl.top_k,
-                          dtype=torch.int32, device=K.device)
+                          dtype=torch.int32, device=gpu)
     log(f"[bench] warmup {W} steps")
     for i in range(W):
         stp.step(i)
@@ -543,7 +561,7 @@ def main():
     copy_gbps = None
     if args.calibrate_copy:
         # torch.neg over 1 GiB fp32: reads 1 GiB, writes 1 GiB
-        x = torch.ones(1 << 28, dtype=torch.float32, device=K.device)
+        x = torch.ones(1 << 28, dtype=torch.float32, device=gpu)
         y = torch.empty_like(x)
         torch.neg(x, out=y)
         torch.cuda.synchronize()
@@ -590,6 +608,7 @@ def main():
                       else "radar_append + radar_decode"),
             "selector": args.selector,
             "omega": "bf16" if s_om == 2 else "f32",
+            "kv": "pinned host memory" if args.kv_host else "device",
             "restructures": restructures,
         },
         "hbm_GBps": round(step_gbps, 1),
@@ -622,6 +641,16 @@ def main():
         "cpu_baseline": cpu,
     }
     line["roofline"]["traffic"] = measured_traffic(dom_name, wl.name, line)
+    if args.kv_host:
+        # the K/V rows each step gathers (selected segments, window, sinks)
+        # cross the host link; its reference rate is PCIe 5.0 x16, one way
+        kv_step = kv_bytes / Ksteps
+        line["host_link"] = {
+            "kv_bytes_per_step": int(kv_step),
+            "achieved": round(kv_step / (ms_step * 1e-3) / 1e9, 2),
+            "peak": HOST_LINK_PEAK_GBPS, "unit": "GB/s",
+            "frac": round(kv_step / (ms_step * 1e-3) / 1e9 / HOST_LINK_PEAK_GBPS, 4),
+        }
     if copy_gbps is not None:
         line["copy_GBps"] = round(copy_gbps, 1)
         line["roofline"]["frac_of_copy"] = round(dom_gbps / copy_gbps, 4)

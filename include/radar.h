@@ -14,7 +14,13 @@
  * Conventions shared by every call
  * --------------------------------
  *  - Every tensor argument is a DEVICE pointer owned by the caller; `cfg` is a
- *    host pointer. The library allocates no device memory, keeps no device
+ *    host pointer. K and V may instead point to pinned host memory mapped
+ *    into the device's address space at the same address (hipHostMalloc);
+ *    the kernels then read over the host link only the rows a call needs
+ *    (a decode: the selected segments, the window and the sinks; an append:
+ *    the closed segment it summarises; an index build: every key), and write
+ *    appended rows there. Summaries, Omega, q and the outputs stay in device
+ *    memory. The library allocates no device memory, keeps no device
  *    state between calls, never synchronises, and launches only on `stream`
  *    (the path override and the profiling switch are host-side settings of
  *    the calling thread).

@@ -149,13 +149,38 @@ def _check(fn, st):
         raise RadarError(fn, st, detail)
 
 
-def _need(x, dtype, name, numel=None, at_least=False):
+class _PtrAttr(ctypes.Structure):
+    # hipPointerAttribute_t
+    _fields_ = [("type", ctypes.c_int), ("device", ctypes.c_int),
+                ("devicePointer", ctypes.c_void_p), ("hostPointer", ctypes.c_void_p),
+                ("isManaged", ctypes.c_int), ("allocationFlags", ctypes.c_uint)]
+
+
+_hip_rt = None
+
+
+def _device_mapped(x) -> bool:
+    """A pinned host tensor whose pages the GPU reaches at the same address
+    (hipHostMalloc memory, as torch's pin_memory=True allocates it)."""
+    global _hip_rt
+    if not x.is_pinned():
+        return False
+    if _hip_rt is None:
+        _hip_rt = ctypes.CDLL("libamdhip64.so")
+    a = _PtrAttr()
+    st = _hip_rt.hipPointerGetAttributes(ctypes.byref(a), ctypes.c_void_p(x.data_ptr()))
+    return st == 0 and a.devicePointer == x.data_ptr()
+
+
+def _need(x, dtype, name, numel=None, at_least=False, host_ok=False):
     """Device, dtype and layout checks; numel: the element count the kernels
     address for this argument (exactly, or at least with at_least), so that
     a tensor of the wrong size is refused before any kernel reads or writes
-    past its end."""
-    if not x.is_cuda:
-        raise ValueError(f"{name} must be a device tensor")
+    past its end. host_ok also accepts pinned host memory mapped for the
+    device (the K/V cache only)."""
+    if not x.is_cuda and not (host_ok and _device_mapped(x)):
+        raise ValueError(f"{name} must be a device tensor" +
+                         (" or pinned host memory mapped for the device" if host_ok else ""))
     if x.dtype != dtype:
         raise ValueError(f"{name} must be {dtype}, got {x.dtype}")
     if not x.is_contiguous():
@@ -166,10 +191,13 @@ def _need(x, dtype, name, numel=None, at_least=False):
 
 
 def _cache(cfg, K, V=None):
+    """K and V may sit in device memory or in pinned, device-mapped host
+    memory (the decode then reads only the selected segments' rows, and the
+    window's, over the host link)."""
     n = cfg.batch * cfg.n_kv_heads * cfg.capacity * cfg.head_dim
-    _need(K, cfg.dtype, "K", n)
+    _need(K, cfg.dtype, "K", n, host_ok=True)
     if V is not None:
-        _need(V, cfg.dtype, "V", n)
+        _need(V, cfg.dtype, "V", n, host_ok=True)
 
 
 def _rows(cfg, k_new, v_new):
@@ -213,7 +241,7 @@ def build_index(cfg: Config, K, omega, t: int, summaries) -> None:
     _cache(cfg, K); _omega(cfg, omega); _summ(cfg, summaries)
     _check("radar_build_index", lib().radar_build_index(
         ctypes.byref(cfg.c_struct()), _ptr(K), _ptr(omega), t, _ptr(summaries),
-        _stream(K)))
+        _stream(summaries)))
 
 
 def _lens(x, cfg: Config, name):
@@ -235,7 +263,7 @@ def append(cfg: Config, K, V, k_new, v_new, omega, t: int, summaries,
     pos = _lens(pos, cfg, "pos")
     _check("radar_append", lib().radar_append(
         ctypes.byref(cfg.c_struct()), _ptr(K), _ptr(V), _ptr(k_new), _ptr(v_new),
-        _ptr(omega), t, _ptr(pos), _ptr(summaries), _stream(K)))
+        _ptr(omega), t, _ptr(pos), _ptr(summaries), _stream(summaries)))
 
 
 def _outputs(cfg, q, k, out, selected, scores, workspace):
@@ -400,6 +428,14 @@ class RadarLayer:
         if schedule not in ("fixed", "sqrt"):
             raise ValueError(schedule)
         self.cfg, self.k, self.schedule = cfg, top_k, schedule
+        # summaries and workspace live on the GPU; K and V may be given in
+        # pinned, device-mapped host memory
+        if K is None:
+            self.device = torch.device(device)
+        elif K.is_cuda:
+            self.device = K.device
+        else:
+            self.device = torch.device("cuda")
         shape = (cfg.batch, cfg.n_kv_heads, cfg.capacity, cfg.head_dim)
         self.K = K if K is not None else torch.zeros(shape, dtype=cfg.dtype, device=device)
         self.V = V if V is not None else torch.zeros(shape, dtype=cfg.dtype, device=device)
@@ -410,11 +446,11 @@ class RadarLayer:
             rows = cfg.capacity // c0              # the smallest c comes first
             self.summaries = torch.zeros(cfg.batch, cfg.n_kv_heads, rows,
                                          cfg.n_features, dtype=torch.float32,
-                                         device=self.K.device)
+                                         device=self.device)
             self.cfg = self._cfg_at(max(t, 1))
         else:
-            self.summaries = new_summaries(cfg, self.K.device)
-        self.workspace = new_workspace(self.cfg, top_k, self.K.device)
+            self.summaries = new_summaries(cfg, self.device)
+        self.workspace = new_workspace(self.cfg, top_k, self.device)
         self.restructures = 0
         if t > 0:
             build_index(self.cfg, self.K, omega, t, self.summaries)
@@ -460,4 +496,4 @@ class RadarLayer:
         # the scratch size follows the window, which grows between
         # restructures under the sqrt schedule
         if workspace_bytes(self.cfg, self.k) > self.workspace.numel():
-            self.workspace = new_workspace(self.cfg, self.k, self.K.device)
+            self.workspace = new_workspace(self.cfg, self.k, self.device)

@@ -1,0 +1,101 @@
+"""The K/V cache in pinned host memory mapped for the device (the offloading
+idea of the paper's memory-efficient variant): the summaries, Omega and the
+workspace stay on the GPU, so the selection reads them there, and the
+attention gathers only the selected segments, the window and the sinks over
+the host link; appends write their rows there. The kernels are the same, so
+every output, selection, score, summary and cache row must equal the
+device-resident run bit for bit, on every decode path and both call forms."""
+import dataclasses
+import os
+import sys
+
+import pytest
+import torch
+
+sys.path.insert(0, os.path.dirname(__file__))
+import _harness as H  # noqa: E402
+
+import paper_2503_10571_amd as radar  # noqa: E402
+import workloads  # noqa: E402
+from workloads import WORKLOADS  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+PATHS = pytest.mark.parametrize("path", [radar.PATH_SPLIT, radar.PATH_FUSED,
+                                         radar.PATH_SELECT],
+                                ids=["split", "fused", "select"])
+
+
+def _bits(x):
+    return x.view(torch.int16 if x.element_size() == 2 else torch.int32)
+
+
+def _pinned(x):
+    t = torch.empty(x.shape, dtype=x.dtype, pin_memory=True)
+    t.copy_(x)
+    return t
+
+
+def _episode(wl, cfg, omega, inp, K, V, steps, merged):
+    summ = radar.new_summaries(cfg, "cuda")
+    radar.build_index(cfg, K, omega, wl.t0, summ)
+    ws = radar.new_workspace(cfg, wl.top_k, "cuda")
+    outs, sels, scs = [], [], []
+    t = wl.t0
+    for i in range(steps):
+        q = inp.q[i].contiguous()
+        kn, vn = inp.k_new[i].contiguous(), inp.v_new[i].contiguous()
+        out = torch.empty_like(q)
+        sel = torch.empty(wl.batch, wl.n_q_heads, wl.top_k, dtype=torch.int32, device="cuda")
+        sc = torch.empty(wl.batch, wl.n_q_heads, wl.top_k, dtype=torch.float32, device="cuda")
+        if merged:
+            t += 1
+            radar.append_decode(cfg, q, K, V, kn, vn, omega, summ, t, wl.top_k, out=out,
+                                selected=sel, scores=sc, workspace=ws)
+        else:
+            radar.append(cfg, K, V, kn, vn, omega, t, summ)
+            t += 1
+            radar.decode(cfg, q, K, V, omega, summ, t, wl.top_k, out=out, selected=sel,
+                         scores=sc, workspace=ws)
+        outs.append(out)
+        sels.append(sel)
+        scs.append(sc)
+    torch.cuda.synchronize()
+    return [summ, torch.stack(outs), torch.stack(sels), torch.stack(scs),
+            K.cpu() if K.is_cuda else K.clone(), V.cpu() if V.is_cuda else V.clone()]
+
+
+@PATHS
+@pytest.mark.parametrize("merged", [False, True], ids=["separate", "merged"])
+def test_host_cache_equals_device_cache(merged, path):
+    # G = 4, two sequences; a segment closes at t = 4352 (step 21 of 24)
+    wl = WORKLOADS["gqa_64k"].scaled(name="kvhost_g4", batch=2, n_q_heads=8,
+                                     n_kv_heads=2, t0=4331)
+    steps = 24
+    print(f"[case] K/V in pinned host memory: {wl.name} path={path} merged={merged}",
+          flush=True)
+    inp = workloads.make_inputs(wl, "cuda", steps=steps)
+    omega = inp.omega.to(torch.bfloat16)
+    cfg = dataclasses.replace(H.config_of(wl, wl.t0 + steps), omega_dtype=torch.bfloat16)
+    radar.set_decode_path(path)
+    try:
+        dev = _episode(wl, cfg, omega, inp, inp.K.clone(), inp.V.clone(), steps, merged)
+        Kh, Vh = _pinned(inp.K), _pinned(inp.V)
+        assert not Kh.is_cuda and Kh.is_pinned()
+        host = _episode(wl, cfg, omega, inp, Kh, Vh, steps, merged)
+    finally:
+        radar.set_decode_path(radar.PATH_AUTO)
+    for a, b, what in zip(dev, host, ("summaries", "outputs", "selected", "scores", "K", "V")):
+        assert torch.equal(_bits(a.cpu()), _bits(b.cpu())), what
+
+
+def test_binding_refuses_unpinned_host_cache():
+    wl = WORKLOADS["tiny"].scaled(name="kvhost_refuse", t0=300, steps=1)
+    cfg = H.config_of(wl, wl.t0 + 1)
+    inp = workloads.make_inputs(wl, "cuda", steps=1)
+    summ = radar.new_summaries(cfg, "cuda")
+    with pytest.raises(ValueError):
+        radar.build_index(cfg, inp.K.cpu(), inp.omega, wl.t0, summ)
+    with pytest.raises(ValueError):
+        radar.decode(cfg, inp.q[0].contiguous(), inp.K.cpu(), inp.V.cpu(), inp.omega,
+                     summ, wl.t0, wl.top_k)
