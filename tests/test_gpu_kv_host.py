@@ -99,3 +99,29 @@ def test_binding_refuses_unpinned_host_cache():
     with pytest.raises(ValueError):
         radar.decode(cfg, inp.q[0].contiguous(), inp.K.cpu(), inp.V.cpu(), inp.omega,
                      summ, wl.t0, wl.top_k)
+
+
+@pytest.mark.parametrize("schedule", ["fixed", "sqrt"])
+def test_layer_with_host_cache(schedule):
+    """RadarLayer over a cache in pinned host memory keeps its summaries and
+    workspace on the GPU and steps exactly like the device-resident layer
+    (with the sqrt schedule, a restructure falls inside the steps)."""
+    wl = WORKLOADS["llama2_16k"].scaled(name="kvhost_layer", n_q_heads=4, n_kv_heads=4,
+                                        t0=2020)
+    steps = 30                                # 2025 = 45^2: a restructure at step 4
+    print(f"[case] RadarLayer on a host cache: schedule={schedule}", flush=True)
+    inp = workloads.make_inputs(wl, "cuda", steps=steps)
+    omega = inp.omega.to(torch.bfloat16)
+    cfg = dataclasses.replace(H.config_of(wl, wl.t0 + steps), omega_dtype=torch.bfloat16)
+    layers = [radar.RadarLayer(cfg, omega, K=inp.K.clone(), V=inp.V.clone(), t=wl.t0,
+                               top_k=wl.top_k, schedule=schedule),
+              radar.RadarLayer(cfg, omega, K=_pinned(inp.K), V=_pinned(inp.V), t=wl.t0,
+                               top_k=wl.top_k, schedule=schedule)]
+    assert layers[1].summaries.is_cuda and layers[1].workspace.is_cuda
+    assert not layers[1].K.is_cuda
+    for i in range(steps):
+        outs = [L.step(inp.q[i].contiguous(), inp.k_new[i].contiguous(),
+                       inp.v_new[i].contiguous()) for L in layers]
+        torch.cuda.synchronize()
+        assert torch.equal(_bits(outs[0]), _bits(outs[1])), i
+    assert torch.equal(_bits(layers[0].summaries), _bits(layers[1].summaries))
