@@ -282,7 +282,7 @@ def cpu_baseline(wl, inp, first_step, n_steps, n_heads, min_s=10.0,
 
 def recall_sweep(wl):
     """Recall of Radar's selection against the exact segment search at the
-    workload's context length, for n in 64..512 and k in 1..64, over the
+    workload's context length, for n in 64..2048 and k in 1..64, over the
     first decode query of the workload's inputs."""
     from paper_2503_10571_amd import recall
     log(f"[recall] generating {wl.name} inputs")
@@ -292,7 +292,7 @@ def recall_sweep(wl):
                        wl.torch_dtype())
     omegas = {n: workloads.make_omega(n, wl.head_dim, seed=1000 + n,
                                       dtype=wl.dtype, device="cuda")
-              for n in (64, 128, 256, 512)}
+              for n in (64, 128, 256, 512, 1024, 2048)}
     ks = [1, 2, 4, 8, 16, 32, 64]
     rows = recall.sweep(cfg, inp.q[0].contiguous(), inp.K, inp.V, wl.t0,
                         omegas, ks)

@@ -933,11 +933,12 @@ __device__ void group_union(const int* sel, unsigned* bits, int G, int per,
 // ---------------------------------------------------------------------------
 // Workgroup = 1, 2 or 4 waves x (16 * RB) summary rows of one (b, kv head)
 // (fewer waves per workgroup when that spreads a small call over more CUs;
-// the waves are independent). Lane l
-// holds features [l*FPL, (l+1)*FPL) of phi(q) for the G heads of the group,
-// so each summary row is one contiguous n*4-byte wave load; all of a wave's
-// rows are loaded before any is reduced. A 16-row batch is transpose-reduced
-// inside each 16-lane row with DPP, then summed over the four rows.
+// the waves are independent). Lane l holds FPL = n / 64 features of phi(q)
+// for the G heads of the group, in chunks of at most 8 (n = 1024 and 2048
+// take 2 and 4 chunks, so the rows of a batch fit in registers); each chunk
+// of a row is one contiguous wave load, and all of a batch's rows are loaded
+// before any is reduced. A 16-row batch is transpose-reduced inside each
+// 16-lane row with DPP, then summed over the four rows.
 template <int N, int G>
 __global__ __launch_bounds__(256) void k_score(const float* __restrict__ phiq,
                                                const float* __restrict__ summ,
@@ -945,6 +946,10 @@ __global__ __launch_bounds__(256) void k_score(const float* __restrict__ phiq,
                                                int Hq, int Hkv, SeqArgs sa,
                                                int64_t s_cap, int nc_cap) {
   constexpr int FPL = N / 64;
+  // features per lane per chunk: all of them up to n = 512; above, 8 (4
+  // for G >= 4, whose accumulators take more registers)
+  constexpr int FC = FPL <= 8 ? FPL : (G >= 4 ? 4 : 8);
+  constexpr int NCH = FPL / FC;            // chunks (1 for n <= 512)
   constexpr int RB = N <= 256 ? 2 : 1;     // 16-row batches per wave
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -954,50 +959,67 @@ __global__ __launch_bounds__(256) void k_score(const float* __restrict__ phiq,
   const int wrow0 = (blockIdx.x * (blockDim.x >> 6) + wave) * (16 * RB);
   if (wrow0 >= n_cand) return;             // wave-uniform; no barriers below
 
-  float pq[G][FPL];
-#pragma unroll
-  for (int g = 0; g < G; ++g) {
-    const float* src = phiq + ((b * Hq + hk * G + g) * N) + lane * FPL;
-#pragma unroll
-    for (int e = 0; e < FPL; ++e) pq[g][e] = src[e];
-  }
-  const float* base = summ + (bh * s_cap) * N + lane * FPL;
-  float x[RB][16][FPL];
+  // chunk ch holds features ch * 64 * FC + lane * FC + e (e < FC) of lane
+  // `lane`, so each chunk of a row is one contiguous 64 * FC * 4-byte wave
+  // load; with one chunk (n <= 512) lane l holds features l * FPL .. + FPL
+  const float* base = summ + (bh * s_cap) * N + lane * FC;
+  // per row and head a running dot product over the chunks
+  float part[RB][G][16];
 #pragma unroll
   for (int bt = 0; bt < RB; ++bt)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int row = min(wrow0 + bt * 16 + r, n_cand - 1);
-      const float* src = base + (int64_t)row * N;
-      if constexpr (FPL % 4 == 0) {
+    for (int g = 0; g < G; ++g)
 #pragma unroll
-        for (int e = 0; e < FPL; e += 4) {
-          const float4 v = ld_stream_f4(src + e);
-          x[bt][r][e] = v.x; x[bt][r][e + 1] = v.y;
-          x[bt][r][e + 2] = v.z; x[bt][r][e + 3] = v.w;
-        }
-      } else if constexpr (FPL == 2) {
-        const float2 v = *reinterpret_cast<const float2*>(src);
-        x[bt][r][0] = v.x; x[bt][r][1] = v.y;
-      } else {
-        x[bt][r][0] = src[0];
-      }
+      for (int r = 0; r < 16; ++r) part[bt][g][r] = 0.f;
+#pragma unroll 1
+  for (int ch = 0; ch < NCH; ++ch) {     // one chunk's rows live at a time
+    float pq[G][FC];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const float* src = phiq + ((b * Hq + hk * G + g) * N) + ch * 64 * FC + lane * FC;
+#pragma unroll
+      for (int e = 0; e < FC; ++e) pq[g][e] = src[e];
     }
+    float x[RB][16][FC];
+#pragma unroll
+    for (int bt = 0; bt < RB; ++bt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = min(wrow0 + bt * 16 + r, n_cand - 1);
+        const float* src = base + (int64_t)row * N + ch * 64 * FC;
+        if constexpr (FC % 4 == 0) {
+#pragma unroll
+          for (int e = 0; e < FC; e += 4) {
+            const float4 v = ld_stream_f4(src + e);
+            x[bt][r][e] = v.x; x[bt][r][e + 1] = v.y;
+            x[bt][r][e + 2] = v.z; x[bt][r][e + 3] = v.w;
+          }
+        } else if constexpr (FC == 2) {
+          const float2 v = *reinterpret_cast<const float2*>(src);
+          x[bt][r][0] = v.x; x[bt][r][1] = v.y;
+        } else {
+          x[bt][r][0] = src[0];
+        }
+      }
+#pragma unroll
+    for (int bt = 0; bt < RB; ++bt)
+#pragma unroll
+      for (int g = 0; g < G; ++g)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          float a = part[bt][g][r];
+#pragma unroll
+          for (int e = 0; e < FC; ++e) a = fmaf(x[bt][r][e], pq[g][e], a);
+          part[bt][g][r] = a;
+        }
+  }
 #pragma unroll
   for (int bt = 0; bt < RB; ++bt) {
     const int row = wrow0 + bt * 16 + (lane & 15);
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      float part[16];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float a = 0.f;
-#pragma unroll
-        for (int e = 0; e < FPL; ++e) a = fmaf(x[bt][r][e], pq[g][e], a);
-        part[r] = a;
-      }
-      transpose_reduce<16>(part, lane);
-      float v = part[0];
+      transpose_reduce<16>(part[bt][g], lane);
+      float v = part[bt][g][0];
       v += __shfl_xor(v, 16);
       v += __shfl_xor(v, 32);
       if (lane < 16 && row < n_cand)
@@ -1906,7 +1928,8 @@ radar_status check_cfg(const radar_config* cfg, Shape* s) {
   if (G != 1 && G != 2 && G != 4 && G != 8) return RADAR_EUNSUPPORTED;
   if (cfg->head_dim != 64 && cfg->head_dim != 128) return RADAR_EUNSUPPORTED;
   const int n = cfg->n_features;
-  if (n != 64 && n != 128 && n != 256 && n != 512) return RADAR_EUNSUPPORTED;
+  if (n != 64 && n != 128 && n != 256 && n != 512 && n != 1024 && n != 2048)
+    return RADAR_EUNSUPPORTED;
   // row counts fit int32; (b, kv head) pairs fit a grid's y dimension
   if (cfg->capacity > INT32_MAX) return RADAR_EUNSUPPORTED;
   if ((int64_t)cfg->batch * cfg->n_kv_heads > 65535) return RADAR_EUNSUPPORTED;
@@ -2098,7 +2121,9 @@ void launch_score(const Shape& s, const float* phiq, const float* summ,
     case 64: launch_score_n<64>(s, phiq, summ, scores, n_cand, sa, st); break;
     case 128: launch_score_n<128>(s, phiq, summ, scores, n_cand, sa, st); break;
     case 256: launch_score_n<256>(s, phiq, summ, scores, n_cand, sa, st); break;
-    default: launch_score_n<512>(s, phiq, summ, scores, n_cand, sa, st); break;
+    case 512: launch_score_n<512>(s, phiq, summ, scores, n_cand, sa, st); break;
+    case 1024: launch_score_n<1024>(s, phiq, summ, scores, n_cand, sa, st); break;
+    default: launch_score_n<2048>(s, phiq, summ, scores, n_cand, sa, st); break;
   }
 }
 
@@ -2249,7 +2274,8 @@ radar_status launch_fused_g(RADAR_FUSED_PARAMS) {
     case 64: return launch_fused_n<T, D, G, 64, SEL>(RADAR_FUSED_ARGS);
     case 128: return launch_fused_n<T, D, G, 128, SEL>(RADAR_FUSED_ARGS);
     case 256: return launch_fused_n<T, D, G, 256, SEL>(RADAR_FUSED_ARGS);
-    default: return launch_fused_n<T, D, G, 512, SEL>(RADAR_FUSED_ARGS);
+    case 512: return launch_fused_n<T, D, G, 512, SEL>(RADAR_FUSED_ARGS);
+    default: return RADAR_EUNSUPPORTED;    // n > 512 takes the split path
   }
 }
 
@@ -2341,7 +2367,9 @@ int64_t pair_bytes(const Shape& s, const SeqArgs& sa) {
 //  - split: phi(q), scores and top-k as separate chip-wide kernels.
 int choose_path(const Shape& s, const SeqArgs& sa) {
   const int n_cand = make_span(sa.t_max, sa).n_cand;
-  const bool fits_select = s.G <= kFusedMaxG && n_cand <= kFusedMaxCand;
+  // the fused and select kernels hold a lane's n / 64 features of every
+  // summary row of a batch in registers: n <= 512
+  const bool fits_select = s.G <= kFusedMaxG && n_cand <= kFusedMaxCand && s.n <= 512;
   const bool fits_fused = fits_select && !(s.dt == RADAR_F32 && s.d == 128);
   switch (g_path_override) {
     case RADAR_PATH_SPLIT: return RADAR_PATH_SPLIT;

@@ -95,6 +95,7 @@ def test_workspace_bytes(L):
     assert radar.workspace_bytes(_cfg(n_q_heads=24, n_kv_heads=8), 16) == 0  # G=3
     assert radar.workspace_bytes(_cfg(head_dim=96), 16) == 0
     assert radar.workspace_bytes(_cfg(n_features=100), 16) == 0
+    assert radar.workspace_bytes(_cfg(n_features=2048), 16) > n16
     assert radar.workspace_bytes(_cfg(dtype=torch.float32), 16) > 0
     # a bf16 Omega with a bf16 cache; refused with an fp32 cache
     assert radar.workspace_bytes(_cfg(omega_dtype=torch.bfloat16), 16) == n16
@@ -160,7 +161,7 @@ def test_validation_before_launch(L):
     assert L.radar_build_index(by(c), good, good, 1, good, None) == 1
     assert L.radar_append(by(c), good, good, good, good, good, 5, null, good,
                           None) == 1
-    for bad in (_cfg(head_dim=256), _cfg(n_features=1024),
+    for bad in (_cfg(head_dim=256), _cfg(n_features=4096), _cfg(n_features=768),
                 _cfg(n_q_heads=96, n_kv_heads=32), _cfg(capacity=1 << 31),
                 _cfg(batch=2048, n_q_heads=32, n_kv_heads=32)):
         assert L.radar_build_index(by(bad.c_struct()), good, good, 1, good,
