@@ -138,7 +138,7 @@ def step_bytes(wl, t, U, s_kv, sqrt_schedule=False, exact=False, s_om=4):
     """Algorithmic HBM bytes of one step whose decode runs at length t (the
     append wrote row t - 1). U: union size per (b, kv head).
     Returns (whole step, decode call, K/V gather, candidate-key scan, row
-    append); with exact=True the selection scans every candidate key
+    append, summary rows read); with exact=True the selection scans every candidate key
     instead of reading phi(q)'s inputs and the summaries. s_om: bytes per
     Omega entry."""
     d, n = wl.head_dim, wl.n_features
@@ -159,7 +159,7 @@ def step_bytes(wl, t, U, s_kv, sqrt_schedule=False, exact=False, s_om=4):
         close += BH * (t * d * s_kv + (t // c) * n * 4)
     scan = BH * n_cand * c * d * s_kv
     decode = (scan if exact else summ + om) + kv + qo
-    return decode + app + close, decode, kv, scan, app
+    return decode + app + close, decode, kv, scan, app, (0 if exact else summ)
 
 
 def run_signature(line):
@@ -172,6 +172,8 @@ def run_signature(line):
            "omega": cfg["omega"]}
     if cfg.get("kv", "device") != "device":
         sig["kv"] = cfg["kv"]
+    if cfg.get("n_features_override"):
+        sig["n_features"] = cfg["n_features"]
     return sig
 
 
@@ -348,6 +350,9 @@ def main():
                     help="instead of timing: recall of Radar's selection "
                          "against the exact search over n and k, one JSON "
                          "line per (n, k)")
+    ap.add_argument("--n-features", type=int, default=0,
+                    help="random features n instead of the workload's "
+                         "(64 ... 2048)")
     ap.add_argument("--kv-host", type=int, default=0,
                     help="1: the K/V cache in pinned host memory mapped for "
                          "the GPU; the decode gathers the selected segments "
@@ -374,6 +379,10 @@ def main():
                            "fused": radar.PATH_FUSED,
                            "select": radar.PATH_SELECT}[args.path])
     wl = workloads.WORKLOADS[args.workload]
+    if args.n_features:
+        # another feature count on the same keys and queries (Omega drawn at
+        # that size)
+        wl = wl.scaled(n_features=args.n_features)
     if args.recall:
         recall_sweep(wl)
         return
@@ -517,11 +526,11 @@ def main():
 
     # ---- algorithmic bytes ------------------------------------------------
     sel_np = sel_log.cpu().numpy()
-    tot_bytes, dec_bytes, kv_bytes, scan_bytes = 0, 0, 0, 0
+    tot_bytes, dec_bytes, kv_bytes, scan_bytes, summ_bytes = 0, 0, 0, 0, 0
     for j in range(Ksteps):
         t = wl.t0 + W + j + 1
         U = union_sizes(sel_np[j], wl.group)
-        b_all, b_dec, b_kv, b_scan, b_app = step_bytes(
+        b_all, b_dec, b_kv, b_scan, b_app, b_summ = step_bytes(
             wl, t, U, s_kv, sqrt_schedule=args.schedule == "sqrt", exact=exact,
             s_om=s_om)
         tot_bytes += b_all
@@ -529,12 +538,14 @@ def main():
         dec_bytes += b_dec + (b_app if merged else 0)
         kv_bytes += b_kv
         scan_bytes += b_scan
+        summ_bytes += b_summ
     step_gbps = tot_bytes / (ms * 1e-3) / 1e9
     path = radar.decode_path(dataclasses.replace(cfg, seg_len=seg_timed,
                                                  window=win_timed),
                              wl.t0 + W + 1, wl.top_k)
-    # dominant kernel: the fused decode (all decode bytes), or the split
-    # path's gather-attention kernel (the K/V bytes)
+    # dominant kernel: the fused decode (all decode bytes), or on the split
+    # path the longer of the gather attention (the K/V bytes) and the score
+    # pass (the summary rows; the longer one for large n)
     if exact:
         # the exact selector runs the split path; its key scan dominates
         path = radar.PATH_SPLIT
@@ -543,6 +554,9 @@ def main():
         dom, dom_name, dom_bytes = "fused", "k_decode_fused", dec_bytes
     else:
         dom, dom_name, dom_bytes = "attend", "k_attend", kv_bytes
+        avg = {k: prof[k][0] / max(prof[k][1], 1) for k in ("attend", "score")}
+        if prof["score"][1] and avg["score"] > avg["attend"]:
+            dom, dom_name, dom_bytes = "score", "k_score", summ_bytes
     dom_ms, dom_n = prof[dom]
     dom_avg_ms = dom_ms / max(dom_n, 1)
     dom_gbps = (dom_bytes / Ksteps) / (dom_avg_ms * 1e-3) / 1e9
@@ -609,6 +623,7 @@ def main():
             "selector": args.selector,
             "omega": "bf16" if s_om == 2 else "f32",
             "kv": "pinned host memory" if args.kv_host else "device",
+            "n_features_override": bool(args.n_features),
             "restructures": restructures,
         },
         "hbm_GBps": round(step_gbps, 1),

@@ -1001,6 +1001,9 @@ __global__ __launch_bounds__(256) void k_score(const float* __restrict__ phiq,
           x[bt][r][0] = src[0];
         }
       }
+    // with several chunks the compiler would sink each load to its first
+    // use and wait on one load at a time; keep the chunk's loads together
+    if constexpr (NCH > 1) __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int bt = 0; bt < RB; ++bt)
 #pragma unroll
