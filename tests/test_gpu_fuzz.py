@@ -56,6 +56,8 @@ def draw(seed):
     # drawn last, so the earlier draws of a seed stay what they were
     opt["merged"] = bool(rng.random() < 0.5)
     opt["omega_bf16"] = bool(wl.dtype == "bf16" and rng.random() < 0.5)
+    if rng.random() < 0.1:                    # the split path's chunked scores
+        wl = wl.scaled(n_features=int(rng.choice([1024, 2048])))
     return wl, opt, path
 
 
