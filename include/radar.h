@@ -117,8 +117,7 @@ typedef struct {
   int32_t n_q_heads;   /* Hq; Hq % Hkv == 0, G = Hq / Hkv in {1, 2, 4, 8}   */
   int32_t n_kv_heads;  /* Hkv >= 1; B * Hkv <= 65535                        */
   int32_t head_dim;    /* d in {64, 128}                                    */
-  int32_t n_features;  /* n in {64, 128, ..., 2048} (powers of two); above
-                          512 the decode takes the split path              */
+  int32_t n_features;  /* n in {64, 128, ..., 2048} (powers of two)         */
   int32_t seg_len;     /* c >= 1 (any value; need not divide anything)      */
   int32_t window;      /* w >= 0                                            */
   int64_t capacity;    /* token rows per head in K and V, 1 .. 2^31 - 1     */

@@ -1420,7 +1420,8 @@ __global__ __launch_bounds__(256) void k_attend(
 //      already in flight (waves whose first row is past the candidates
 //      load none);
 //   2. Eq. 6 scores of all candidates into LDS (16 or 32 summary rows per
-//      wave per pass, streaming loads);
+//      wave per pass, streaming loads; above n = 512 each 16-row batch in
+//      feature chunks, and phase 1 writes phi(q) to LDS chunk by chunk);
 //   3. waves < G take the top-k of one head each, while the other waves
 //      already attend the window tiles (the window never depends on the
 //      selection);
@@ -1537,7 +1538,10 @@ __global__ __launch_bounds__(512) void k_decode_fused(
       constexpr bool kPrefetch = NP <= 8;
       const int r = lane >> 4, jj = lane & 15;
       float qv[G][QPL], nrm[G];
-      float ph[NP][G];
+      // above n = 512 each chunk's features go to LDS at once (all NP
+      // passes would not fit in registers)
+      constexpr bool kChunkOut = N > 512;
+      float ph[kChunkOut ? PC : NP][G];
 #pragma unroll
       for (int c0 = 0; c0 < NP; c0 += PC) {
         // the Omega loads come first in each copy of the phase, so the
@@ -1588,15 +1592,27 @@ __global__ __launch_bounds__(512) void k_decode_fused(
           }
 #pragma unroll
           for (int g = 0; g < G; ++g)
-            ph[c0 + p][g] = fast_exp2(fmaf(row_sum(a[g]), s1, -nrm[g] * s2)) * inv_sqrt_n;
+            ph[kChunkOut ? p : c0 + p][g] =
+                fast_exp2(fmaf(row_sum(a[g]), s1, -nrm[g] * s2)) * inv_sqrt_n;
+        }
+        if constexpr (kChunkOut) {
+          if (jj == 0) {
+#pragma unroll
+            for (int p = 0; p < PC; ++p)
+#pragma unroll
+              for (int g = 0; g < G; ++g)
+                phq[g * N + (c0 + p) * 4 * NW + wave * 4 + r] = ph[p][g];
+          }
         }
       }
-      if (!kPrefetch && rb0 < n_cand) load_rows(rb0);
-      if (jj == 0) {
+      if constexpr (!kChunkOut) {
+        if (!kPrefetch && rb0 < n_cand) load_rows(rb0);
+        if (jj == 0) {
 #pragma unroll
-        for (int p = 0; p < NP; ++p)
+          for (int p = 0; p < NP; ++p)
 #pragma unroll
-          for (int g = 0; g < G; ++g) phq[g * N + p * 4 * NW + wave * 4 + r] = ph[p][g];
+            for (int g = 0; g < G; ++g) phq[g * N + p * 4 * NW + wave * 4 + r] = ph[p][g];
+        }
       }
     };
     if constexpr (sizeof(T) == 2) {
@@ -1608,7 +1624,62 @@ __global__ __launch_bounds__(512) void k_decode_fused(
     __syncthreads();
 
     // ---- 2. scores ------------------------------------------------------
-    {
+    if constexpr (N > 512) {
+      // each 16-row batch in chunks of FC features per lane (chunk ch of
+      // lane l: features ch * 64 * FC + l * FC + e), the layout and order
+      // of the split path's score kernel, so a lane holds one chunk of the
+      // batch's rows at a time
+      constexpr int FC = G >= 4 ? 4 : 8;
+      constexpr int NCH = FPL / FC;
+      const float* rbase = summ + (bh * s_cap) * N + lane * FC;
+      for (int rb = wave * 16; rb < n_cand; rb += NW * 16) {
+        float part[G][16];
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) part[g][i] = 0.f;
+#pragma unroll 1
+        for (int ch = 0; ch < NCH; ++ch) {
+          float xx[16][FC];
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            const int row = min(rb + i, n_cand - 1);
+            const float* src = rbase + (int64_t)row * N + ch * 64 * FC;
+#pragma unroll
+            for (int e = 0; e < FC; e += 4) {
+              const float4 v = ld_stream_f4(src + e);
+              xx[i][e] = v.x; xx[i][e + 1] = v.y; xx[i][e + 2] = v.z; xx[i][e + 3] = v.w;
+            }
+          }
+          float pq[G][FC];
+#pragma unroll
+          for (int g = 0; g < G; ++g)
+#pragma unroll
+            for (int e = 0; e < FC; ++e) pq[g][e] = phq[g * N + ch * 64 * FC + lane * FC + e];
+          // keep the chunk's loads together (the compiler would otherwise
+          // sink each to its first use and wait on one at a time)
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int g = 0; g < G; ++g)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+              float a = part[g][i];
+#pragma unroll
+              for (int e = 0; e < FC; ++e) a = fmaf(xx[i][e], pq[g][e], a);
+              part[g][i] = a;
+            }
+        }
+        const int row = rb + (lane & 15);
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+          transpose_reduce<16>(part[g], lane);
+          float v = part[g][0];
+          v += __shfl_xor(v, 16);
+          v += __shfl_xor(v, 32);
+          if (lane < 16 && row < n_cand) sc[g * kFusedMaxCand + row] = v;
+        }
+      }
+    } else {
       float pq[G][FPL];
 #pragma unroll
       for (int g = 0; g < G; ++g)
@@ -2278,7 +2349,8 @@ radar_status launch_fused_g(RADAR_FUSED_PARAMS) {
     case 128: return launch_fused_n<T, D, G, 128, SEL>(RADAR_FUSED_ARGS);
     case 256: return launch_fused_n<T, D, G, 256, SEL>(RADAR_FUSED_ARGS);
     case 512: return launch_fused_n<T, D, G, 512, SEL>(RADAR_FUSED_ARGS);
-    default: return RADAR_EUNSUPPORTED;    // n > 512 takes the split path
+    case 1024: return launch_fused_n<T, D, G, 1024, SEL>(RADAR_FUSED_ARGS);
+    default: return launch_fused_n<T, D, G, 2048, SEL>(RADAR_FUSED_ARGS);
   }
 }
 
@@ -2370,9 +2442,7 @@ int64_t pair_bytes(const Shape& s, const SeqArgs& sa) {
 //  - split: phi(q), scores and top-k as separate chip-wide kernels.
 int choose_path(const Shape& s, const SeqArgs& sa) {
   const int n_cand = make_span(sa.t_max, sa).n_cand;
-  // the fused and select kernels hold a lane's n / 64 features of every
-  // summary row of a batch in registers: n <= 512
-  const bool fits_select = s.G <= kFusedMaxG && n_cand <= kFusedMaxCand && s.n <= 512;
+  const bool fits_select = s.G <= kFusedMaxG && n_cand <= kFusedMaxCand;
   const bool fits_fused = fits_select && !(s.dt == RADAR_F32 && s.d == 128);
   switch (g_path_override) {
     case RADAR_PATH_SPLIT: return RADAR_PATH_SPLIT;

@@ -107,13 +107,13 @@ def test_full_size_sampled(name, steps, ngroups, path):
                                          (1024, 4, "f32"), (2048, 1, "f32"),
                                          (2048, 8, "bf16")])
 def test_large_feature_counts(n, G, dtype):
-    """n = 1024 and 2048 (the paper's default feature count): the split
-    path's scores read each summary row in feature chunks; every decode path
-    request takes the split path there."""
+    """n = 1024 and 2048 (the paper's default feature count): the score
+    passes read each summary row in feature chunks (the split path's score
+    kernel and the fused and select kernels' phase 2)."""
     wl = Workload(f"n{n}_g{G}", batch=2, n_q_heads=2 * G, n_kv_heads=2, head_dim=128,
                   t0=2100, seg_len=64, top_k=6, n_features=n, window=64, dtype=dtype,
                   steps=6, keys="clustered", planted=2)
-    for path in (radar.PATH_AUTO, radar.PATH_FUSED):
+    for path in (radar.PATH_SPLIT, radar.PATH_FUSED, radar.PATH_SELECT):
         _run(wl, 6, path=path)
 
 
@@ -147,12 +147,12 @@ def test_path_choice():
         assert radar.decode_path(cfg(g5), g5.t0 + 1, g5.top_k) == radar.PATH_FUSED
         many = mha.scaled(seg_len=64, window=64)           # 2047 candidates
         assert radar.decode_path(cfg(many), many.t0 + 1, 16) == radar.PATH_SPLIT
-        wide = mha.scaled(n_features=2048)                  # n > 512
-        assert radar.decode_path(cfg(wide), wide.t0 + 1, 16) == radar.PATH_SPLIT
+        wide = mha.scaled(n_features=2048)                  # the paper's n
+        assert radar.decode_path(cfg(wide), wide.t0 + 1, 16) == radar.PATH_FUSED
         radar.set_decode_path(radar.PATH_SELECT)
         assert radar.decode_path(cfg(g5), g5.t0 + 1, g5.top_k) == radar.PATH_SELECT
         assert radar.decode_path(cfg(g8), g8.t0 + 1, 16) == radar.PATH_SPLIT
-        assert radar.decode_path(cfg(wide), wide.t0 + 1, 16) == radar.PATH_SPLIT
+        assert radar.decode_path(cfg(wide), wide.t0 + 1, 16) == radar.PATH_SELECT
     finally:
         radar.set_decode_path(radar.PATH_AUTO)
 
