@@ -43,3 +43,25 @@ def test_json_line_fields():
         assert key in rl, key
     assert rl["bound"] == "hbm" and rl["unit"] == "GB/s" and rl["peak"] == 8000.0
     assert 0 < rl["frac"] < 1 and abs(rl["frac"] - rl["achieved"] / rl["peak"]) < 1e-3
+
+
+@pytest.mark.gpu
+def test_json_line_options():
+    """--kv-host adds the host-link rate of the K/V gather; --n-features
+    replaces the workload's feature count (and is named in config)."""
+    print("[case] bench.py tiny workload, --kv-host 1 --n-features 1024", flush=True)
+    r = subprocess.run([sys.executable, BENCH, "--workload", "tiny", "--steps", "4",
+                        "--warmup", "1", "--cpu-baseline", "0", "--peaks", "0",
+                        "--calibrate-copy", "0", "--build-reps", "1", "--build-warmup", "1",
+                        "--kv-host", "1", "--n-features", "1024"],
+                       capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0, r.stderr[-2000:]
+    lines = [ln for ln in r.stdout.splitlines() if ln.strip()]
+    assert len(lines) == 1, lines
+    d = json.loads(lines[0])
+    assert d["config"]["kv"] == "pinned host memory"
+    assert d["config"]["n_features"] == 1024 and d["config"]["n_features_override"]
+    hl = d["host_link"]
+    assert hl["unit"] == "GB/s" and hl["kv_bytes_per_step"] > 0
+    assert 0 < hl["achieved"] and abs(hl["frac"] - hl["achieved"] / hl["peak"]) < 1e-3
+    assert d["roofline"]["traffic"] is None        # no counter record for this run
