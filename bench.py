@@ -134,27 +134,29 @@ def union_sizes(sel, G):
     return out
 
 
-def step_bytes(wl, t, U, s_kv, sqrt_schedule=False, exact=False, s_om=4):
+def step_bytes(wl, t, U, s_kv, sqrt_schedule=False, exact=False, s_om=4, n_sink=0):
     """Algorithmic HBM bytes of one step whose decode runs at length t (the
     append wrote row t - 1). U: union size per (b, kv head).
     Returns (whole step, decode call, K/V gather, candidate-key scan, row
     append, summary rows read); with exact=True the selection scans every candidate key
     instead of reading phi(q)'s inputs and the summaries. s_om: bytes per
-    Omega entry."""
+    Omega entry; n_sink: attention-sink rows, always attended, after which
+    the segments and the window start."""
     d, n = wl.head_dim, wl.n_features
     if sqrt_schedule:
         c, w = radar.schedule_sqrt(t)
     else:
         c, w = wl.seg_len, wl.window
-    ws, n_cand = window_split(t, c, w)
-    W = t - ws
+    te = t - n_sink                    # tokens after the sinks
+    ws, n_cand = window_split(te, c, w)
+    W = te - ws
     BH = wl.batch * wl.n_kv_heads
     summ = BH * n_cand * n * 4
-    kv = int(np.sum(U * c + W)) * d * 2 * s_kv
+    kv = int(np.sum(U * c + W + n_sink)) * d * 2 * s_kv
     qo = wl.batch * wl.n_q_heads * d * 2 * s_kv
     om = n * d * s_om
     app = BH * 4 * d * s_kv            # read k_new, v_new; write both rows
-    close = BH * (c * d * s_kv + n * 4) if t % c == 0 else 0
+    close = BH * (c * d * s_kv + n * 4) if te % c == 0 else 0
     if sqrt_schedule and w == 0:       # restructure: all t keys re-summarised
         close += BH * (t * d * s_kv + (t // c) * n * 4)
     scan = BH * n_cand * c * d * s_kv
@@ -174,6 +176,9 @@ def run_signature(line):
         sig["kv"] = cfg["kv"]
     if cfg.get("n_features_override"):
         sig["n_features"] = cfg["n_features"]
+    for key, default in (("gqa_mode", "union"), ("n_sink", 0)):
+        if cfg.get(key, default) != default:
+            sig[key] = cfg[key]
     return sig
 
 
@@ -350,6 +355,11 @@ def main():
                     help="instead of timing: recall of Radar's selection "
                          "against the exact search over n and k, one JSON "
                          "line per (n, k)")
+    ap.add_argument("--gqa-mode", default="union", choices=["union", "per_head"],
+                    help="grouped query heads attend their group's union, or "
+                         "each its own selection")
+    ap.add_argument("--sinks", type=int, default=0,
+                    help="attention-sink rows at the start of the cache")
     ap.add_argument("--n-features", type=int, default=0,
                     help="random features n instead of the workload's "
                          "(64 ... 2048)")
@@ -370,6 +380,10 @@ def main():
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the decode path runs on a single "
               "device (run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+    if args.sinks and args.schedule == "sqrt":
+        print("bench.py: --sinks with --schedule sqrt is not measured (the byte "
+              "model's restructure term has no sinks)", file=sys.stderr)
         sys.exit(2)
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
@@ -401,7 +415,10 @@ def main():
         assert torch.equal(omega.float(), inp.omega)
     cfg = radar.Config(wl.batch, wl.n_q_heads, wl.n_kv_heads, wl.head_dim,
                        wl.n_features, wl.seg_len, wl.window, wl.t0 + total,
-                       wl.torch_dtype(), omega_dtype=omega.dtype)
+                       wl.torch_dtype(), n_sink=args.sinks,
+                       gqa_mode=(radar.GQA_PER_HEAD if args.gqa_mode == "per_head"
+                                 else radar.GQA_UNION),
+                       omega_dtype=omega.dtype)
     s_kv = 2 if wl.dtype == "bf16" else 4
     s_om = omega.element_size()
     K, V = inp.K, inp.V
@@ -532,7 +549,7 @@ def main():
         U = union_sizes(sel_np[j], wl.group)
         b_all, b_dec, b_kv, b_scan, b_app, b_summ = step_bytes(
             wl, t, U, s_kv, sqrt_schedule=args.schedule == "sqrt", exact=exact,
-            s_om=s_om)
+            s_om=s_om, n_sink=args.sinks)
         tot_bytes += b_all
         # with the merged call the fused kernel also does the row append
         dec_bytes += b_dec + (b_app if merged else 0)
@@ -567,7 +584,8 @@ def main():
     log("[bench] kernels: " + json.dumps(kern))
 
     cpu = None
-    if args.cpu_baseline and not exact:
+    # the oracle's timing covers the default options only
+    if args.cpu_baseline and not exact and args.sinks == 0 and args.gqa_mode == "union":
         log("[bench] cpu baseline (fp64 oracle)")
         cpu = cpu_baseline(wl, inp, W, Ksteps, n_heads=args.cpu_heads,
                            sqrt_schedule=args.schedule == "sqrt")
@@ -624,6 +642,8 @@ def main():
             "omega": "bf16" if s_om == 2 else "f32",
             "kv": "pinned host memory" if args.kv_host else "device",
             "n_features_override": bool(args.n_features),
+            "gqa_mode": args.gqa_mode,
+            "n_sink": args.sinks,
             "restructures": restructures,
         },
         "hbm_GBps": round(step_gbps, 1),
