@@ -57,3 +57,21 @@ def test_traffic_only_for_the_same_run():
         assert bench.measured_traffic(k, w, _line(rec, omega="other")) is None
     assert bench.measured_traffic("k_decode_fused", "no_such_workload",
                                   {"steps": 1, "warmup": 0, "config": {}}) is None
+
+
+def test_byte_model_with_sinks():
+    """The sinks are attended on top of the same candidates and window:
+    shifting the context by the sinks adds exactly their rows to the K/V
+    bytes and leaves the summary bytes alone."""
+    import numpy as np
+    wl = workloads.WORKLOADS["mha_128k"]
+    BH = wl.batch * wl.n_kv_heads
+    U = np.full(BH, wl.top_k)
+    for t in (wl.t0 + 1, wl.t0 + 255, wl.t0 + 256):
+        base = bench.step_bytes(wl, t, U, 2)
+        assert base == bench.step_bytes(wl, t, U, 2, n_sink=0)
+        for s in (1, 64):
+            sh = bench.step_bytes(wl, t + s, U, 2, n_sink=s)
+            assert sh[2] - base[2] == BH * s * wl.head_dim * 2 * 2      # K/V gather
+            assert sh[5] == base[5]                                      # summary rows
+            assert sh[4] == base[4]                                      # row append
