@@ -902,8 +902,14 @@ __device__ void group_union(const int* sel, unsigned* bits, int G, int per,
   }
   __syncthreads();
   if (tid < kWave) {
+    // this lane's word of every head's map, read once (the per-bit head
+    // masks below then need no LDS reads)
+    uint32_t wv[kMaxG];
+#pragma unroll
+    for (int g = 0; g < kMaxG; ++g) wv[g] = g < nmaps ? bits[g * kBitmapWords + tid] : 0u;
     uint32_t word = 0u;
-    for (int g = 0; g < nmaps; ++g) word |= bits[g * kBitmapWords + tid];
+#pragma unroll
+    for (int g = 0; g < kMaxG; ++g) word |= wv[g];
     const int pc = __popc(word);
     // exclusive prefix sum of the popcounts over the 64 lanes
     int incl = pc;
@@ -918,8 +924,8 @@ __device__ void group_union(const int* sel, unsigned* bits, int G, int per,
       unsigned m = kAllHeads;
       if (masks) {
         m = 0u;
-        for (int g = 0; g < G; ++g)
-          m |= ((bits[g * kBitmapWords + tid] >> bit) & 1u) << g;
+#pragma unroll
+        for (int g = 0; g < kMaxG; ++g) m |= ((wv[g] >> bit) & 1u) << g;
       }
       uni[pos++] = (tid * 32 + bit) | (int)(m << kUniIdBits);
       word &= word - 1u;
