@@ -101,6 +101,16 @@ def test_per_head_gqa(wl, path):
     _run(wl, steps, path, per_head=True)
 
 
+@PATHS
+def test_per_head_widest_union(path):
+    # eight heads, each selecting the largest k from the largest candidate
+    # count (2048 one-token segments): the union and its eight-bit head masks
+    # span the whole bitmap
+    wl = _edge("ph_g8_k256", n_q_heads=8, n_kv_heads=1, t0=2055, seg_len=1,
+               window=8, top_k=256, n_features=64, keys="clustered")
+    _run(wl, 1, path, per_head=True)
+
+
 # --------------------------------------------------------------------------
 # ragged batches
 # --------------------------------------------------------------------------
