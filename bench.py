@@ -227,9 +227,13 @@ def cpu_baseline(wl, inp, first_step, n_steps, n_heads, min_s=10.0,
     from oracle import radar_oracle as orc
     G, c = wl.group, wl.seg_len
     rng = np.random.default_rng(5)
-    pairs = [(int(b), int(h)) for b, h in
-             zip(rng.integers(0, wl.batch, n_heads),
-                 rng.integers(0, wl.n_q_heads, n_heads))]
+    # distinct pairs, drawn without replacement (all of them when the
+    # workload has no more than n_heads)
+    total = wl.batch * wl.n_q_heads
+    pick = (np.arange(total) if n_heads >= total
+            else np.sort(rng.choice(total, n_heads, replace=False)))
+    pairs = [(int(i) // wl.n_q_heads, int(i) % wl.n_q_heads) for i in pick]
+    all_pairs = len(pairs) == total
     om = inp.omega.double().cpu().numpy()
     last = first_step + n_steps
     state = []
@@ -280,7 +284,8 @@ def cpu_baseline(wl, inp, first_step, n_steps, n_heads, min_s=10.0,
     step_s = per_head_step * wl.batch * wl.n_q_heads
     return {"value": wl.batch / step_s, "unit": "tokens/s",
             "cores": blas_threads(), "kind": "oracle",
-            "sample": (f"{len(state)} sampled (batch, q head) pairs x "
+            "sample": ((f"all {len(state)}" if all_pairs else f"{len(state)} sampled") +
+                       f" (batch, q head) pairs x "
                        f"{n_steps} decode steps x {passes} pass(es) "
                        f"({done} head-steps, {el:.1f} s), scaled to all "
                        f"{wl.batch * wl.n_q_heads} heads; the index build "
