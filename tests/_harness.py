@@ -13,7 +13,8 @@ Acceptance rules:
     the GPU selected plus the window (identical to the oracle's own output
     whenever the sets agree);
   * scores of the selected segments: relative error against the oracle's
-    Eq. 6 values, reported and bounded;
+    Eq. 6 values at most 1e-5 (the tie band: an error below it cannot move
+    a segment across the band);
   * summaries: relative error per element <= 1e-4.
 """
 from __future__ import annotations
@@ -30,8 +31,21 @@ from oracle import radar_oracle as orc
 
 TIE_BAND = 1e-5
 OUT_TOL = {"f32": 2e-3, "bf16": 1e-2}
-SCORE_TOL = 2e-5
+SCORE_TOL = 1e-5
 SUMM_TOL = 1e-4
+
+# The largest errors and the band swaps seen by every check of this process
+# (the GPU run's margins against the tolerances above; tests/conftest.py
+# prints them at the end of the session).
+MARGINS = {"episodes": 0, "heads": 0, "band_swaps": 0, "max_score_err": 0.0,
+           "max_summ_err": 0.0, "max_out_err_f32": 0.0, "max_out_err_bf16": 0.0,
+           "tolerances": {"score": SCORE_TOL, "summary": SUMM_TOL,
+                          "out_f32": OUT_TOL["f32"], "out_bf16": OUT_TOL["bf16"],
+                          "tie_band": TIE_BAND}}
+
+
+def note_score_err(err):
+    MARGINS["max_score_err"] = max(MARGINS["max_score_err"], float(err))
 
 
 def config_of(wl: workloads.Workload, capacity: int, n_sink: int = 0,
@@ -100,11 +114,12 @@ class Episode:
 
     def __init__(self, wl, steps, groups=None, device="cuda",
                  path=radar.PATH_AUTO, n_sink=0, per_head=False, lens0=None,
-                 merged=False, omega_bf16=False):
+                 merged=False, omega_bf16=False, kv_host=False):
         self.wl = wl
         self.steps = steps
         self.path = path
         self.merged = merged
+        self.kv_host = kv_host
         self.n_sink, self.per_head = n_sink, per_head
         self.lens0 = list(lens0) if lens0 is not None else None
         self.inp = workloads.make_inputs(wl, device, steps=steps)
@@ -142,14 +157,35 @@ class Episode:
     def run(self, check_steps=None):
         radar.set_decode_path(self.path)
         try:
-            return self._run(check_steps)
+            st = self._run(check_steps)
         finally:
             radar.set_decode_path(radar.PATH_AUTO)
+            self._note_margins()
+        return st
+
+    def _note_margins(self):
+        st = self.stats
+        M = MARGINS
+        M["episodes"] += 1
+        M["heads"] += st.heads
+        M["band_swaps"] += st.band_swaps
+        M["max_score_err"] = max(M["max_score_err"], st.max_score_err)
+        M["max_summ_err"] = max(M["max_summ_err"], st.max_summ_err)
+        key = "max_out_err_" + self.wl.dtype
+        M[key] = max(M[key], st.max_out_err)
 
     def _run(self, check_steps):
         wl, inp, cfg = self.wl, self.inp, self.cfg
         dev = inp.K.device
-        K, V = inp.K.clone(), inp.V.clone()
+        if self.kv_host:
+            # the cache in pinned host memory mapped for the device (the
+            # kernels read it over the host link); everything else on the GPU
+            K = torch.empty(inp.K.shape, dtype=inp.K.dtype, pin_memory=True)
+            V = torch.empty(inp.V.shape, dtype=inp.V.dtype, pin_memory=True)
+            K.copy_(inp.K)
+            V.copy_(inp.V)
+        else:
+            K, V = inp.K.clone(), inp.V.clone()
         summ = radar.new_summaries(cfg, dev)
         radar.build_index(cfg, K, self.omega_dev, wl.t0, summ)
         lens = [wl.t0] * wl.batch if self.lens0 is None else list(self.lens0)

@@ -89,6 +89,32 @@ def test_host_cache_equals_device_cache(merged, path):
         assert torch.equal(_bits(a.cpu()), _bits(b.cpu())), what
 
 
+KVH_ORACLE = [
+    # G = 4, bf16, two sequences; a segment closes at t = 4352 (step 20)
+    WORKLOADS["gqa_64k"].scaled(name="kvhost_oracle_g4", batch=2, n_q_heads=8,
+                                n_kv_heads=2, t0=4331),
+    # one head per group, fp32 cache, d = 64; a segment closes at t = 1280
+    WORKLOADS["tiny"].scaled(name="kvhost_oracle_f32", t0=1270),
+]
+
+
+@PATHS
+@pytest.mark.parametrize("merged", [False, True], ids=["separate", "merged"])
+@pytest.mark.parametrize("wl", KVH_ORACLE, ids=[w.name for w in KVH_ORACLE])
+def test_host_cache_matches_oracle(wl, merged, path):
+    """With K and V in pinned host memory, every step's selections, scores
+    and outputs, and the summaries (built over the host link, and refreshed
+    by the append that closes a segment) against the fp64 oracle."""
+    steps = 24
+    print(f"[case] K/V in pinned host memory vs oracle: {wl.name} path={path} "
+          f"merged={merged}", flush=True)
+    ep = H.Episode(wl, steps, path=path, merged=merged, kv_host=True,
+                   omega_bf16=wl.dtype == "bf16")
+    st = ep.run()
+    assert not ep.K.is_cuda and ep.K.is_pinned()
+    assert st.heads == steps * wl.batch * wl.n_q_heads
+
+
 def test_binding_refuses_unpinned_host_cache():
     wl = WORKLOADS["tiny"].scaled(name="kvhost_refuse", t0=300, steps=1)
     cfg = H.config_of(wl, wl.t0 + 1)

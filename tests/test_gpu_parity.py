@@ -103,6 +103,24 @@ def test_full_size_sampled(name, steps, ngroups, path):
     torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("name,steps,close_step,path", [
+    ("mha_128k", 258, 255, radar.PATH_AUTO), ("mha_128k", 258, 255, radar.PATH_SPLIT),
+    ("gqa_64k", 258, 255, radar.PATH_AUTO), ("gqa_512k", 614, 611, radar.PATH_AUTO)],
+    ids=["mha_128k-auto", "mha_128k-split", "gqa_64k-auto", "gqa_512k-auto"])
+def test_full_size_segment_close(name, steps, close_step, path):
+    """Full-size workloads past their first segment close (the append at
+    step close_step fills a segment: t = 131328 at 128K, 65792 at 64K GQA,
+    524900 at 512K), on one sampled (batch, kv head) group: selections,
+    scores and outputs checked against the oracle around the close, and the
+    group's summaries (the closed segment's included) at the end."""
+    wl = WORKLOADS[name]
+    assert (wl.t0 + close_step + 1) % wl.seg_len == 0
+    _run(wl, steps, groups=H.sample_groups(wl, 1, seed=2),
+         check_steps={0, close_step - 1, close_step, close_step + 1, steps - 1},
+         path=path)
+    torch.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("n,G,dtype", [(1024, 1, "bf16"), (2048, 4, "bf16"),
                                          (1024, 4, "f32"), (2048, 1, "f32"),
                                          (2048, 8, "bf16")])
@@ -365,6 +383,8 @@ def test_exact_ties_take_lower_index(path, k):
     V = rng.standard_normal((B, NH, t0 + 1, d))
     q = rng.standard_normal((B, NH, d)) * 0.5
     om = rng.standard_normal((n, d))
+    # both sides read the same values: the fp32 tensors the GPU gets, widened
+    K, V, q, om = (x.astype(np.float32).astype(np.float64) for x in (K, V, q, om))
     wl = Workload("ties", B, NH, NH, d, t0, c, k, n, 5, "f32", 1, "gauss", 1)
     cfg = H.config_of(wl, t0 + 1)
     Kt = torch.tensor(K, dtype=torch.float32, device="cuda")

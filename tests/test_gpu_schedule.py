@@ -67,6 +67,7 @@ def test_sqrt_schedule_episode(path, dtype, Hq, Hkv, d, k):
                     picks = [int(x) for x in s_np[0, h, :k_eff]]
                     union.update(picks)
                     err = np.max(np.abs(sc_np[0, h, :k_eff] - ora[picks]) / ora[picks])
+                    H.note_score_err(err)
                     assert err <= H.SCORE_TOL, (i, h, err)
                 toks = orc.attended_tokens(sorted(union), c, ws, t)
                 for h in range(g * G, (g + 1) * G):
