@@ -23,7 +23,8 @@
  *    memory. The library allocates no device memory, keeps no device
  *    state between calls, never synchronises, and launches only on `stream`
  *    (the path override and the profiling switch are host-side settings of
- *    the calling thread).
+ *    the calling thread). The one device buffer of its own is the scratch
+ *    array of radar_append_decode_noalloc, whose contents no call depends on.
  *  - Layouts are dense, row-major, element type `kv_dtype` for q / K / V /
  *    k_new / v_new / out, `omega_dtype` for Omega, fp32 for summaries and
  *    scores, int32 for segment ids:
@@ -94,7 +95,7 @@
 extern "C" {
 #endif
 
-#define RADAR_ABI_VERSION 4
+#define RADAR_ABI_VERSION 5
 
 typedef enum {
   RADAR_OK = 0,
@@ -194,6 +195,33 @@ radar_status radar_append_decode(const radar_config* cfg, const void* q,
                                  int32_t* selected, float* scores,
                                  void* workspace, size_t workspace_bytes,
                                  hipStream_t stream);
+
+/* Bytes of the library's own decode scratch (one copy per GPU). */
+#define RADAR_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): exactly
+ * radar_append_decode, with the same arguments, kernels and results, except
+ * that the decode's scratch is a device array of the library's own of
+ * RADAR_NOALLOC_SCRATCH_BYTES bytes instead of a caller workspace. The call
+ * allocates nothing: each GPU the library runs on holds one copy of the
+ * array (placed by the loader with the library's code), found on the first
+ * call on that device, until the process ends. `stream` must belong to the
+ * current device (else RADAR_EINVAL). A shape and k whose
+ * radar_decode_workspace_bytes exceeds RADAR_NOALLOC_SCRATCH_BYTES return
+ * RADAR_EWORKSPACE before anything is launched. The array keeps what the
+ * last call wrote; no call depends on its contents on entry. Every call on
+ * one GPU uses the same array, so calls that may overlap on one GPU (other
+ * streams, other host threads) race on it and must be serialised by the
+ * caller. */
+radar_status radar_append_decode_noalloc(const radar_config* cfg,
+                                         const void* q, void* K, void* V,
+                                         const void* k_new, const void* v_new,
+                                         const void* omega, float* summaries,
+                                         int64_t t, const int64_t* pos,
+                                         int32_t k, void* out,
+                                         int32_t* selected, float* scores,
+                                         hipStream_t stream);
 
 /* Exact segment search (the exact-selection ablation of Section 3.3): like
  * radar_decode, but each query head selects the k candidate segments with

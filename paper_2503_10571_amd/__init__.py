@@ -17,7 +17,9 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libradar.so")
 
-ABI_VERSION = 4
+ABI_VERSION = 5
+# bytes of the library's own decode scratch (RADAR_NOALLOC_SCRATCH_BYTES)
+NOALLOC_SCRATCH_BYTES = 32 << 20
 RADAR_F32, RADAR_BF16 = 0, 1
 GQA_UNION, GQA_PER_HEAD = 0, 1
 STATUS = {0: "ok", 1: "invalid argument", 2: "position outside the cache capacity",
@@ -104,6 +106,8 @@ def lib() -> ctypes.CDLL:
                                          _P, _P, sz, _P]
         L.radar_append_decode.argtypes = [cfgp, _P, _P, _P, _P, _P, _P, _P, i64,
                                           _P, i32, _P, _P, _P, _P, sz, _P]
+        L.radar_append_decode_noalloc.argtypes = [cfgp, _P, _P, _P, _P, _P, _P,
+                                                  _P, i64, _P, i32, _P, _P, _P, _P]
         L.radar_decode_workspace_bytes.argtypes = [cfgp, i32]
         L.radar_decode_workspace_bytes.restype = sz
         L.radar_attend_selected.argtypes = [cfgp, _P, _P, _P, _P, i32, i64, _P,
@@ -127,7 +131,8 @@ def lib() -> ctypes.CDLL:
         for fn in ("radar_peak_mfma", "radar_peak_exp"):
             getattr(L, fn).restype = ctypes.c_int
         for fn in ("radar_build_index", "radar_append", "radar_decode",
-                   "radar_append_decode", "radar_decode_exact",
+                   "radar_append_decode", "radar_append_decode_noalloc",
+                   "radar_decode_exact",
                    "radar_attend_selected",
                    "radar_profile_enable", "radar_profile_read"):
             getattr(L, fn).restype = ctypes.c_int
@@ -312,6 +317,31 @@ def append_decode(cfg: Config, q, K, V, k_new, v_new, omega, summaries,
         _ptr(v_new), _ptr(omega), _ptr(summaries), t, _ptr(pos), k, _ptr(out),
         _ptr(selected), _ptr(scores), _ptr(workspace), workspace.numel(),
         _stream(q)))
+    return out
+
+
+def append_decode_noalloc(cfg: Config, q, K, V, k_new, v_new, omega, summaries,
+                          t: int, k: int, out, selected=None, scores=None,
+                          pos=None):
+    """radar_append_decode_noalloc: append_decode() with the decode's scratch
+    in the library's own device array instead of a workspace (for callers
+    that cannot allocate: nothing is allocated here either, so `out` must be
+    given). Calls that may overlap on one GPU must be serialised."""
+    _query(cfg, q); _cache(cfg, K, V); _rows(cfg, k_new, v_new)
+    _omega(cfg, omega); _summ(cfg, summaries)
+    pos = _lens(pos, cfg, "pos")
+    if out is None:
+        raise ValueError("out must be given (this call allocates nothing)")
+    _need(out, cfg.dtype, "out", cfg.batch * cfg.n_q_heads * cfg.head_dim)
+    n_sel = cfg.batch * cfg.n_q_heads * k
+    if selected is not None:
+        _need(selected, torch.int32, "selected", n_sel, at_least=True)
+    if scores is not None:
+        _need(scores, torch.float32, "scores", n_sel, at_least=True)
+    _check("radar_append_decode_noalloc", lib().radar_append_decode_noalloc(
+        ctypes.byref(cfg.c_struct()), _ptr(q), _ptr(K), _ptr(V), _ptr(k_new),
+        _ptr(v_new), _ptr(omega), _ptr(summaries), t, _ptr(pos), k, _ptr(out),
+        _ptr(selected), _ptr(scores), _stream(q)))
     return out
 
 

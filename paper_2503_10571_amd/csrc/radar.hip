@@ -44,6 +44,7 @@
 #include <cstdint>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <type_traits>
 #include <vector>
 
@@ -2595,6 +2596,92 @@ radar_status run_decode(const Shape& s, const WsLayout& L, const SeqArgs& sa,
   return launch_attend(s, q, Kp, Vp, plan.ag, sa, out, w, L, stream);
 }
 
+radar_status append_decode_impl(const radar_config* cfg, const void* q, void* K, void* V,
+                                const void* k_new, const void* v_new, const void* omega,
+                                float* summaries, int64_t t, const int64_t* pos,
+                                int32_t k, void* out, int32_t* selected, float* scores,
+                                void* workspace, size_t workspace_bytes,
+                                hipStream_t stream) {
+  Shape s;
+  radar_status r = check_append(cfg, &s, K, V, k_new, v_new, omega, summaries, pos);
+  if (r != RADAR_OK) return r;
+  if (!q || !out) return RADAR_EINVAL;
+  if (!aligned16(q) || !aligned16(out) || (selected && !aligned16(selected)) ||
+      (scores && !aligned16(scores)))
+    return RADAR_EINVAL;
+  WsLayout L;
+  SeqArgs sa;
+  r = check_decode(cfg, &s, t, pos, k, workspace, workspace_bytes, &L, &sa);
+  if (r != RADAR_OK) return r;
+  sa.lens_add = pos ? 1 : 0;
+  DecodePlan plan;
+  r = plan_decode(s, L, sa, &plan);
+  if (r != RADAR_OK) return r;
+  unsigned char* w = static_cast<unsigned char*>(workspace);
+  const AppendArgs ap = append_args(s, K, V, k_new, v_new, pos, t - 1);
+  if (s.w == 0) {
+    // Without a window the segment this row completes is already a
+    // candidate of the same step: write the row and refresh its summary
+    // first, then decode.
+    launch(RADAR_K_APPEND, k_append, dim3((unsigned)(s.B * s.Hkv)), dim3(64), 0,
+           stream, ap, s.cap, s.Hkv);
+    r = launch_status();
+    if (r == RADAR_OK) r = refresh_closed(s, K, omega, summaries, t - 1, pos, stream);
+    if (r != RADAR_OK) return r;
+    return run_decode(s, L, sa, plan, q, K, V, omega, summaries, out, selected, scores,
+                      w, AppendArgs{}, stream);
+  }
+  // With w >= 1 the completed segment ends inside the window, so the decode
+  // does not read its summary: the refresh runs after it.
+  r = run_decode(s, L, sa, plan, q, K, V, omega, summaries, out, selected, scores, w,
+                 ap, stream);
+  if (r != RADAR_OK) return r;
+  return refresh_closed(s, K, omega, summaries, t - 1, pos, stream);
+}
+
+
+// ---- the decode scratch without allocation ---------------------------------
+// radar_append_decode_noalloc keeps the decode's workspace in this array
+// instead of a caller buffer: one copy per GPU the library runs on (the
+// loader places it with the code object), held until the process ends.
+// Host code never passes the array's name to a kernel (on the host it is
+// only a stand-in for the symbol): the device address comes from
+// hipGetSymbolAddress, looked up once per device with that device current.
+constexpr size_t kScratchBytes = RADAR_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The scratch address on the device of `stream` (which must be the current
+// device: the lookup runs with it current).
+radar_status scratch_of(hipStream_t stream, void** out) {
+  int cur = -1, dev = -1;
+  if (hipGetDevice(&cur) != hipSuccess) return launch_status();
+  if (stream) {
+    if (hipStreamGetDevice(stream, &dev) != hipSuccess) return launch_status();
+  } else {
+    dev = cur;
+  }
+  if (dev != cur) return RADAR_EINVAL;
+  if (dev < 0 || dev >= kMaxDevices) return RADAR_EUNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) {
+      snprintf(g_last_error, sizeof g_last_error, "hipGetSymbolAddress: %s",
+               hipGetErrorString(e));
+      (void)hipGetLastError();
+      return RADAR_EHIP;
+    }
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return RADAR_OK;
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------------------
@@ -2759,42 +2846,29 @@ radar_status radar_append_decode(const radar_config* cfg, const void* q, void* K
                                  const int64_t* pos, int32_t k, void* out,
                                  int32_t* selected, float* scores, void* workspace,
                                  size_t workspace_bytes, hipStream_t stream) {
-  Shape s;
-  radar_status r = check_append(cfg, &s, K, V, k_new, v_new, omega, summaries, pos);
-  if (r != RADAR_OK) return r;
-  if (!q || !out) return RADAR_EINVAL;
-  if (!aligned16(q) || !aligned16(out) || (selected && !aligned16(selected)) ||
-      (scores && !aligned16(scores)))
-    return RADAR_EINVAL;
-  WsLayout L;
-  SeqArgs sa;
-  r = check_decode(cfg, &s, t, pos, k, workspace, workspace_bytes, &L, &sa);
-  if (r != RADAR_OK) return r;
-  sa.lens_add = pos ? 1 : 0;
-  DecodePlan plan;
-  r = plan_decode(s, L, sa, &plan);
-  if (r != RADAR_OK) return r;
-  unsigned char* w = static_cast<unsigned char*>(workspace);
-  const AppendArgs ap = append_args(s, K, V, k_new, v_new, pos, t - 1);
-  if (s.w == 0) {
-    // Without a window the segment this row completes is already a
-    // candidate of the same step: write the row and refresh its summary
-    // first, then decode.
-    launch(RADAR_K_APPEND, k_append, dim3((unsigned)(s.B * s.Hkv)), dim3(64), 0,
-           stream, ap, s.cap, s.Hkv);
-    r = launch_status();
-    if (r == RADAR_OK) r = refresh_closed(s, K, omega, summaries, t - 1, pos, stream);
-    if (r != RADAR_OK) return r;
-    return run_decode(s, L, sa, plan, q, K, V, omega, summaries, out, selected, scores,
-                      w, AppendArgs{}, stream);
-  }
-  // With w >= 1 the completed segment ends inside the window, so the decode
-  // does not read its summary: the refresh runs after it.
-  r = run_decode(s, L, sa, plan, q, K, V, omega, summaries, out, selected, scores, w,
-                 ap, stream);
-  if (r != RADAR_OK) return r;
-  return refresh_closed(s, K, omega, summaries, t - 1, pos, stream);
+  return append_decode_impl(cfg, q, K, V, k_new, v_new, omega, summaries, t, pos, k,
+                            out, selected, scores, workspace, workspace_bytes, stream);
 }
+
+radar_status radar_append_decode_noalloc(const radar_config* cfg, const void* q,
+                                         void* K, void* V, const void* k_new,
+                                         const void* v_new, const void* omega,
+                                         float* summaries, int64_t t,
+                                         const int64_t* pos, int32_t k, void* out,
+                                         int32_t* selected, float* scores,
+                                         hipStream_t stream) {
+  Shape s;
+  if (check_cfg(cfg, &s) != RADAR_OK || k < 1 || k > kMaxK)
+    return append_decode_impl(cfg, q, K, V, k_new, v_new, omega, summaries, t, pos, k,
+                              out, selected, scores, nullptr, 0, stream);
+  if (ws_layout(s, k).total > kScratchBytes) return RADAR_EWORKSPACE;
+  void* w = nullptr;
+  const radar_status r = scratch_of(stream, &w);
+  if (r != RADAR_OK) return r;
+  return append_decode_impl(cfg, q, K, V, k_new, v_new, omega, summaries, t, pos, k,
+                            out, selected, scores, w, kScratchBytes, stream);
+}
+
 
 radar_status radar_decode_exact(const radar_config* cfg, const void* q,
                                 const void* K, const void* V, int64_t t,

@@ -114,12 +114,14 @@ class Episode:
 
     def __init__(self, wl, steps, groups=None, device="cuda",
                  path=radar.PATH_AUTO, n_sink=0, per_head=False, lens0=None,
-                 merged=False, omega_bf16=False, kv_host=False):
+                 merged=False, omega_bf16=False, noalloc=False, kv_host=False):
         self.wl = wl
         self.steps = steps
         self.path = path
         self.merged = merged
+        self.noalloc = noalloc
         self.kv_host = kv_host
+        assert merged or not noalloc
         self.n_sink, self.per_head = n_sink, per_head
         self.lens0 = list(lens0) if lens0 is not None else None
         self.inp = workloads.make_inputs(wl, device, steps=steps)
@@ -201,7 +203,12 @@ class Episode:
             q = inp.q[i].contiguous()
             pos = None if self.lens0 is None else \
                 torch.tensor(lens, dtype=torch.int64, device=dev)
-            if self.merged:
+            if self.merged and self.noalloc:
+                lens = [x + 1 for x in lens]
+                radar.append_decode_noalloc(cfg, q, K, V, kn, vn, self.omega_dev,
+                                            summ, max(lens), wl.top_k, out,
+                                            selected=sel, scores=sc, pos=pos)
+            elif self.merged:
                 lens = [x + 1 for x in lens]
                 radar.append_decode(cfg, q, K, V, kn, vn, self.omega_dev, summ,
                                     max(lens), wl.top_k, out=out, selected=sel,

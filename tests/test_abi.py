@@ -39,7 +39,7 @@ def test_exports_every_declared_symbol(L):
 
 
 def test_version_and_strings(L):
-    assert L.radar_abi_version() == radar.ABI_VERSION == 4
+    assert L.radar_abi_version() == radar.ABI_VERSION == 5
     for st in range(6):
         assert L.radar_status_string(st).decode()
     assert L.radar_last_error() is not None
@@ -207,6 +207,21 @@ def test_validation_before_launch(L):
                                  ws - 1, None) == 5
     assert L.radar_append_decode(*ad, 1000, null, 16, null, None, None, good,
                                  ws, None) == 1
+    # append_decode_noalloc: the same checks (a bad config or k fails
+    # before the scratch is looked up), and a shape whose scratch exceeds the
+    # library's array is refused
+    assert L.radar_append_decode_noalloc(None, good, good, good, good, good,
+                                         good, good, 1000, null, 16, good,
+                                         None, None, None) == 1
+    assert L.radar_append_decode_noalloc(*ad, 1000, null, 0, good, None, None,
+                                         None) == 3
+    assert L.radar_append_decode_noalloc(*ad, 1000, null, 300, good, None,
+                                         None, None) == 3
+    huge = _cfg(batch=64, capacity=1 << 20).c_struct()
+    assert L.radar_decode_workspace_bytes(by(huge), 16) > radar.NOALLOC_SCRATCH_BYTES
+    assert L.radar_append_decode_noalloc(by(huge), good, good, good, good, good,
+                                         good, good, 1000, null, 16, good,
+                                         None, None, None) == 5
     # measurement microkernels
     work = ctypes.c_double()
     assert L.radar_peak_mfma(0, good, by(work), None) == 1
@@ -223,3 +238,24 @@ def test_product_path_has_no_fallback(monkeypatch, tmp_path):
     monkeypatch.setattr(radar, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(RuntimeError, match="missing"):
         radar.lib()
+
+
+def test_noalloc_scratch_size_matches_the_header():
+    """The binding's copy of RADAR_NOALLOC_SCRATCH_BYTES is the header's, and
+    it holds the decode workspace of every benchmark workload."""
+    import workloads
+    text = open(HEADER).read()
+    m = re.search(r"#define RADAR_NOALLOC_SCRATCH_BYTES \(\(size_t\)(\d+) << (\d+)\)",
+                  text)
+    assert m, "macro not found"
+    assert int(m.group(1)) << int(m.group(2)) == radar.NOALLOC_SCRATCH_BYTES
+
+
+def test_noalloc_scratch_holds_every_workload(L):
+    import workloads
+    import torch
+    for wl in workloads.WORKLOADS.values():
+        cfg = radar.Config(wl.batch, wl.n_q_heads, wl.n_kv_heads, wl.head_dim,
+                           wl.n_features, wl.seg_len, wl.window, wl.capacity + 64,
+                           wl.torch_dtype())
+        assert 0 < radar.workspace_bytes(cfg, wl.top_k) <= radar.NOALLOC_SCRATCH_BYTES, wl.name
