@@ -57,8 +57,13 @@ class Stepper:
     cost stays small next to the GPU time)."""
 
     def __init__(self, cfg, inp, K, V, summ, ws, out, k, omega, sqrt_schedule=False,
-                 exact=False, merged=True):
+                 exact=False, merged=True, extra_layers=()):
         self.L = radar.lib()
+        # further layers (K, V, summaries) the token also passes through;
+        # each step decodes it in every layer in turn (fixed schedule)
+        P0 = ctypes.c_void_p
+        self.extra = [(P0(a.data_ptr()), P0(b.data_ptr()), P0(c.data_ptr()))
+                      for a, b, c in extra_layers]
         self.sqrt = sqrt_schedule
         self.exact = exact
         self.merged = merged
@@ -90,6 +95,11 @@ class Stepper:
                     self.cfgp, self.q[i], self.K, self.V, self.kn[i], self.vn[i],
                     self.om, self.summ, t + 1, None, self.k, self.out, sel, None,
                     self.ws, self.ws_n, self.stream)
+                for (Kl, Vl, Sl) in self.extra:
+                    st = st or self.L.radar_append_decode(
+                        self.cfgp, self.q[i], Kl, Vl, self.kn[i], self.vn[i],
+                        self.om, Sl, t + 1, None, self.k, self.out, None, None,
+                        self.ws, self.ws_n, self.stream)
                 if st:
                     raise radar.RadarError("radar_append_decode", st)
                 return
@@ -110,6 +120,14 @@ class Stepper:
                     raise radar.RadarError("radar_build_index", st)
                 self.restructures += 1
             self.cfg_c.window = t + 1 - c * c
+        for (Kl, Vl, Sl) in self.extra:
+            st = self.L.radar_append(self.cfgp, Kl, Vl, self.kn[i], self.vn[i],
+                                     self.om, t, None, Sl, self.stream)
+            st = st or self.L.radar_decode(self.cfgp, self.q[i], Kl, Vl, self.om, Sl,
+                                           t + 1, None, self.k, self.out, None, None,
+                                           self.ws, self.ws_n, self.stream)
+            if st:
+                raise radar.RadarError("radar_append / radar_decode", st)
         if self.exact:
             st = self.L.radar_decode_exact(self.cfgp, self.q[i], self.K, self.V,
                                            t + 1, None, self.k, self.out, sel,
@@ -165,42 +183,54 @@ def step_bytes(wl, t, U, s_kv, sqrt_schedule=False, exact=False, s_om=4, n_sink=
 
 
 def run_signature(line):
-    """What fixes the bytes per launch of a run besides the workload: the
-    step range (the context grows by one row a step) and the call form."""
+    """What fixes the HBM traffic of a launch relative to its algorithmic
+    bytes besides the kernel source: the workload and the call form (the
+    step range only scales both, one row per step)."""
     cfg = line["config"]
-    sig = {"steps": line["steps"], "warmup": line["warmup"],
-           "decode_path": cfg["decode_path"], "schedule": cfg["schedule"],
+    sig = {"decode_path": cfg["decode_path"], "schedule": cfg["schedule"],
            "calls": cfg["calls"], "selector": cfg["selector"],
            "omega": cfg["omega"]}
     if cfg.get("kv", "device") != "device":
         sig["kv"] = cfg["kv"]
     if cfg.get("n_features_override"):
         sig["n_features"] = cfg["n_features"]
-    for key, default in (("gqa_mode", "union"), ("n_sink", 0)):
+    for key, default in (("gqa_mode", "union"), ("n_sink", 0), ("layers", 1)):
         if cfg.get(key, default) != default:
             sig[key] = cfg[key]
     return sig
 
 
-def measured_traffic(kernel, workload, line):
-    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
-    record (FETCH_SIZE and WRITE_SIZE KiB per dispatch, each divided by the
-    scale a 1 GiB copy kernel shows), or None when there is no record, the
-    kernel source has changed since it was taken, or the record's run had
-    another step range or call form than this one (its launches then move
-    other bytes)."""
+def source_sha256():
+    """One hash over every file the library is built from."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.json")
+    from paper_2503_10571_amd import _build
+    h = hashlib.sha256()
+    for path in _build.sources():
+        h.update(os.path.relpath(path, ROOT).encode())
+        h.update(open(path, "rb").read())
+    return h.hexdigest()
+
+
+def measured_traffic(kernel, workload, line, alg_bytes_per_launch, profiles=None):
+    """HBM traffic per launch of `kernel` from the committed rocprofv3
+    counter record: the record's FETCH_SIZE + WRITE_SIZE bytes (each divided
+    by the scale a 1 GiB copy kernel shows) over its algorithmic bytes,
+    times this run's algorithmic bytes per launch. FETCH_SIZE counts L2
+    misses, so bytes served by the Infinity Cache count as traffic too.
+    Returns (bytes, ratio), or None when there is no record, the library's
+    sources have changed since it was taken, or it was taken with another
+    call form."""
+    path = os.path.join(profiles or os.path.join(ROOT, "profiles"),
+                        f"traffic_{kernel}_{workload}.json")
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
-    src = os.path.join(ROOT, rec["source"])
-    if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["source_sha256"]:
+    if rec.get("sources_sha256") != source_sha256():
         return None
     if rec.get("run") != run_signature(line):
         return None
-    return int(rec["fetch_size_kib"] * 1024 / rec["fetch_scale"] +
-               rec["write_size_kib"] * 1024 / rec["write_scale"])
+    ratio = float(rec["traffic_ratio"])
+    return int(ratio * alg_bytes_per_launch), ratio
 
 
 def blas_threads():
@@ -215,81 +245,137 @@ def blas_threads():
     return int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
 
 
-def cpu_baseline(wl, inp, first_step, n_steps, n_heads, min_s=10.0,
-                 max_s=25.0, sqrt_schedule=False):
-    """The fp64 oracle (as it stands) on `n_heads` sampled (b, q head) pairs
-    over the timed steps: per step a segment-close refresh when one is due,
-    then phi(q), scores, top-k and exact attention. The pass over the steps
-    repeats until at least `min_s` seconds of work (at most `max_s`). Scaled
-    to the workload's tokens/s (all heads). With the sqrt schedule the
-    segment length follows Algorithm 1 and a perfect square rebuilds the
-    summaries inside the timed step."""
+def _widen(x):
+    """A torch tensor (fp32, or bf16 carried as its raw 16-bit words) as
+    float64 numpy."""
+    if x.dtype == np.uint16:
+        return (x.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    return x.astype(np.float64)
+
+
+def _as_words(t):
+    t = t.contiguous().cpu()
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).numpy().view(np.uint16)
+    return t.float().numpy()
+
+
+def oracle_worker(job):
+    """The fp64 oracle on some (batch, q head) pairs of a workload, one BLAS
+    thread: per decode step a segment-close refresh when one is due, then
+    phi(q), scores, top-k and exact attention. Repeats its pass over the
+    steps until min_s seconds of work (at most max_s). Returns (head-steps,
+    seconds). Module level so that a process pool can run it."""
+    try:
+        from threadpoolctl import threadpool_limits
+    except Exception:
+        threadpool_limits = None
+    if threadpool_limits is not None:
+        with threadpool_limits(1):
+            return _oracle_run(job)
+    return _oracle_run(job)
+
+
+def _oracle_run(job):
     from oracle import radar_oracle as orc
-    G, c = wl.group, wl.seg_len
-    rng = np.random.default_rng(5)
-    # distinct pairs, drawn without replacement (all of them when the
-    # workload has no more than n_heads)
-    total = wl.batch * wl.n_q_heads
-    pick = (np.arange(total) if n_heads >= total
-            else np.sort(rng.choice(total, n_heads, replace=False)))
-    pairs = [(int(i) // wl.n_q_heads, int(i) % wl.n_q_heads) for i in pick]
-    all_pairs = len(pairs) == total
-    om = inp.omega.double().cpu().numpy()
-    last = first_step + n_steps
+    (t0, first_step, n_steps, c, w, top_k, sqrt_schedule, om_words, pairs,
+     min_s, max_s) = job
+    om = _widen(om_words)
     state = []
-    for b, h in pairs:
-        g = h // G
-        keys = inp.keys_at(last, b, g).double().cpu().numpy()
-        vals = inp.values_at(last, b, g).double().cpu().numpy()
-        t_start = wl.t0 + first_step
+    for (keys_w, vals_w, qs_w) in pairs:
+        keys, vals, qs = _widen(keys_w), _widen(vals_w), _widen(qs_w)
+        t_start = t0 + first_step
         c0 = orc.sqrt_schedule(t_start)[0] if sqrt_schedule else c
         summ = orc.segment_summaries(keys[:t_start], om, c0)  # index (untimed)
-        state.append([b, h, keys, vals, summ])
-    qs = inp.q[first_step:last].double().cpu().numpy()
-    start_summ = [st[4] for st in state]
+        state.append([keys, vals, qs, summ, summ])
     done, passes = 0, 0
     t_begin = time.perf_counter()
     while True:
-        for st, s0 in zip(state, start_summ):
-            st[4] = s0
+        for st in state:
+            st[3] = st[4]
         for i in range(n_steps):
-            t = wl.t0 + first_step + i + 1
-            if sqrt_schedule:
-                cs, w = orc.sqrt_schedule(t)
-            else:
-                cs, w = c, wl.window
+            t = t0 + first_step + i + 1
+            cs, ww = orc.sqrt_schedule(t) if sqrt_schedule else (c, w)
             for st in state:
-                b, h, keys, vals, summ = st
-                if sqrt_schedule and w == 0:   # restructure at a square
-                    st[4] = summ = orc.segment_summaries(keys[:t], om, cs)
+                keys, vals, qs, summ, _ = st
+                if sqrt_schedule and ww == 0:   # restructure at a square
+                    st[3] = summ = orc.segment_summaries(keys[:t], om, cs)
                 elif not sqrt_schedule and t % c == 0:
                     # the appended row closed a segment
-                    new = orc.segment_summaries(keys[:t], om, c,
-                                                first=t // c - 1)
-                    st[4] = summ = np.concatenate([summ, new], 0)
-                ws, n_cand = orc.window_split(t, cs, w)
-                phi_q = orc.random_features(qs[i, b, h], om)
-                _, sel = orc.decode_head(phi_q, summ, n_cand, wl.top_k)
+                    new = orc.segment_summaries(keys[:t], om, c, first=t // c - 1)
+                    st[3] = summ = np.concatenate([summ, new], 0)
+                ws, n_cand = orc.window_split(t, cs, ww)
+                phi_q = orc.random_features(qs[i], om)
+                _, sel = orc.decode_head(phi_q, summ, n_cand, top_k)
                 toks = orc.attended_tokens(sel, cs, ws, t)
-                orc.attend(qs[i, b, h], keys, vals, toks)
+                orc.attend(qs[i], keys, vals, toks)
                 done += 1
             if time.perf_counter() - t_begin > max_s:
                 break
         passes += 1
-        if time.perf_counter() - t_begin >= min_s or \
-                time.perf_counter() - t_begin > max_s:
+        el = time.perf_counter() - t_begin
+        if el >= min_s or el > max_s:
             break
-    el = time.perf_counter() - t_begin
-    per_head_step = el / done
-    step_s = per_head_step * wl.batch * wl.n_q_heads
-    return {"value": wl.batch / step_s, "unit": "tokens/s",
-            "cores": blas_threads(), "kind": "oracle",
-            "sample": ((f"all {len(state)}" if all_pairs else f"{len(state)} sampled") +
-                       f" (batch, q head) pairs x "
-                       f"{n_steps} decode steps x {passes} pass(es) "
-                       f"({done} head-steps, {el:.1f} s), scaled to all "
-                       f"{wl.batch * wl.n_q_heads} heads; the index build "
-                       "before the sample is untimed")}
+    return done, time.perf_counter() - t_begin
+
+
+def cpu_baseline(wl, inp, first_step, n_steps, n_heads=4, min_s=8.0, max_s=20.0,
+                 sqrt_schedule=False, workers=None):
+    """The fp64 oracle (as it stands) timed on the host on a bounded sample
+    of the timed steps: sampled (batch, q head) pairs, each decoded over the
+    timed steps. Two timings, each scaled to the workload's tokens/s over
+    all heads: one process with one BLAS thread on `n_heads` pairs, and a
+    pool of one-thread worker processes, one per usable core (at most 16),
+    each on its own pair; `value` is the pool's. The oracle's per-head loop
+    is serial Python, so the pool is how it uses the cores."""
+    import multiprocessing as mp
+    cores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") \
+        else (os.cpu_count() or 1)
+    P = max(1, min(cores, 16)) if workers is None else workers
+    total = wl.batch * wl.n_q_heads
+    rng = np.random.default_rng(5)
+    n_pick = min(total, max(n_heads, P))
+    pick = (np.arange(total) if n_pick >= total
+            else np.sort(rng.choice(total, n_pick, replace=False)))
+    pairs = [(int(i) // wl.n_q_heads, int(i) % wl.n_q_heads) for i in pick]
+    last = first_step + n_steps
+    data = []
+    for b, h in pairs:
+        g = h // wl.group
+        data.append((_as_words(inp.keys_at(last, b, g)), _as_words(inp.values_at(last, b, g)),
+                     _as_words(inp.q[first_step:last, b, h])))
+    om = _as_words(inp.omega)
+    common = (wl.t0, first_step, n_steps, wl.seg_len, wl.window, wl.top_k,
+              sqrt_schedule, om)
+
+    def per_token(done, sec):
+        return wl.batch / (sec / done * total)
+
+    # one process, one thread
+    d1, s1 = oracle_worker(common + (data[:n_heads], min_s, max_s))
+    one = per_token(d1, s1)
+    # one worker per core, a pair each (the pairs cycle when there are fewer)
+    jobs = [common + ([data[i % len(data)]], min_s, max_s) for i in range(P)]
+    ctx = mp.get_context("spawn")
+    t_begin = time.perf_counter()
+    with ctx.Pool(P) as pool:
+        res = pool.map(oracle_worker, jobs)
+    wall = time.perf_counter() - t_begin
+    done = sum(r[0] for r in res)
+    busy = max(r[1] for r in res)
+    allc = per_token(done, busy)
+    return {"value": allc, "unit": "tokens/s", "cores": P, "kind": "oracle",
+            "value_1_thread": one, "cores_affinity": cores,
+            "cpu_count": os.cpu_count(), "blas_threads_per_process": 1,
+            "sample": (f"{P} one-thread worker processes, each decoding one "
+                       f"(batch, q head) pair ({len(data)} distinct pairs of "
+                       f"{total}) over the {n_steps} timed steps until "
+                       f"{min_s:.0f} s of work ({done} head-steps in "
+                       f"{busy:.1f} s per worker, {wall:.1f} s with start-up); "
+                       f"value_1_thread: one process, one thread, {min(n_heads, len(data))} "
+                       f"pairs, {d1} head-steps in {s1:.1f} s; both scaled to all "
+                       f"{total} heads; each pair's index build before the "
+                       "sample is untimed")}
 
 
 def recall_sweep(wl):
@@ -322,7 +408,7 @@ def main():
     ap.add_argument("--workload", default="mha_128k",
                     choices=sorted(workloads.WORKLOADS))
     ap.add_argument("--cpu-baseline", type=int, default=1)
-    ap.add_argument("--cpu-heads", type=int, default=8)
+    ap.add_argument("--cpu-heads", type=int, default=4)
     ap.add_argument("--calibrate-copy", type=int, default=1,
                     help="also run a plain 1 GiB read+write elementwise "
                          "kernel: this GPU's copy bandwidth (and the counter "
@@ -351,7 +437,7 @@ def main():
     ap.add_argument("--build-warmup", type=int, default=4,
                     help="untimed index builds before the timed ones")
     ap.add_argument("--path", default="auto",
-                    choices=["auto", "split", "fused", "select"],
+                    choices=["auto", "split", "fused", "select", "scored"],
                     help="decode path (auto: the library's choice)")
     ap.add_argument("--selector", default="radar", choices=["radar", "exact"],
                     help="radar: Eq. 6 scores (the method); exact: the exact "
@@ -377,6 +463,17 @@ def main():
                          "projection rounds it to bf16 anyway; same results, "
                          "half the Omega bytes), fp32 otherwise; f32: always "
                          "fp32")
+    ap.add_argument("--layers", type=int, default=1,
+                    help="layers the token passes through each step, each with "
+                         "its own K/V cache and summaries (the same contents): "
+                         "with two or more, a step's working set no longer "
+                         "fits the Infinity Cache between its visits, as in a "
+                         "multi-layer decode; tokens/s counts one token "
+                         "through all layers")
+    ap.add_argument("--cold-pass", type=int, default=1,
+                    help="also time the dominant kernel with the Infinity "
+                         "Cache and L2 swept between steps (a 1 GiB "
+                         "read-modify-write outside the event bracket)")
     ap.add_argument("--schedule", default="fixed", choices=["fixed", "sqrt"],
                     help="fixed: the workload's segment length and window; "
                          "sqrt: Algorithm 1's restructuring (c = sqrt(t) at "
@@ -390,13 +487,19 @@ def main():
         print("bench.py: --sinks with --schedule sqrt is not measured (the byte "
               "model's restructure term has no sinks)", file=sys.stderr)
         sys.exit(2)
+    if args.layers < 1 or (args.layers > 1 and (args.schedule != "fixed" or
+                                                  args.selector != "radar" or
+                                                  args.kv_host or args.graph)):
+        print("bench.py: --layers > 1 runs the fixed schedule, the radar selector "
+              "and a device cache, eagerly", file=sys.stderr)
+        sys.exit(2)
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(2)
 
     radar.set_decode_path({"auto": radar.PATH_AUTO, "split": radar.PATH_SPLIT,
-                           "fused": radar.PATH_FUSED,
-                           "select": radar.PATH_SELECT}[args.path])
+                           "fused": radar.PATH_FUSED, "select": radar.PATH_SELECT,
+                           "scored": radar.PATH_SCORED}[args.path])
     wl = workloads.WORKLOADS[args.workload]
     if args.n_features:
         # another feature count on the same keys and queries (Omega drawn at
@@ -471,9 +574,15 @@ def main():
 
     # ---- decode steps ----------------------------------------------------
     merged = bool(args.merged) and not exact
+    extra_layers = []
+    for _ in range(args.layers - 1):
+        # another layer: its own copy of the cache and of the summaries
+        Kl, Vl, Sl = K.clone(), V.clone(), summ.clone()
+        extra_layers.append((Kl, Vl, Sl))
+    torch.cuda.synchronize()
     stp = Stepper(cfg, inp, K, V, summ, ws, out, wl.top_k, omega,
                   sqrt_schedule=args.schedule == "sqrt", exact=exact,
-                  merged=merged)
+                  merged=merged, extra_layers=extra_layers)
     sel_log = torch.empty(Ksteps, wl.batch, wl.n_q_heads, wl.top_k,
                           dtype=torch.int32, device=gpu)
     log(f"[bench] warmup {W} steps")
@@ -495,9 +604,14 @@ def main():
                               K, omega, t_timed, summ)
         torch.cuda.synchronize()
 
-    def profiled_pass():
+    def profiled_pass(flush=None):
+        # flush: a buffer swept (read and written) between steps, outside the
+        # kernels' event brackets, so that every step starts with the
+        # Infinity Cache and the L2s holding none of the step's data
         radar.profile_enable(True)
         for j in range(Ksteps):
+            if flush is not None:
+                flush.add_(1)
             stp.step(W + j)
         torch.cuda.synchronize()
         p = radar.profile_read()
@@ -545,16 +659,24 @@ def main():
         # the same steps again with every kernel bracketed by HIP events
         rewind()
         prof = profiled_pass()
+    prof_cold = None
+    if args.cold_pass and not args.kv_host:
+        log("[bench] cold pass: 1 GiB swept between steps")
+        rewind()
+        flush = torch.zeros(1 << 28, dtype=torch.int32, device=gpu)
+        prof_cold = profiled_pass(flush)
+        del flush
 
     # ---- algorithmic bytes ------------------------------------------------
     sel_np = sel_log.cpu().numpy()
     tot_bytes, dec_bytes, kv_bytes, scan_bytes, summ_bytes = 0, 0, 0, 0, 0
+    NL = args.layers           # every layer moves the same bytes
     for j in range(Ksteps):
         t = wl.t0 + W + j + 1
         U = union_sizes(sel_np[j], wl.group)
-        b_all, b_dec, b_kv, b_scan, b_app, b_summ = step_bytes(
+        b_all, b_dec, b_kv, b_scan, b_app, b_summ = (NL * x for x in step_bytes(
             wl, t, U, s_kv, sqrt_schedule=args.schedule == "sqrt", exact=exact,
-            s_om=s_om, n_sink=args.sinks)
+            s_om=s_om, n_sink=args.sinks))
         tot_bytes += b_all
         # with the merged call the fused kernel also does the row append
         dec_bytes += b_dec + (b_app if merged else 0)
@@ -574,6 +696,12 @@ def main():
         dom, dom_name, dom_bytes = "score", "k_segment_mass", scan_bytes
     elif path == radar.PATH_FUSED:
         dom, dom_name, dom_bytes = "fused", "k_decode_fused", dec_bytes
+    elif path == radar.PATH_SCORED:
+        # the fused kernel from its top-k on: the K/V gather (and the rows the
+        # merged call appends)
+        dom, dom_name = "scored", "k_decode_fused (scored)"
+        dom_bytes = kv_bytes + (NL * Ksteps * wl.batch * wl.n_kv_heads * 4 * wl.head_dim
+                                * s_kv if merged else 0)
     else:
         dom, dom_name, dom_bytes = "attend", "k_attend", kv_bytes
         avg = {k: prof[k][0] / max(prof[k][1], 1) for k in ("attend", "score")}
@@ -581,8 +709,18 @@ def main():
             dom, dom_name, dom_bytes = "score", "k_score", summ_bytes
     dom_ms, dom_n = prof[dom]
     dom_avg_ms = dom_ms / max(dom_n, 1)
-    dom_gbps = (dom_bytes / Ksteps) / (dom_avg_ms * 1e-3) / 1e9
+    per_launch = dom_bytes / (Ksteps * NL)     # one launch per layer and step
+    dom_gbps = per_launch / (dom_avg_ms * 1e-3) / 1e9
     tokens_s = wl.batch * Ksteps / (ms * 1e-3)
+    cold = None
+    if prof_cold is not None and prof_cold[dom][1]:
+        c_avg = prof_cold[dom][0] / prof_cold[dom][1]
+        c_gbps = per_launch / (c_avg * 1e-3) / 1e9
+        cold = {"avg_us": round(c_avg * 1e3, 2), "achieved": round(c_gbps, 1),
+                "frac": round(c_gbps / HBM_PEAK_GBPS, 4),
+                "sweep": "1 GiB read and written between steps, outside the "
+                         "event bracket (evicts the 256 MB Infinity Cache and "
+                         "the L2s)"}
 
     kern = {k: {"avg_us": round(v[0] / max(v[1], 1) * 1e3, 2), "launches": v[1]}
             for k, v in prof.items() if v[1]}
@@ -590,7 +728,8 @@ def main():
 
     cpu = None
     # the oracle's timing covers the default options only
-    if args.cpu_baseline and not exact and args.sinks == 0 and args.gqa_mode == "union":
+    if args.cpu_baseline and not exact and args.sinks == 0 and args.gqa_mode == "union" \
+            and NL == 1:
         log("[bench] cpu baseline (fp64 oracle)")
         cpu = cpu_baseline(wl, inp, W, Ksteps, n_heads=args.cpu_heads,
                            sqrt_schedule=args.schedule == "sqrt")
@@ -612,6 +751,13 @@ def main():
         del x, y
 
     peaks = radar.peak_rates() if args.peaks else None
+    read_gbps = None
+    if args.peaks:
+        del extra_layers
+        stp.extra = []
+        torch.cuda.empty_cache()
+        read_gbps = radar.peak_read_gbps()
+        log(f"[bench] non-temporal read stream: {read_gbps:.1f} GB/s")
 
     line = {
         "metric": METRIC,
@@ -636,7 +782,8 @@ def main():
             "top_k": wl.top_k, "n_features": wl.n_features,
             "window": wl.window,
             "decode_path": {radar.PATH_SPLIT: "split", radar.PATH_FUSED: "fused",
-                            radar.PATH_SELECT: "select"}.get(path, "?"),
+                            radar.PATH_SELECT: "select",
+                            radar.PATH_SCORED: "scored"}.get(path, "?"),
             "schedule": args.schedule,
             "launch": "hip graph replay" if args.graph else "eager",
             "kernel_events": ("inline" if args.kernel_events == "inline" and not args.graph
@@ -650,6 +797,7 @@ def main():
             "gqa_mode": args.gqa_mode,
             "n_sink": args.sinks,
             "restructures": restructures,
+            "layers": NL,
         },
         "hbm_GBps": round(step_gbps, 1),
         "hbm_frac": round(step_gbps / HBM_PEAK_GBPS, 4),
@@ -662,8 +810,9 @@ def main():
             "unit": "GB/s",
             "frac": round(dom_gbps / HBM_PEAK_GBPS, 4),
             "traffic": None,              # filled in below
-            "bytes_per_launch": int(dom_bytes // Ksteps),
+            "bytes_per_launch": int(per_launch),
             "avg_us": round(dom_avg_ms * 1e3, 2),
+            "cold_cache": cold,
         },
         "kernels_us": {k: v["avg_us"] for k, v in kern.items()},
         "index_build": {
@@ -680,7 +829,16 @@ def main():
         },
         "cpu_baseline": cpu,
     }
-    line["roofline"]["traffic"] = measured_traffic(dom_name, wl.name, line)
+    tr = measured_traffic(dom_name, wl.name, line, per_launch)
+    if tr is not None:
+        line["roofline"]["traffic"] = tr[0]
+        line["roofline"]["traffic_ratio"] = round(tr[1], 4)
+        line["roofline"]["traffic_counter"] = (
+            "rocprofv3 FETCH_SIZE + WRITE_SIZE (L2-miss bytes: Infinity Cache "
+            "hits count too), scaled by a copy kernel's reading")
+    if read_gbps is not None:
+        line["roofline"]["read_peak_GBps"] = round(read_gbps, 1)
+        line["roofline"]["frac_of_read_peak"] = round(dom_gbps / read_gbps, 4)
     if args.kv_host:
         # the K/V rows each step gathers (selected segments, window, sinks)
         # cross the host link; its reference rate is PCIe 5.0 x16, one way

@@ -284,8 +284,14 @@ typedef enum {
   RADAR_PATH_FUSED = 2,  /* used when the shape fits (G <= 4, at most 1024
                             candidate segments, not fp32 with d = 128),
                             else split                                      */
-  RADAR_PATH_SELECT = 3  /* used when G <= 4 and at most 1024 candidate
+  RADAR_PATH_SELECT = 3, /* used when G <= 4 and at most 1024 candidate
                             segments, else split                            */
+  RADAR_PATH_SCORED = 4  /* phi(q) and the scores as the split path's
+                            chip-wide kernels, then R workgroups per pair
+                            that each take the pair's top-k and union from
+                            those scores and share its attention (the fused
+                            kernel from its top-k on); used when G <= 4 and
+                            not fp32 with d = 128, else split              */
 } radar_path;
 
 /* Choose the decode path for later calls from this host thread (default
@@ -308,7 +314,9 @@ typedef enum {
   RADAR_K_COMBINE = 6,  /* merge of the partials                           */
   RADAR_K_FUSED = 7,    /* the whole decode step, fused path               */
   RADAR_K_SELECT = 8,   /* phi(q) to union of one pair, select path        */
-  RADAR_K_COUNT = 9
+  RADAR_K_SCORED = 9,   /* top-k, union, attention from given scores,
+                           scored path                                     */
+  RADAR_K_COUNT = 10
 } radar_kernel;
 
 /* Measurement hook (not part of the method). While enabled on the calling
@@ -338,6 +346,15 @@ radar_status radar_peak_mfma(int32_t iters, float* sink, double* work,
                              hipStream_t stream);
 radar_status radar_peak_exp(int32_t iters, float* sink, double* work,
                             hipStream_t stream);
+
+/* Measurement microkernel (not part of the method), for reporting the decode
+ * kernels against the read rate this GPU sustains: one pass of non-temporal
+ * 16-byte loads (the loads the decode kernels stream K, V and the summaries
+ * with) over `bytes` bytes of the device buffer `buf` (16-byte aligned, a
+ * multiple of 16 bytes), on `stream`; the caller times the launch. sink as
+ * for radar_peak_mfma. */
+radar_status radar_peak_read(const void* buf, size_t bytes, float* sink,
+                             hipStream_t stream);
 
 /* Static text for a status code. */
 const char* radar_status_string(radar_status status);

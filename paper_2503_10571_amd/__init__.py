@@ -127,6 +127,8 @@ def lib() -> ctypes.CDLL:
                                          ctypes.POINTER(ctypes.c_int64), i32]
         L.radar_peak_sink_floats.restype = sz
         L.radar_peak_mfma.argtypes = [i32, _P, ctypes.POINTER(ctypes.c_double), _P]
+        L.radar_peak_read.argtypes = [_P, sz, _P, _P]
+        L.radar_peak_read.restype = ctypes.c_int
         L.radar_peak_exp.argtypes = [i32, _P, ctypes.POINTER(ctypes.c_double), _P]
         for fn in ("radar_peak_mfma", "radar_peak_exp"):
             getattr(L, fn).restype = ctypes.c_int
@@ -376,7 +378,7 @@ def attend_selected(cfg: Config, q, K, V, selected, t: int, out=None,
 
 
 KERNELS = ("append", "build", "phi_q", "score", "topk", "attend", "combine",
-           "fused", "select")
+           "fused", "select", "scored")
 
 
 def schedule_sqrt(t: int):
@@ -388,11 +390,11 @@ def schedule_sqrt(t: int):
     return c.value, w.value
 
 
-PATH_AUTO, PATH_SPLIT, PATH_FUSED, PATH_SELECT = 0, 1, 2, 3
+PATH_AUTO, PATH_SPLIT, PATH_FUSED, PATH_SELECT, PATH_SCORED = 0, 1, 2, 3, 4
 
 
 def set_decode_path(path: int) -> None:
-    """Force the split, fused or select decode path on this thread
+    """Force the split, fused, select or scored decode path on this thread
     (PATH_AUTO = automatic)."""
     _check("radar_set_decode_path", lib().radar_set_decode_path(path))
 
@@ -441,6 +443,29 @@ def peak_rates(device="cuda", iters=4096) -> dict:
         sec = e0.elapsed_time(e1) / 3 * 1e-3
         out[name] = work.value / sec / 1e12
     return out
+
+
+def peak_read_gbps(device="cuda", nbytes=4 << 30, reps=5) -> float:
+    """Measured HBM read rate (GB/s) of one pass of non-temporal 16-byte
+    loads over a fresh `nbytes` buffer, the loads the decode kernels stream
+    with (measurement only)."""
+    L = lib()
+    sink = torch.empty(int(L.radar_peak_sink_floats()), dtype=torch.float32,
+                       device=device)
+    buf = torch.ones(nbytes // 4, dtype=torch.int32, device=device)
+    st = ctypes.c_void_p(torch.cuda.current_stream(sink.device).cuda_stream)
+    _check("radar_peak_read", L.radar_peak_read(_ptr(buf), nbytes, _ptr(sink), st))
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        _check("radar_peak_read", L.radar_peak_read(_ptr(buf), nbytes, _ptr(sink), st))
+    e1.record()
+    torch.cuda.synchronize()
+    sec = e0.elapsed_time(e1) / reps * 1e-3
+    del buf
+    return nbytes / sec / 1e9
 
 
 class RadarLayer:

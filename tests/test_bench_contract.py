@@ -65,3 +65,18 @@ def test_json_line_options():
     assert hl["unit"] == "GB/s" and hl["kv_bytes_per_step"] > 0
     assert 0 < hl["achieved"] and abs(hl["frac"] - hl["achieved"] / hl["peak"]) < 1e-3
     assert d["roofline"]["traffic"] is None        # no counter record for this run
+
+
+def test_cpu_baseline_runs_the_oracle_in_a_pool():
+    """The oracle's host timing: one process and a pool of one-thread
+    workers over the affinity cores, both scaled to all heads (CPU)."""
+    sys.path.insert(0, ROOT)
+    import bench
+    import workloads
+    wl = workloads.WORKLOADS["llama2_16k"].scaled(name="cpu_pool", n_q_heads=4,
+                                                  n_kv_heads=4, t0=700)
+    inp = workloads.make_inputs(wl, "cpu", steps=3)
+    r = bench.cpu_baseline(wl, inp, 0, 3, n_heads=2, min_s=0.2, max_s=5.0, workers=2)
+    assert r["kind"] == "oracle" and r["unit"] == "tokens/s"
+    assert r["cores"] == 2 and r["value"] > 0 and r["value_1_thread"] > 0
+    assert r["cores_affinity"] >= 1 and r["blas_threads_per_process"] == 1

@@ -1,8 +1,8 @@
 """bench.py reports the committed counter traffic of its dominant kernel only
-for a run with the record's kernel source, step range and call form (the
-bytes a launch moves depend on all three)."""
+for a run with the record's library sources and call form, as the record's
+traffic-to-algorithmic ratio times the run's own algorithmic bytes per
+launch (the step range scales both)."""
 import glob
-import hashlib
 import json
 import os
 import sys
@@ -14,49 +14,55 @@ import bench  # noqa: E402
 import workloads  # noqa: E402
 
 
-def _line(rec, **over):
-    run = dict(rec["run"], **over)
-    return {"steps": run["steps"], "warmup": run["warmup"],
-            "config": {k: v for k, v in run.items() if k not in ("steps", "warmup")}}
+def _line(run, **over):
+    return {"config": dict(run, **over)}
 
 
 def _records():
-    out = []
-    for p in sorted(glob.glob(os.path.join(ROOT, "profiles", "traffic_*.json"))):
-        out.append(json.load(open(p)))
-    return out
+    return [json.load(open(p)) for p in
+            sorted(glob.glob(os.path.join(ROOT, "profiles", "traffic_*.json")))]
 
 
-def test_records_are_for_the_default_runs():
+def test_records_are_for_the_default_call_form():
     recs = _records()
     assert recs, "no committed traffic records"
     for rec in recs:
         wl = workloads.WORKLOADS[rec["workload"]]
         run = rec["run"]
-        assert run["steps"] == wl.steps and run["warmup"] == 16, rec["workload"]
         assert run["schedule"] == "fixed" and run["selector"] == "radar"
         assert run["calls"] == "radar_append_decode"
         assert run["omega"] == ("bf16" if wl.dtype == "bf16" else "f32")
 
 
-def test_traffic_only_for_the_same_run():
+def test_traffic_only_for_the_same_sources_and_call_form(tmp_path):
+    run = {"decode_path": "fused", "schedule": "fixed", "calls": "radar_append_decode",
+           "selector": "radar", "omega": "bf16"}
+    rec = {"kernel": "k_decode_fused", "workload": "mha_128k",
+           "sources_sha256": bench.source_sha256(), "traffic_ratio": 1.01, "run": run}
+    (tmp_path / "traffic_k_decode_fused_mha_128k.json").write_text(json.dumps(rec))
+    t = bench.measured_traffic("k_decode_fused", "mha_128k", _line(run), 1000,
+                               profiles=str(tmp_path))
+    assert t == (1010, 1.01)
+    for over in ({"calls": "radar_append + radar_decode"}, {"schedule": "sqrt"},
+                 {"omega": "f32"}, {"decode_path": "split"}, {"layers": 4},
+                 {"kv": "pinned host memory"}):
+        assert bench.measured_traffic("k_decode_fused", "mha_128k", _line(run, **over),
+                                      1000, profiles=str(tmp_path)) is None, over
+    rec["sources_sha256"] = "0" * 64
+    (tmp_path / "traffic_k_decode_fused_mha_128k.json").write_text(json.dumps(rec))
+    assert bench.measured_traffic("k_decode_fused", "mha_128k", _line(run), 1000,
+                                  profiles=str(tmp_path)) is None
+    assert bench.measured_traffic("k_decode_fused", "no_such_workload", _line(run),
+                                  1000) is None
+
+
+def test_committed_records_are_consistent():
+    """A record's ratio is its traffic over its algorithmic bytes."""
     for rec in _records():
-        k, w = rec["kernel"], rec["workload"]
-        t = bench.measured_traffic(k, w, _line(rec))
-        src = os.path.join(ROOT, rec["source"])
-        fresh = hashlib.sha256(open(src, "rb").read()).hexdigest() == rec["source_sha256"]
-        if not fresh:
-            assert t is None
+        if "traffic_ratio" not in rec:
             continue
-        # the record rounds the KiB and the scales; the bytes agree to 1e-3
-        assert abs(t - rec["traffic_bytes_per_launch"]) <= 1e-3 * rec["traffic_bytes_per_launch"]
-        assert bench.measured_traffic(k, w, _line(rec, steps=rec["run"]["steps"] // 2)) is None
-        assert bench.measured_traffic(k, w, _line(rec, warmup=0)) is None
-        assert bench.measured_traffic(k, w, _line(rec, calls="radar_append + radar_decode")) is None
-        assert bench.measured_traffic(k, w, _line(rec, schedule="sqrt")) is None
-        assert bench.measured_traffic(k, w, _line(rec, omega="other")) is None
-    assert bench.measured_traffic("k_decode_fused", "no_such_workload",
-                                  {"steps": 1, "warmup": 0, "config": {}}) is None
+        r = rec["traffic_bytes_per_launch"] / rec["algorithmic_bytes_per_launch"]
+        assert abs(r - rec["traffic_ratio"]) < 1e-3, rec["workload"]
 
 
 def test_byte_model_with_sinks():

@@ -86,8 +86,9 @@ CASES = [
 ]
 
 
-@pytest.mark.parametrize("path", [radar.PATH_SPLIT, radar.PATH_FUSED, radar.PATH_SELECT],
-                         ids=["split", "fused", "select"])
+@pytest.mark.parametrize("path", [radar.PATH_SPLIT, radar.PATH_FUSED, radar.PATH_SELECT,
+                                  radar.PATH_SCORED],
+                         ids=["split", "fused", "select", "scored"])
 @pytest.mark.parametrize("wl,opt", CASES, ids=[c[0].name for c in CASES])
 def test_no_write_outside_buffers(wl, opt, path):
     print(f"[case] canaries {wl.name} path={path}", flush=True)

@@ -2,7 +2,7 @@
 
 Each case draws a shape (dtype, head_dim, group size, kv heads, batch,
 features, segment length, window, k, sinks, GQA mode, ragged start lengths),
-a decode path and the call form (radar_append + radar_decode, or one
+a decode path (a fifth of the cases the scored path) and the call form (radar_append + radar_decode, or one
 radar_append_decode) from its own seed, then runs 3 decode steps through the
 C ABI with the same acceptance as the core parity tests (tie band 1e-5 on
 the Eq. 6 scores; outputs 2e-3 fp32 / 1e-2 bf16; summaries 1e-4), and one
@@ -58,6 +58,8 @@ def draw(seed):
     opt["omega_bf16"] = bool(wl.dtype == "bf16" and rng.random() < 0.5)
     if rng.random() < 0.1:                    # the split path's chunked scores
         wl = wl.scaled(n_features=int(rng.choice([1024, 2048])))
+    if rng.random() < 0.2:                    # the scored path
+        path = radar.PATH_SCORED
     return wl, opt, path
 
 

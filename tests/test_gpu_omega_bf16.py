@@ -21,8 +21,9 @@ from workloads import WORKLOADS  # noqa: E402
 pytestmark = pytest.mark.gpu
 
 PATHS = pytest.mark.parametrize("path", [radar.PATH_SPLIT, radar.PATH_FUSED,
-                                         radar.PATH_SELECT],
-                                ids=["split", "fused", "select"])
+                                         radar.PATH_SELECT,
+                                 radar.PATH_SCORED],
+                                ids=["split", "fused", "select", "scored"])
 
 
 def _workloads():

@@ -33,8 +33,9 @@ def _announce(name):
 
 
 PATHS = pytest.mark.parametrize("path", [radar.PATH_SPLIT, radar.PATH_FUSED,
-                                 radar.PATH_SELECT],
-                                ids=["split", "fused", "select"])
+                                 radar.PATH_SELECT,
+                                 radar.PATH_SCORED],
+                                ids=["split", "fused", "select", "scored"])
 
 
 def _run(wl, steps, groups=None, check_steps=None, path=radar.PATH_AUTO):
@@ -131,7 +132,7 @@ def test_large_feature_counts(n, G, dtype):
     wl = Workload(f"n{n}_g{G}", batch=2, n_q_heads=2 * G, n_kv_heads=2, head_dim=128,
                   t0=2100, seg_len=64, top_k=6, n_features=n, window=64, dtype=dtype,
                   steps=6, keys="clustered", planted=2)
-    for path in (radar.PATH_SPLIT, radar.PATH_FUSED, radar.PATH_SELECT):
+    for path in (radar.PATH_SPLIT, radar.PATH_FUSED, radar.PATH_SELECT, radar.PATH_SCORED):
         _run(wl, 6, path=path)
 
 

@@ -19,8 +19,9 @@ pytestmark = pytest.mark.gpu
 
 
 @pytest.mark.parametrize("path", [radar.PATH_SPLIT, radar.PATH_FUSED,
-                                 radar.PATH_SELECT],
-                         ids=["split", "fused", "select"])
+                                 radar.PATH_SELECT,
+                          radar.PATH_SCORED],
+                         ids=["split", "fused", "select", "scored"])
 @pytest.mark.parametrize("dtype,Hq,Hkv,d,k", [("bf16", 4, 2, 64, 3),
                                               ("f32", 2, 2, 128, 2)])
 def test_sqrt_schedule_episode(path, dtype, Hq, Hkv, d, k):
