@@ -95,7 +95,7 @@
 extern "C" {
 #endif
 
-#define RADAR_ABI_VERSION 5
+#define RADAR_ABI_VERSION 6
 
 typedef enum {
   RADAR_OK = 0,

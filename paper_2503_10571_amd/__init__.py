@@ -17,7 +17,7 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libradar.so")
 
-ABI_VERSION = 5
+ABI_VERSION = 6
 # bytes of the library's own decode scratch (RADAR_NOALLOC_SCRATCH_BYTES)
 NOALLOC_SCRATCH_BYTES = 32 << 20
 RADAR_F32, RADAR_BF16 = 0, 1
