@@ -699,7 +699,7 @@ def main():
     elif path == radar.PATH_SCORED:
         # the fused kernel from its top-k on: the K/V gather (and the rows the
         # merged call appends)
-        dom, dom_name = "scored", "k_decode_fused (scored)"
+        dom, dom_name = "scored", "k_decode_fused_scored"
         dom_bytes = kv_bytes + (NL * Ksteps * wl.batch * wl.n_kv_heads * 4 * wl.head_dim
                                 * s_kv if merged else 0)
     else:

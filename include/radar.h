@@ -279,7 +279,9 @@ typedef enum {
   RADAR_PATH_AUTO = 0,   /* fused when the shape fits and either B * Hkv >=
                             #CUs, one pair's step reads <= 256 KB, or a
                             pair's summary rows are <= 384 KB; else select
-                            when the rows are <= 384 KB; split otherwise    */
+                            when the rows are <= 384 KB; else scored when
+                            G <= 4 and not fp32 with d = 128; split
+                            otherwise                                       */
   RADAR_PATH_SPLIT = 1,
   RADAR_PATH_FUSED = 2,  /* used when the shape fits (G <= 4, at most 1024
                             candidate segments, not fp32 with d = 128),

@@ -122,6 +122,19 @@ def test_full_size_segment_close(name, steps, close_step, path):
     torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("path", [radar.PATH_AUTO, radar.PATH_SPLIT, radar.PATH_SELECT,
+                                  radar.PATH_SCORED, radar.PATH_FUSED],
+                         ids=["auto", "split", "select", "scored", "fused"])
+def test_paper_default_16k(path):
+    """The paper's own settings (n = 2048, k = 64, w = 1024, c = 128) at its
+    16K prefill on a GQA layer, at full size on two sampled groups, across a
+    segment close (t = 16512 at step 127). (With 120 candidates the fused
+    and select kernels take it too when forced.)"""
+    wl = WORKLOADS["paper_16k"]
+    _run(wl, 129, groups=H.sample_groups(wl, 2, seed=3),
+         check_steps={0, 1, 126, 127, 128}, path=path)
+
+
 @pytest.mark.parametrize("n,G,dtype", [(1024, 1, "bf16"), (2048, 4, "bf16"),
                                          (1024, 4, "f32"), (2048, 1, "f32"),
                                          (2048, 8, "bf16")])
@@ -139,8 +152,9 @@ def test_large_feature_counts(n, G, dtype):
 def test_path_choice():
     """The fused path serves shapes with at least one (b, kv head) pair per
     CU, small steps, or few summary rows per pair (several workgroups per
-    pair); the select path fp32 d = 128 caches with few rows; G > 4, more
-    than 1024 candidates or many rows per pair take the split path."""
+    pair); the select path fp32 d = 128 caches with few rows; the scored
+    path the other shapes with G <= 4 (many rows per pair, more than 1024
+    candidates); G = 8 and fp32 d = 128 with many rows the split path."""
     def cfg(wl):
         return H.config_of(wl, wl.t0 + 1)
     n_cu = torch.cuda.get_device_properties(0).multi_processor_count
@@ -148,7 +162,11 @@ def test_path_choice():
     assert mha.batch * mha.n_kv_heads >= n_cu
     assert radar.decode_path(cfg(mha), mha.t0 + 1, mha.top_k) == radar.PATH_FUSED
     g5 = WORKLOADS["gqa_512k"]
-    assert radar.decode_path(cfg(g5), g5.t0 + 1, g5.top_k) == radar.PATH_SPLIT
+    assert radar.decode_path(cfg(g5), g5.t0 + 1, g5.top_k) == radar.PATH_SCORED
+    pd = WORKLOADS["paper_16k"]
+    assert radar.decode_path(cfg(pd), pd.t0 + 1, pd.top_k) == radar.PATH_SCORED
+    f32_many = WORKLOADS["gqa_512k"].scaled(dtype="f32")
+    assert radar.decode_path(cfg(f32_many), f32_many.t0 + 1, 32) == radar.PATH_SPLIT
     # a small step per pair (launch-bound): fused even with few pairs
     tiny = WORKLOADS["tiny"]
     assert radar.decode_path(cfg(tiny), tiny.t0 + 1, tiny.top_k) == radar.PATH_FUSED
@@ -172,6 +190,11 @@ def test_path_choice():
         assert radar.decode_path(cfg(g5), g5.t0 + 1, g5.top_k) == radar.PATH_SELECT
         assert radar.decode_path(cfg(g8), g8.t0 + 1, 16) == radar.PATH_SPLIT
         assert radar.decode_path(cfg(wide), wide.t0 + 1, 16) == radar.PATH_SELECT
+        radar.set_decode_path(radar.PATH_SCORED)
+        assert radar.decode_path(cfg(mha), mha.t0 + 1, 16) == radar.PATH_SCORED
+        assert radar.decode_path(cfg(many), many.t0 + 1, 16) == radar.PATH_SCORED
+        assert radar.decode_path(cfg(g8), g8.t0 + 1, 16) == radar.PATH_SPLIT
+        assert radar.decode_path(cfg(f32_many), f32_many.t0 + 1, 32) == radar.PATH_SPLIT
     finally:
         radar.set_decode_path(radar.PATH_AUTO)
 

@@ -6,7 +6,7 @@ CPU oracle consume the tensors it returns, so the two sides always see the same
 inputs. Omega, the Gaussian projection the method samples once (Alg. 1,
 initialisation), is drawn here and passed in as an input.
 
-The five workloads stand in for the paper's long-context decoding setups (the
+The workloads stand in for the paper's long-context decoding setups (the
 16K-token prefill of the PG-19 perplexity runs, Llama-2 MHA and Llama-3 /
 Mistral GQA head shapes, prompts up to 32K and beyond); none of the paper's
 datasets or weights are used.
@@ -67,6 +67,11 @@ WORKLOADS = {
     # 512K context, c close to sqrt(t), with a full index build.
     "gqa_512k": Workload("gqa_512k", 1, 32, 8, 128, 524288, 724, 32, 512, 724,
                          "bf16", 1024, "clustered", 0),
+    # The paper's own Radar settings at its 16K-token prefill (n = 2048
+    # features, k = 64 segments, a 1024-token window, c = sqrt(16384)) on a
+    # Llama-3 / Mistral-shaped GQA layer; context only.
+    "paper_16k": Workload("paper_16k", 1, 32, 8, 128, 16384, 128, 64, 2048, 1024,
+                          "bf16", 256, "clustered", 0),
 }
 
 # Seeds: Omega = 1234 + index, data = 1000 * index + {0 keys, 1 values,
