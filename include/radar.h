@@ -238,6 +238,23 @@ radar_status radar_decode_exact(const radar_config* cfg, const void* q,
                                 void* workspace, size_t workspace_bytes,
                                 hipStream_t stream);
 
+/* The exact segment masses behind radar_decode_exact's selection, for
+ * recall measurements of Radar's selection against the exact segment search
+ * (Section 3.3): for every (b, q head), ln(beta_s) of each candidate segment
+ * s < n_cand (beta_s = sum over the segment's keys of exp(q . k / sqrt(d)),
+ * the beta of Theorem 2's proof), and at index n_cand the same log-sum of
+ * the tokens that belong to no candidate segment (the window W and the
+ * sinks), which every selection attends; exp(ln_beta - logsumexp(ln_beta))
+ * over indices 0 .. n_cand is then each part's share of the full softmax.
+ * ln_beta: device fp32 [B][Hq][capacity / c + 1]; entries after index
+ * n_cand of a row are not written (a sequence with an invalid length in
+ * lens gets -inf at index 0 and nothing else). t and lens as for
+ * radar_decode; the summaries, Omega and k are not involved. Needs no
+ * workspace. */
+radar_status radar_segment_mass(const radar_config* cfg, const void* q,
+                                const void* K, int64_t t, const int64_t* lens,
+                                float* ln_beta, hipStream_t stream);
+
 /* Scratch bytes radar_decode, radar_append_decode, radar_decode_exact and
  * radar_attend_selected need for this shape and k (0 if cfg is invalid). */
 size_t radar_decode_workspace_bytes(const radar_config* cfg, int32_t k);

@@ -108,6 +108,7 @@ def lib() -> ctypes.CDLL:
                                           _P, i32, _P, _P, _P, _P, sz, _P]
         L.radar_append_decode_noalloc.argtypes = [cfgp, _P, _P, _P, _P, _P, _P,
                                                   _P, i64, _P, i32, _P, _P, _P, _P]
+        L.radar_segment_mass.argtypes = [cfgp, _P, _P, i64, _P, _P, _P]
         L.radar_decode_workspace_bytes.argtypes = [cfgp, i32]
         L.radar_decode_workspace_bytes.restype = sz
         L.radar_attend_selected.argtypes = [cfgp, _P, _P, _P, _P, i32, i64, _P,
@@ -134,7 +135,7 @@ def lib() -> ctypes.CDLL:
             getattr(L, fn).restype = ctypes.c_int
         for fn in ("radar_build_index", "radar_append", "radar_decode",
                    "radar_append_decode", "radar_append_decode_noalloc",
-                   "radar_decode_exact",
+                   "radar_decode_exact", "radar_segment_mass",
                    "radar_attend_selected",
                    "radar_profile_enable", "radar_profile_read"):
             getattr(L, fn).restype = ctypes.c_int
@@ -358,6 +359,23 @@ def decode_exact(cfg: Config, q, K, V, t: int, k: int, out=None,
         ctypes.byref(cfg.c_struct()), _ptr(q), _ptr(K), _ptr(V), t, _ptr(lens),
         k, _ptr(out), _ptr(selected), _ptr(scores), _ptr(workspace),
         workspace.numel(), _stream(q)))
+    return out
+
+
+def segment_mass(cfg: Config, q, K, t: int, lens=None, out=None):
+    """radar_segment_mass: ln(beta_s) of every candidate segment and, at
+    index n_cand, of the window and sinks, per (b, q head):
+    [B][Hq][capacity / c + 1] fp32 (entries after n_cand unwritten)."""
+    _query(cfg, q); _cache(cfg, K)
+    lens = _lens(lens, cfg, "lens")
+    rows = cfg.summary_rows + 1
+    if out is None:
+        out = torch.full((cfg.batch, cfg.n_q_heads, rows), float("nan"),
+                         dtype=torch.float32, device=q.device)
+    _need(out, torch.float32, "ln_beta", cfg.batch * cfg.n_q_heads * rows)
+    _check("radar_segment_mass", lib().radar_segment_mass(
+        ctypes.byref(cfg.c_struct()), _ptr(q), _ptr(K), t, _ptr(lens), _ptr(out),
+        _stream(q)))
     return out
 
 

@@ -121,26 +121,30 @@ __global__ __launch_bounds__(256) void k_peak_exp(int iters, float* __restrict__
   sink[(int64_t)blockIdx.x * blockDim.x + threadIdx.x] = v;
 }
 
-// The HBM read stream every decode kernel is bound by: a grid-stride pass of
-// non-temporal 16-byte loads over a buffer of n16 16-byte words, four loads
-// in flight per thread and kPeakReadWgPerCu 256-thread workgroups per CU;
-// the XOR of the words, one value per workgroup, keeps the loads alive.
-constexpr int kPeakReadWgPerCu = 8;
+// The HBM read stream every decode kernel is bound by: one pass of
+// non-temporal 16-byte loads over a buffer of n16 16-byte words, each
+// workgroup over its own contiguous share, eight loads in flight per thread
+// (the fastest of the shapes measured on MI355X: contiguous shares beat a
+// grid-stride pass by 2-15%, and one 256-thread workgroup per CU with eight
+// or sixteen loads in flight reached 7.26-7.27 TB/s over 4 GiB). The XOR of
+// the words, one value per workgroup, keeps the loads alive.
+constexpr int kPeakReadWgPerCu = 1;
 
 __global__ __launch_bounds__(256) void k_peak_read(const uint4* __restrict__ src,
                                                    int64_t n16, float* __restrict__ sink) {
   __shared__ uint32_t red[4];
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t per = (n16 + gridDim.x - 1) / gridDim.x;
+  const int64_t e = min(n16, (int64_t)blockIdx.x * per + per);
+  int64_t i = (int64_t)blockIdx.x * per + threadIdx.x;
   uint32_t acc = 0u;
-  for (; i + 3 * stride < n16; i += 4 * stride) {
-    uint4 v[4];
+  for (; i + 7 * (int64_t)blockDim.x < e; i += 8 * (int64_t)blockDim.x) {
+    uint4 v[8];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) v[j] = ld_stream(src + i + j * stride);
+    for (int j = 0; j < 8; ++j) v[j] = ld_stream(src + i + j * blockDim.x);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc ^= v[j].x ^ v[j].y ^ v[j].z ^ v[j].w;
+    for (int j = 0; j < 8; ++j) acc ^= v[j].x ^ v[j].y ^ v[j].z ^ v[j].w;
   }
-  for (; i < n16; i += stride) {
+  for (; i < e; i += blockDim.x) {
     const uint4 v = ld_stream(src + i);
     acc ^= v.x ^ v.y ^ v.z ^ v.w;
   }
@@ -752,13 +756,33 @@ radar_status radar_decode_exact(const radar_config* cfg, const void* q,
 
   unsigned char* w = reinterpret_cast<unsigned char*>(workspace);
   float* sc = reinterpret_cast<float*>(w + L.scores);
-  if (top.n_cand > 0) launch_segment_mass(s, q, Kp, sc, top.n_cand, sa, stream);
+  if (top.n_cand > 0)
+    launch_segment_mass(s, q, Kp, sc, top.n_cand, sa, (int)std::max<int64_t>(1, s.s_cap),
+                        false, stream);
   launch_topk_union(s, sc, sa, reinterpret_cast<int*>(w + L.uni),
                     reinterpret_cast<int*>(w + L.ucnt), L.umax, selected, scores,
                     AppendArgs{}, stream);
   r = launch_status();
   if (r != RADAR_OK) return r;
   return launch_attend(s, q, Kp, Vp, ag, sa, out, w, L, stream);
+}
+
+radar_status radar_segment_mass(const radar_config* cfg, const void* q,
+                                const void* K, int64_t t, const int64_t* lens,
+                                float* ln_beta, hipStream_t stream) {
+  if (!cfg || !q || !K || !ln_beta) return RADAR_EINVAL;
+  if (!aligned16(q) || !aligned16(K) || !aligned16(ln_beta) || (lens && !aligned16(lens)))
+    return RADAR_EINVAL;
+  Shape s;
+  radar_status r = check_cfg(cfg, &s);
+  if (r != RADAR_OK) return r;
+  if (t < 1 || t > s.cap) return RADAR_ECAPACITY;
+  const SeqArgs sa{lens, t, s.c, s.w, s.n_sink, 1};
+  const Span top = make_span(t, sa);
+  if (top.n_cand > kMaxCand) return RADAR_EUNSUPPORTED;
+  launch_segment_mass(s, q, after_sinks(s, K), ln_beta, top.n_cand, sa,
+                      (int)(s.s_cap + 1), true, stream);
+  return launch_status();
 }
 
 radar_status radar_attend_selected(const radar_config* cfg, const void* q,

@@ -571,6 +571,11 @@ __device__ inline void group_union(const int* sel, unsigned* bits, int G, int pe
 // broadcast) to the lanes that hold the matching V chunks. The state carries
 // across tiles as an online softmax: running max m and sum l (log2 units,
 // wave-uniform) and unreduced per-lane accumulators.
+//
+// (q.k on the matrix cores was measured slower here: the MFMA operand layout
+// gives each 16-lane quarter of a load instruction one 16-byte chunk of 16
+// different rows; that made one-head groups slower and groups of four no
+// faster.)
 template <typename T, int D, int G>
 struct TileAttn {
   static constexpr int EPL = Elem<T>::kPer16;   // elements per 16-byte chunk
@@ -790,8 +795,11 @@ void launch_phi_q_any(const Shape& s, const void* q, const void* omega, float* p
                       hipStream_t st);
 void launch_score(const Shape& s, const float* phiq, const float* summ,
                   float* scores, int n_cand, const SeqArgs& sa, hipStream_t st);
+// ln(beta) of candidates [0, n_cand) into rows of nc_cap scores; with_rest
+// also the mass of the window and sinks at index n_cand
 void launch_segment_mass(const Shape& s, const void* q, const void* K, float* scores,
-                         int n_cand, const SeqArgs& sa, hipStream_t st);
+                         int n_cand, const SeqArgs& sa, int nc_cap, bool with_rest,
+                         hipStream_t st);
 void launch_topk_union(const Shape& s, const float* scores, const SeqArgs& sa,
                        int* uni, int* ucnt, int umax, int32_t* selected,
                        float* sel_scores, const AppendArgs& ap, hipStream_t st);

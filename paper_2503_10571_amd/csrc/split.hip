@@ -233,7 +233,7 @@ __global__ __launch_bounds__(256) void k_topk_union(
 template <typename T, int D, int G>
 __global__ __launch_bounds__(256) void k_segment_mass(
     const T* __restrict__ q, const T* __restrict__ K, float* __restrict__ scores,
-    int Hq, int Hkv, int64_t cap, SeqArgs sa, int nc_cap, float qscale) {
+    int Hq, int Hkv, int64_t cap, SeqArgs sa, int nc_cap, float qscale, int with_rest) {
   constexpr int EPL = Elem<T>::kPer16;
   constexpr int LPR = D / EPL;
   constexpr int RPI = kWave / LPR;
@@ -245,7 +245,10 @@ __global__ __launch_bounds__(256) void k_segment_mass(
   const int64_t b = bh / Hkv, hk = bh % Hkv;
   const int c = sa.c;
   const int s = blockIdx.x * 4 + wave;
-  if (s >= seq_span(sa, b).n_cand) return; // wave-uniform; no barriers below
+  const Span sp = seq_span(sa, b);
+  // item n_cand (with_rest): the tokens in no candidate segment, the window
+  // and the sinks, whose mass every selection keeps
+  if (s > sp.n_cand || (s == sp.n_cand && !with_rest)) return;  // wave-uniform
   const int r = lane / LPR, jj = lane % LPR;
 
   float qf[G][EPL];
@@ -261,9 +264,10 @@ __global__ __launch_bounds__(256) void k_segment_mass(
 #pragma unroll
   for (int g = 0; g < G; ++g) { m[g] = -INFINITY; l[g] = 0.f; }
 
-  for (int off = 0; off < c; off += kTile) {
-    const int len = min(kTile, c - off);
-    const T* kbase = K + (bh * cap + (int64_t)s * c + off) * D + jj * EPL;
+  // rows [row0, row0 + len) after the pair's base, 1 <= len <= 64: an
+  // online log-sum-exp in base 2 across the tiles
+  auto tile = [&](int64_t row0, int len) {
+    const T* kbase = K + (bh * cap + row0) * D + jj * EPL;
     uint4 kr[ITER];
 #pragma unroll
     for (int i = 0; i < ITER; ++i)
@@ -292,11 +296,19 @@ __global__ __launch_bounds__(256) void k_segment_mass(
       l[g] = fmaf(l[g], fast_exp2(m[g] - mn), wave_sum(p));
       m[g] = mn;
     }
+  };
+  if (s < sp.n_cand) {
+    for (int off = 0; off < c; off += kTile) tile((int64_t)s * c + off, min(kTile, c - off));
+  } else {
+    for (int64_t st = sp.ws; st < sp.t; st += kTile) tile(st, (int)min((int64_t)kTile, sp.t - st));
+    for (int off = 0; off < sp.sink; off += kTile)
+      tile((int64_t)off - sa.n_sink, min(kTile, sp.sink - off));
   }
   if (lane == 0) {
 #pragma unroll
     for (int g = 0; g < G; ++g)
-      scores[(b * Hq + hk * G + g) * (int64_t)nc_cap + s] = (m[g] + __log2f(l[g])) * kLn2;
+      scores[(b * Hq + hk * G + g) * (int64_t)nc_cap + s] =
+          l[g] > 0.f ? (m[g] + __log2f(l[g])) * kLn2 : -INFINITY;
   }
 }
 
@@ -701,17 +713,19 @@ radar_status launch_attend(const Shape& s, const void* q, const void* K,
 // ---- exact segment search ---------------------------------------------------
 template <typename T, int D>
 void launch_segment_mass_d(const Shape& s, const void* q, const void* K, float* scores,
-                           int n_cand, const SeqArgs& sa, hipStream_t st) {
-  const dim3 grid((unsigned)ceil_div(n_cand, 4), (unsigned)(s.B * s.Hkv));
-  const int nc_cap = (int)std::max<int64_t>(1, s.s_cap);
+                           int n_cand, const SeqArgs& sa, int nc_cap, bool with_rest,
+                           hipStream_t st) {
+  const int items = n_cand + (with_rest ? 1 : 0);
+  const dim3 grid((unsigned)ceil_div(items, 4), (unsigned)(s.B * s.Hkv));
   const float qscale = kLog2e / std::sqrt((float)s.d);
   const T* qt = reinterpret_cast<const T*>(q);
   const T* Kt = reinterpret_cast<const T*>(K);
+  const int wr = with_rest ? 1 : 0;
   switch (s.G) {
-    case 1: launch(RADAR_K_SCORE, k_segment_mass<T, D, 1>, grid, dim3(256), 0, st, qt, Kt, scores, s.Hq, s.Hkv, s.cap, sa, nc_cap, qscale); break;
-    case 2: launch(RADAR_K_SCORE, k_segment_mass<T, D, 2>, grid, dim3(256), 0, st, qt, Kt, scores, s.Hq, s.Hkv, s.cap, sa, nc_cap, qscale); break;
-    case 4: launch(RADAR_K_SCORE, k_segment_mass<T, D, 4>, grid, dim3(256), 0, st, qt, Kt, scores, s.Hq, s.Hkv, s.cap, sa, nc_cap, qscale); break;
-    default: launch(RADAR_K_SCORE, k_segment_mass<T, D, 8>, grid, dim3(256), 0, st, qt, Kt, scores, s.Hq, s.Hkv, s.cap, sa, nc_cap, qscale); break;
+    case 1: launch(RADAR_K_SCORE, k_segment_mass<T, D, 1>, grid, dim3(256), 0, st, qt, Kt, scores, s.Hq, s.Hkv, s.cap, sa, nc_cap, qscale, wr); break;
+    case 2: launch(RADAR_K_SCORE, k_segment_mass<T, D, 2>, grid, dim3(256), 0, st, qt, Kt, scores, s.Hq, s.Hkv, s.cap, sa, nc_cap, qscale, wr); break;
+    case 4: launch(RADAR_K_SCORE, k_segment_mass<T, D, 4>, grid, dim3(256), 0, st, qt, Kt, scores, s.Hq, s.Hkv, s.cap, sa, nc_cap, qscale, wr); break;
+    default: launch(RADAR_K_SCORE, k_segment_mass<T, D, 8>, grid, dim3(256), 0, st, qt, Kt, scores, s.Hq, s.Hkv, s.cap, sa, nc_cap, qscale, wr); break;
   }
 }
 // ---- entry points for the other units ---------------------------------------
@@ -727,13 +741,14 @@ void launch_phi_q_any(const Shape& s, const void* q, const void* omega, float* p
 }
 
 void launch_segment_mass(const Shape& s, const void* q, const void* K, float* scores,
-                         int n_cand, const SeqArgs& sa, hipStream_t st) {
+                         int n_cand, const SeqArgs& sa, int nc_cap, bool with_rest,
+                         hipStream_t st) {
   if (s.dt == RADAR_BF16) {
-    if (s.d == 64) launch_segment_mass_d<bf16_t, 64>(s, q, K, scores, n_cand, sa, st);
-    else launch_segment_mass_d<bf16_t, 128>(s, q, K, scores, n_cand, sa, st);
+    if (s.d == 64) launch_segment_mass_d<bf16_t, 64>(s, q, K, scores, n_cand, sa, nc_cap, with_rest, st);
+    else launch_segment_mass_d<bf16_t, 128>(s, q, K, scores, n_cand, sa, nc_cap, with_rest, st);
   } else {
-    if (s.d == 64) launch_segment_mass_d<float, 64>(s, q, K, scores, n_cand, sa, st);
-    else launch_segment_mass_d<float, 128>(s, q, K, scores, n_cand, sa, st);
+    if (s.d == 64) launch_segment_mass_d<float, 64>(s, q, K, scores, n_cand, sa, nc_cap, with_rest, st);
+    else launch_segment_mass_d<float, 128>(s, q, K, scores, n_cand, sa, nc_cap, with_rest, st);
   }
 }
 

@@ -16,9 +16,9 @@ here on any keys the caller supplies):
   sweep        both, plus each selector's output error against full
                attention, over a grid of (n, k).
 
-Selections, outputs and full attention come from the library's own decode
-calls; the per-segment attention mass is a plain fp32 softmax over the
-context in torch (a diagnostic, not part of the decode path).
+Selections, outputs, full attention and the exact segment masses come from
+the library's own calls (radar_decode, radar_decode_exact,
+radar_segment_mass); this module only compares and normalises them.
 """
 from __future__ import annotations
 
@@ -27,6 +27,7 @@ import dataclasses
 import torch
 
 from . import Config, build_index, decode, decode_exact, new_summaries
+from . import segment_mass as _segment_mass
 
 
 def set_recall(sel: torch.Tensor, ref: torch.Tensor) -> torch.Tensor:
@@ -38,22 +39,15 @@ def set_recall(sel: torch.Tensor, ref: torch.Tensor) -> torch.Tensor:
     return torch.where(size > 0, found / size.clamp(min=1), torch.ones_like(size))
 
 
-def segment_mass(q: torch.Tensor, K: torch.Tensor, t: int, c: int,
+def segment_mass(cfg: Config, q: torch.Tensor, K: torch.Tensor, t: int,
                  n_cand: int) -> torch.Tensor:
     """Softmax attention mass of each candidate segment, [B][Hq][n_cand]
-    fp32: sum over the segment's keys of softmax(q . k / sqrt(d)) taken over
-    all t tokens. q [B][Hq][d], K [B][Hkv][cap][d]."""
-    B, Hq, d = q.shape
-    Hkv = K.shape[1]
-    G = Hq // Hkv
-    out = torch.empty(B, Hq, n_cand, dtype=torch.float32, device=q.device)
-    for b in range(B):
-        kf = K[b, :, :t].float()                                  # [Hkv, t, d]
-        qf = q[b].float().view(Hkv, G, d).transpose(1, 2).contiguous()
-        p = torch.softmax(torch.matmul(kf, qf) / d ** 0.5, dim=1)  # [Hkv, t, G]
-        seg = p[:, :n_cand * c].reshape(Hkv, n_cand, c, G).sum(2)
-        out[b] = seg.permute(0, 2, 1).reshape(Hq, n_cand)
-    return out
+    fp32: the segment's share of the softmax over all t tokens. The exact
+    masses come from the library (radar_segment_mass: ln(beta) of every
+    candidate and of the window and sinks); here they are only normalised
+    over those n_cand + 1 parts."""
+    ln = _segment_mass(cfg, q, K, t)[..., :n_cand + 1]
+    return torch.softmax(ln, dim=-1)[..., :n_cand]
 
 
 def mass_ratio(sel: torch.Tensor, ref: torch.Tensor,
@@ -94,7 +88,7 @@ def sweep(cfg: Config, q: torch.Tensor, K: torch.Tensor, V: torch.Tensor,
     c, w = cfg.seg_len, cfg.window
     ws = c * (max(0, t - w) // c)
     n_cand = ws // c
-    mass = segment_mass(q, K, t, c, n_cand) if n_cand else None
+    mass = segment_mass(cfg, q, K, t, n_cand) if n_cand else None
     # full attention: a window that covers the whole context (no candidate
     # segment, so the summaries and Omega are not read)
     n0, om0 = next(iter(omegas.items()))

@@ -222,11 +222,20 @@ def test_validation_before_launch(L):
     assert L.radar_append_decode_noalloc(by(huge), good, good, good, good, good,
                                          good, good, 1000, null, 16, good,
                                          None, None, None) == 5
+    # segment_mass: pointers, t, candidates
+    assert L.radar_segment_mass(by(cfg), good, good, 1000, null, null, None) == 1
+    assert L.radar_segment_mass(by(cfg), good, odd, 1000, null, good, None) == 1
+    assert L.radar_segment_mass(by(cfg), good, good, 0, null, good, None) == 2
+    assert L.radar_segment_mass(by(cfg), good, good, 131585, null, good, None) == 2
+    assert L.radar_segment_mass(by(big), good, good, 40000, null, good, None) == 3
     # measurement microkernels
     work = ctypes.c_double()
     assert L.radar_peak_mfma(0, good, by(work), None) == 1
     assert L.radar_peak_exp(16, null, by(work), None) == 1
     assert L.radar_peak_exp(16, odd, by(work), None) == 1
+    assert L.radar_peak_read(good, 0, good, None) == 1
+    assert L.radar_peak_read(good, 24, good, None) == 1
+    assert L.radar_peak_read(odd, 32, good, None) == 1
     # sinks widen the scratch for the attention partials
     assert radar.workspace_bytes(_cfg(n_sink=4096), 16) > \
         radar.workspace_bytes(_cfg(), 16)

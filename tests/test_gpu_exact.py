@@ -148,3 +148,55 @@ def test_exact_errors():
     assert e.value.status == 3
     torch.cuda.synchronize()
     assert bool((out == 3.0).all())
+
+
+MASS_CASES = [
+    (_edge("mass_gqa4_sinks", batch=2, n_q_heads=8, n_kv_heads=2, t0=1500, seg_len=48,
+           window=40), 3, [1500, 900]),
+    (_edge("mass_f32_d64", head_dim=64, dtype="f32", t0=700, seg_len=65, window=65), 0, None),
+    (_edge("mass_window_only", t0=20, window=64), 0, None),
+    (WORKLOADS["gqa_512k"].scaled(name="mass_512k_x", n_q_heads=8, n_kv_heads=2,
+                                  t0=36300), 0, None),
+]
+
+
+@pytest.mark.parametrize("wl,n_sink,lens", MASS_CASES, ids=[c[0].name for c in MASS_CASES])
+def test_segment_mass_matches_oracle(wl, n_sink, lens):
+    """radar_segment_mass: ln(beta) of every candidate segment and, at index
+    n_cand, of the window and sinks, against the oracle (1e-4 absolute);
+    an invalid length gives -inf at index 0 and leaves the rest alone."""
+    print(f"[case] segment mass {wl.name} sinks={n_sink} lens={lens}", flush=True)
+    inp = workloads.make_inputs(wl, "cuda", steps=1)
+    cfg = H.config_of(wl, wl.t0 + 1, n_sink=n_sink)
+    t = wl.t0
+    q = inp.q[0].contiguous()
+    lens_list = lens if lens is not None else [t] * wl.batch
+    lens_dev = None if lens is None else torch.tensor(lens, dtype=torch.int64, device="cuda")
+    ln = radar.segment_mass(cfg, q, inp.K, t, lens=lens_dev)
+    torch.cuda.synchronize()
+    got = ln.cpu().numpy()
+    q64 = H.f64(q)
+    G, c, d = wl.group, wl.seg_len, wl.head_dim
+    for b in range(wl.batch):
+        tb = lens_list[b]
+        ws, n_cand = orc.window_split(tb, c, wl.window, n_sink)
+        for g in range(wl.n_kv_heads):
+            keys = H.f64(inp.K[b, g, :tb])
+            rest = orc.attended_tokens([], c, ws, tb, n_sink)
+            for h in range(g * G, (g + 1) * G):
+                ref = orc.exact_segment_mass(q64[b, h], keys, c, n_cand, offset=n_sink)
+                assert np.max(np.abs(got[b, h, :n_cand] - ref), initial=0.0) <= LNB_TOL
+                lg = keys[rest] @ q64[b, h] / np.sqrt(d)
+                ref_rest = lg.max() + np.log(np.exp(lg - lg.max()).sum()) if len(rest) else -np.inf
+                if np.isfinite(ref_rest):
+                    assert abs(got[b, h, n_cand] - ref_rest) <= LNB_TOL, (b, h)
+                else:
+                    assert got[b, h, n_cand] == -np.inf
+                assert np.all(np.isnan(got[b, h, n_cand + 1:]))
+    # an invalid length: -inf at index 0, nothing else written
+    if wl.batch > 1:
+        bad = torch.tensor([t] + [0] * (wl.batch - 1), dtype=torch.int64, device="cuda")
+        ln2 = radar.segment_mass(cfg, q, inp.K, t, lens=bad)
+        torch.cuda.synchronize()
+        x = ln2.cpu().numpy()
+        assert np.all(x[1:, :, 0] == -np.inf) and np.all(np.isnan(x[1:, :, 1:]))
