@@ -141,6 +141,14 @@ class Stepper:
             raise radar.RadarError("radar_decode", st)
 
 
+def union_stats(us):
+    """min / mean / max of the per-pair union sizes of every timed step, and
+    the mean over steps of each step's mean / max."""
+    a = np.stack([np.asarray(u, dtype=np.float64) for u in us])
+    return {"min": int(a.min()), "mean": round(float(a.mean()), 2), "max": int(a.max()),
+            "mean_over_max": round(float(np.mean(a.mean(1) / np.maximum(a.max(1), 1))), 4)}
+
+
 def union_sizes(sel, G):
     """sel [B][Hq][k] int32 -> union size per (b, kv head) [B * Hkv]."""
     B, Hq, k = sel.shape
@@ -671,9 +679,11 @@ def main():
     sel_np = sel_log.cpu().numpy()
     tot_bytes, dec_bytes, kv_bytes, scan_bytes, summ_bytes = 0, 0, 0, 0, 0
     NL = args.layers           # every layer moves the same bytes
+    u_all = []
     for j in range(Ksteps):
         t = wl.t0 + W + j + 1
         U = union_sizes(sel_np[j], wl.group)
+        u_all.append(U)
         b_all, b_dec, b_kv, b_scan, b_app, b_summ = (NL * x for x in step_bytes(
             wl, t, U, s_kv, sqrt_schedule=args.schedule == "sqrt", exact=exact,
             s_om=s_om, n_sink=args.sinks))
@@ -815,6 +825,10 @@ def main():
             "cold_cache": cold,
         },
         "kernels_us": {k: v["avg_us"] for k, v in kern.items()},
+        # segments attended per (b, kv head) over the timed steps: a pair's
+        # share of the attention is proportional to it, so mean / max bounds
+        # how evenly the pairs' workgroups finish
+        "union_segments": union_stats(u_all),
         "index_build": {
             "ms": round(build_ms, 3),
             "warmup_builds": max(1, args.build_warmup),

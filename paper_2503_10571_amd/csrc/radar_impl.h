@@ -252,10 +252,11 @@ __device__ __forceinline__ void static_for(F&& f) {
   }
 }
 
+// (a plain DPP move, every lane's source valid for these controls: the
+// compiler folds it into the add or max that consumes it)
 template <int CTRL>
 __device__ __forceinline__ float dpp_f(float v) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(
-      __float_as_int(v), __float_as_int(v), CTRL, 0xf, 0xf, false));
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xf, 0xf, true));
 }
 
 // Value of the partner lane in a pairing that differs from this lane in bit
@@ -566,8 +567,9 @@ __device__ inline void group_union(const int* sel, unsigned* bits, int G, int pe
 // tile at a time: lane (r, jj) (r = lane / LPR) reads the 16-byte chunk jj of
 // rows r, r + RPI, ... so every load instruction covers RPI whole rows
 // contiguously (rows past the tile end re-read its last row and are masked).
-// q.k partials are transpose-reduced so that each lane ends with one token's
-// logit, softmax runs across the wave, and p is broadcast back (DPP row
+// q.k partials (bf16: v_dot2_f32_bf16 on the raw pairs, the scale applied to
+// the sums; fp32: fma of the pre-scaled query) are transpose-reduced so that
+// each lane ends with one token's logit, softmax runs across the wave, and p is broadcast back (DPP row
 // broadcast) to the lanes that hold the matching V chunks. The state carries
 // across tiles as an online softmax: running max m and sum l (log2 units,
 // wave-uniform) and unreduced per-lane accumulators.
@@ -584,19 +586,29 @@ struct TileAttn {
   static constexpr int ITER = kTile / RPI;      // load instructions per tile
   static_assert(ITER == LPR, "tile shape");
 
-  float qf[G][EPL];
+  // bf16: the raw query pairs (dot2 operands) and the scale applied to
+  // the sums; fp32: the queries times the scale
+  static constexpr bool BF = sizeof(T) == 2;
+  float qf[BF ? 1 : G][EPL];
+  uint32_t q2[BF ? G : 1][EPL / 2];
+  float qs;
   float m[G], l[G], acc[G][EPL];
 
   // q0: the group's first query head; qscale folds log2(e) / sqrt(d)
   __device__ __forceinline__ void init(const T* __restrict__ q0, float qscale,
                                        int lane) {
     const int jj = lane % LPR;
+    qs = qscale;
 #pragma unroll
     for (int g = 0; g < G; ++g) {
       const uint4 u = *reinterpret_cast<const uint4*>(q0 + g * D + jj * EPL);
-      unpack16<T>(u, qf[g]);
+      if constexpr (BF) {
+        q2[g][0] = u.x; q2[g][1] = u.y; q2[g][2] = u.z; q2[g][3] = u.w;
+      } else {
+        unpack16<T>(u, qf[g]);
 #pragma unroll
-      for (int e = 0; e < EPL; ++e) qf[g][e] *= qscale;
+        for (int e = 0; e < EPL; ++e) qf[g][e] *= qscale;
+      }
       m[g] = -INFINITY;
       l[g] = 0.f;
 #pragma unroll
@@ -613,15 +625,24 @@ struct TileAttn {
                                        int len, int lane, unsigned hmask) {
     const int r = lane / LPR;
     const int jj = lane % LPR;
-    const T* kbase = K + row0 * D + jj * EPL;
-    const T* vbase = V + row0 * D + jj * EPL;
     uint4 kr[ITER], vr[ITER];
+    if (BF && len == kTile) {              // uniform: no row to clamp
+      const T* kbase = K + (row0 + r) * D + jj * EPL;
+      const T* vbase = V + (row0 + r) * D + jj * EPL;
 #pragma unroll
-    for (int i = 0; i < ITER; ++i)
-      kr[i] = ld_stream(kbase + (int64_t)min(i * RPI + r, len - 1) * D);
+      for (int i = 0; i < ITER; ++i) kr[i] = ld_stream(kbase + i * RPI * D);
 #pragma unroll
-    for (int i = 0; i < ITER; ++i)
-      vr[i] = ld_stream(vbase + (int64_t)min(i * RPI + r, len - 1) * D);
+      for (int i = 0; i < ITER; ++i) vr[i] = ld_stream(vbase + i * RPI * D);
+    } else {
+      const T* kbase = K + row0 * D + jj * EPL;
+      const T* vbase = V + row0 * D + jj * EPL;
+#pragma unroll
+      for (int i = 0; i < ITER; ++i)
+        kr[i] = ld_stream(kbase + (int64_t)min(i * RPI + r, len - 1) * D);
+#pragma unroll
+      for (int i = 0; i < ITER; ++i)
+        vr[i] = ld_stream(vbase + (int64_t)min(i * RPI + r, len - 1) * D);
+    }
 
     // logits: lane (r, jj) ends with the logit of tile row jj * RPI + r
     float lg[G];
@@ -629,20 +650,35 @@ struct TileAttn {
       float pl[G][ITER];
 #pragma unroll
       for (int i = 0; i < ITER; ++i) {
-        float kf[EPL];
-        unpack16<T>(kr[i], kf);
+        if constexpr (BF) {
+          // bf16 pairs: exact products, fp32 sums
+          const uint32_t kw[4] = {kr[i].x, kr[i].y, kr[i].z, kr[i].w};
 #pragma unroll
-        for (int g = 0; g < G; ++g) {
-          float a = 0.f;
+          for (int g = 0; g < G; ++g) {
+            float a = 0.f;
 #pragma unroll
-          for (int e = 0; e < EPL; ++e) a = fmaf(qf[g][e], kf[e], a);
-          pl[g][i] = a;
+            for (int w = 0; w < 4; ++w)
+              a = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2v_t, q2[g][w]),
+                                                  __builtin_bit_cast(bf16x2v_t, kw[w]), a,
+                                                  false);
+            pl[g][i] = a;
+          }
+        } else {
+          float kf[EPL];
+          unpack16<T>(kr[i], kf);
+#pragma unroll
+          for (int g = 0; g < G; ++g) {
+            float a = 0.f;
+#pragma unroll
+            for (int e = 0; e < EPL; ++e) a = fmaf(qf[g][e], kf[e], a);
+            pl[g][i] = a;
+          }
         }
       }
 #pragma unroll
       for (int g = 0; g < G; ++g) {
         transpose_reduce<LPR>(pl[g], lane);
-        lg[g] = pl[g][0];
+        lg[g] = BF ? pl[g][0] * qs : pl[g][0];
       }
     }
     const bool mine_ok = (jj * RPI + r) < len;
