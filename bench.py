@@ -141,6 +141,53 @@ class Stepper:
             raise radar.RadarError("radar_decode", st)
 
 
+def phase_clock_pass(stp, W, Ksteps, gpu, max_wgs=8192):
+    """The timed steps once more with the fused kernel's phase stamps on:
+    per step, the stamps of every workgroup of its (last) fused-kernel
+    launch. Returns µs figures: the spread of the workgroups' start, the
+    launch's span (first entry to last merge), each workgroup's total, and
+    per phase the mean and max over workgroups (means over the steps)."""
+    S = radar.CLOCK_STAMPS
+    clocks = torch.empty(max_wgs, S, dtype=torch.int64, device=gpu)
+    khz = radar.wall_clock_khz()
+    if khz <= 0:
+        return None
+    to_us = 1e3 / khz
+    rows = []
+    radar.set_phase_clock(clocks)
+    try:
+        for j in range(Ksteps):
+            clocks.fill_(-1)
+            stp.step(W + j)
+            torch.cuda.synchronize()
+            c = clocks.cpu().numpy()
+            c = c[c[:, 0] >= 0]
+            if len(c):
+                rows.append(c.astype(np.float64))
+    finally:
+        radar.set_phase_clock(None)
+    if not rows:
+        return None
+    acc = {"start_skew": [], "span": [], "wg_mean": [], "wg_max": []}
+    ph = {name: ([], []) for name in radar.CLOCK_PHASES}
+    for c in rows:
+        acc["start_skew"].append((c[:, 0].max() - c[:, 0].min()) * to_us)
+        acc["span"].append((c[:, 6].max() - c[:, 0].min()) * to_us)
+        tot = (c[:, 6] - c[:, 0]) * to_us
+        acc["wg_mean"].append(tot.mean())
+        acc["wg_max"].append(tot.max())
+        for i, name in enumerate(radar.CLOCK_PHASES, start=1):
+            d = (c[:, i] - c[:, i - 1]) * to_us
+            ph[name][0].append(d.mean())
+            ph[name][1].append(d.max())
+    r = lambda v: round(float(np.mean(v)), 2)
+    return {"unit": "us", "clock_khz": khz, "steps": len(rows),
+            "workgroups": int(len(rows[-1])),
+            "start_skew": r(acc["start_skew"]), "span": r(acc["span"]),
+            "workgroup_total": {"mean": r(acc["wg_mean"]), "max": r(acc["wg_max"])},
+            "phases": {name: {"mean": r(v[0]), "max": r(v[1])} for name, v in ph.items()}}
+
+
 def union_stats(us):
     """min / mean / max of the per-pair union sizes of every timed step, and
     the mean over steps of each step's mean / max."""
@@ -478,6 +525,10 @@ def main():
                          "fits the Infinity Cache between its visits, as in a "
                          "multi-layer decode; tokens/s counts one token "
                          "through all layers")
+    ap.add_argument("--phase-clock", type=int, default=0,
+                    help="also replay the timed steps with the fused kernel's "
+                         "per-workgroup phase stamps on (radar_set_phase_clock) "
+                         "and report each phase's duration")
     ap.add_argument("--cold-pass", type=int, default=1,
                     help="also time the dominant kernel with the Infinity "
                          "Cache and L2 swept between steps (a 1 GiB "
@@ -667,6 +718,11 @@ def main():
         # the same steps again with every kernel bracketed by HIP events
         rewind()
         prof = profiled_pass()
+    phases = None
+    if args.phase_clock:
+        log("[bench] phase-clock pass")
+        rewind()
+        phases = phase_clock_pass(stp, W, Ksteps, gpu)
     prof_cold = None
     if args.cold_pass and not args.kv_host:
         log("[bench] cold pass: 1 GiB swept between steps")
@@ -824,6 +880,7 @@ def main():
             "avg_us": round(dom_avg_ms * 1e3, 2),
             "cold_cache": cold,
         },
+        "phase_clock": phases,
         "kernels_us": {k: v["avg_us"] for k, v in kern.items()},
         # segments attended per (b, kv head) over the timed steps: a pair's
         # share of the attention is proportional to it, so mean / max bounds

@@ -95,7 +95,7 @@
 extern "C" {
 #endif
 
-#define RADAR_ABI_VERSION 6
+#define RADAR_ABI_VERSION 7
 
 typedef enum {
   RADAR_OK = 0,
@@ -352,6 +352,24 @@ radar_status radar_profile_enable(int32_t on);
  * next profiled launches, so a profiled pass that follows another creates
  * no events. */
 radar_status radar_profile_read(double* ms, int64_t* launches, int32_t n);
+
+/* Measurement hook (not part of the method): phase clocks of the fused
+ * decode kernel (fused, select and scored paths). While a buffer is set on
+ * the calling host thread, workgroup w < max_wgs of every such launch writes
+ * RADAR_CLOCK_STAMPS readings of the GPU's constant-rate wall clock
+ * (hipDeviceAttributeWallClockRate kHz) to clocks[w * RADAR_CLOCK_STAMPS +
+ * i]: 0 entry, 1 phi(q) done, 2 segment scores done, 3 top-k and window
+ * tiles done, 4 union done, 5 segment tiles done (every wave), 6 output or
+ * partial written, 7 unused. Each is taken by the workgroup's first thread
+ * after the barrier that ends the phase; a phase the launch does not run
+ * keeps the stamp before it. clocks: device memory of max_wgs *
+ * RADAR_CLOCK_STAMPS uint64 values, rewritten by every launch (the last
+ * launch's stamps remain); clocks = NULL stops. Results do not change. */
+#define RADAR_CLOCK_STAMPS 8
+radar_status radar_set_phase_clock(uint64_t* clocks, int32_t max_wgs);
+
+/* The rate of that clock on the current device, in kHz (0 on error). */
+int64_t radar_wall_clock_khz(void);
 
 /* Measurement microkernels (not part of the method), for reporting the
  * index build against what this GPU sustains: radar_peak_mfma runs dense

@@ -17,7 +17,7 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libradar.so")
 
-ABI_VERSION = 6
+ABI_VERSION = 7
 # bytes of the library's own decode scratch (RADAR_NOALLOC_SCRATCH_BYTES)
 NOALLOC_SCRATCH_BYTES = 32 << 20
 RADAR_F32, RADAR_BF16 = 0, 1
@@ -117,6 +117,8 @@ def lib() -> ctypes.CDLL:
         L.radar_status_string.restype = ctypes.c_char_p
         L.radar_last_error.restype = ctypes.c_char_p
         L.radar_profile_enable.argtypes = [i32]
+        L.radar_set_phase_clock.argtypes = [_P, i32]
+        L.radar_wall_clock_khz.restype = i64
         L.radar_schedule_sqrt.argtypes = [i64, ctypes.POINTER(i32),
                                           ctypes.POINTER(i32)]
         L.radar_schedule_sqrt.restype = ctypes.c_int
@@ -435,6 +437,31 @@ def profile_read() -> dict:
     cnt = (ctypes.c_int64 * n)()
     _check("radar_profile_read", lib().radar_profile_read(ms, cnt, n))
     return {k: (ms[i], cnt[i]) for i, k in enumerate(KERNELS)}
+
+
+CLOCK_STAMPS = 8
+# radar_set_phase_clock's stamps: the phase that ends at stamp i (i >= 1)
+CLOCK_PHASES = ("phi_q", "scores", "topk_window", "union", "segment_tiles", "merge")
+
+
+def set_phase_clock(clocks=None) -> None:
+    """radar_set_phase_clock (measurement only): while `clocks` (a device
+    int64 tensor [max_wgs][CLOCK_STAMPS]) is set, every fused-kernel launch
+    from this thread writes its workgroups' phase stamps there; None stops."""
+    if clocks is None:
+        _check("radar_set_phase_clock", lib().radar_set_phase_clock(None, 0))
+        return
+    if (clocks.dtype != torch.int64 or clocks.dim() != 2 or
+            clocks.shape[1] != CLOCK_STAMPS or not clocks.is_cuda or
+            not clocks.is_contiguous()):
+        raise ValueError("clocks: a contiguous device int64 tensor [max_wgs][8]")
+    _check("radar_set_phase_clock",
+           lib().radar_set_phase_clock(_ptr(clocks), clocks.shape[0]))
+
+
+def wall_clock_khz() -> int:
+    """Rate of the clock behind the phase stamps (kHz)."""
+    return int(lib().radar_wall_clock_khz())
 
 
 def peak_rates(device="cuda", iters=4096) -> dict:

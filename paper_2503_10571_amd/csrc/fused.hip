@@ -54,7 +54,7 @@ __global__ __launch_bounds__(512) void k_decode_fused(
     float s2, float inv_sqrt_n, float qscale, int* __restrict__ uni_out,
     int* __restrict__ ucnt_out, int umax, AppendArgs ap, int R, int n_pairs,
     float* __restrict__ part, int maxwg, const float* __restrict__ gscores,
-    int nc_cap) {
+    int nc_cap, uint64_t* __restrict__ clk, int clk_max) {
   constexpr bool SEL = MODE == kFusedSelect;
   constexpr bool SCORED = MODE == kFusedScored;
   constexpr int NW = kFusedWaves;
@@ -83,6 +83,19 @@ __global__ __launch_bounds__(512) void k_decode_fused(
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
+  // measurement hook: the first thread stamps the phase boundaries (every
+  // stamp starts as the entry time: phases 1-2 when they do not run keep it;
+  // later stamps are written on every path)
+  const bool clocked = clk != nullptr && (int)blockIdx.x < clk_max;   // uniform
+  uint64_t* const cw = clk + (clocked ? (int64_t)blockIdx.x * RADAR_CLOCK_STAMPS : 0);
+  auto stamp = [&](int i) {
+    if (clocked && tid == 0) cw[i] = (uint64_t)wall_clock64();
+  };
+  if (clocked && tid == 0) {
+    const uint64_t t0 = (uint64_t)wall_clock64();
+#pragma unroll
+    for (int i = 0; i < RADAR_CLOCK_STAMPS; ++i) cw[i] = t0;
+  }
   // workgroup rj < R of pair bh: the workgroups of a pair differ by a
   // multiple of n_pairs, so they share an XCD (and its L2) when n_pairs is a
   // multiple of 8 (dealing a pair's workgroups over all XCDs instead measured
@@ -234,6 +247,7 @@ __global__ __launch_bounds__(512) void k_decode_fused(
       phase1(std::false_type{});
     }
     __syncthreads();
+    stamp(1);
 
     // ---- 2. scores ------------------------------------------------------
     if constexpr (N > 512) {
@@ -322,6 +336,7 @@ __global__ __launch_bounds__(512) void k_decode_fused(
       }
     }
     __syncthreads();
+    stamp(2);
   }
   }
 
@@ -365,6 +380,7 @@ __global__ __launch_bounds__(512) void k_decode_fused(
     }
   }
   __syncthreads();
+  stamp(3);
 
   // ---- 4. union -----------------------------------------------------------
   // With one query head per group its selection is the set to attend (in
@@ -378,14 +394,21 @@ __global__ __launch_bounds__(512) void k_decode_fused(
     segs = uni_lds;
     n_segs = ucnt_lds;
   }
+  stamp(4);
   if constexpr (SEL) {                     // hand the union to the split path
     for (int i = tid; i < n_segs; i += NW * 64) uni_out[bh * umax + i] = segs[i];
     if (tid == 0) ucnt_out[bh] = n_segs;
+    stamp(5);
+    stamp(6);
     return;
   }
   const int seg_tiles = n_segs * tiles_per_seg;
 
   // ---- 5. segment tiles ---------------------------------------------------
+  // (64-row tiles dealt round robin over the pair's waves; equal shares of
+  // rows instead, cut at segment ends, measured slower: the shares start
+  // mid-tile, so waves run more partial tiles, each costing nearly a whole
+  // one)
   for (int i = rj + wave * R; i < seg_tiles; i += NW * R) {
     const int e = segs[i / tiles_per_seg];
     const int s = e & ((1 << kUniIdBits) - 1);
@@ -398,6 +421,7 @@ __global__ __launch_bounds__(512) void k_decode_fused(
   // ---- 6. merge -----------------------------------------------------------
   ta.reduce_rows();
   __syncthreads();                         // phq / sc are dead from here on
+  stamp(5);
   const int jj = lane % LPR;
   if (lane < LPR) {
 #pragma unroll
@@ -432,6 +456,10 @@ __global__ __launch_bounds__(512) void k_decode_fused(
       if (e == 0) { pj[0] = M; pj[1] = L; }
     }
   }
+  if (clocked) {
+    __syncthreads();
+    stamp(6);
+  }
 }
 
 // The launch helpers below are compiled once per unit, each with its own
@@ -455,7 +483,8 @@ radar_status launch_fused_tdg(const FusedArgs& a) {
          reinterpret_cast<T*>(a.out), a.selected, a.sel_scores, s.Hq, s.Hkv, s.cap,
          s.s_cap, (int)ceil_div(s.c, kTile), a.sa, s.per_head, s1, s2,
          1.f / std::sqrt((float)s.n), kLog2e / std::sqrt((float)s.d), a.uni_out,
-         a.ucnt_out, a.umax, a.ap, a.R, n_pairs, a.part, a.maxwg, a.gscores, a.nc_cap);
+         a.ucnt_out, a.umax, a.ap, a.R, n_pairs, a.part, a.maxwg, a.gscores, a.nc_cap,
+         g_clock, g_clock_max);
   return launch_status();
 }
 

@@ -49,6 +49,8 @@
 namespace radar_impl {
 
 thread_local char g_last_error[256] = "";
+thread_local uint64_t* g_clock = nullptr;
+thread_local int g_clock_max = 0;
 thread_local Profiler g_prof;
 
 int g_num_cu = 0;
@@ -565,6 +567,22 @@ int32_t radar_decode_path(const radar_config* cfg, int64_t t, int32_t k) {
   if (check_cfg(cfg, &s) != RADAR_OK || k < 1 || k > kMaxK || t < 1 || t > s.cap)
     return -1;
   return choose_path(s, SeqArgs{nullptr, t, s.c, s.w, s.n_sink, k});
+}
+
+radar_status radar_set_phase_clock(uint64_t* clocks, int32_t max_wgs) {
+  if (clocks && (max_wgs < 1 || (reinterpret_cast<uintptr_t>(clocks) & 7u)))
+    return RADAR_EINVAL;
+  g_clock = clocks;
+  g_clock_max = clocks ? max_wgs : 0;
+  return RADAR_OK;
+}
+
+int64_t radar_wall_clock_khz(void) {
+  int dev = 0, khz = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess)
+    return 0;
+  return khz;
 }
 
 radar_status radar_profile_enable(int32_t on) {

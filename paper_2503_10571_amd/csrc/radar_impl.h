@@ -741,6 +741,10 @@ constexpr int kFusedMaxCand = 1024;
 // ---------------------------------------------------------------------------
 // text of the last HIP error seen by this thread
 extern thread_local char g_last_error[256];
+// phase-clock buffer of the fused kernel's launches from this thread (null:
+// off) and the number of workgroups it has room for
+extern thread_local uint64_t* g_clock;
+extern thread_local int g_clock_max;
 
 // ---- launch helper with optional per-kernel event timing -----------------
 // While profiling is enabled on a host thread, every launch goes through

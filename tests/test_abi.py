@@ -39,7 +39,7 @@ def test_exports_every_declared_symbol(L):
 
 
 def test_version_and_strings(L):
-    assert L.radar_abi_version() == radar.ABI_VERSION == 6
+    assert L.radar_abi_version() == radar.ABI_VERSION == 7
     for st in range(6):
         assert L.radar_status_string(st).decode()
     assert L.radar_last_error() is not None
