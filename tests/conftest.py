@@ -29,8 +29,7 @@ def pytest_collection_modifyitems(config, items):
 def pytest_terminal_summary(terminalreporter, exitstatus, config):
     """The parity margins of the session: the largest score, summary and
     output errors the oracle checks saw, the band swaps, and the tolerances
-    they were held to. Also written as JSON to $RADAR_MARGINS_OUT, or to
-    gpurun_out/parity_margins.json when that folder exists."""
+    they were held to. Also written as JSON to $RADAR_MARGINS_OUT when set."""
     import json
     h = sys.modules.get("_harness")
     if h is None or not h.MARGINS["episodes"]:
@@ -42,8 +41,6 @@ def pytest_terminal_summary(terminalreporter, exitstatus, config):
             for k, v in M.items() if k != "tolerances")
         + " | tolerances: " + json.dumps(M["tolerances"]))
     path = os.environ.get("RADAR_MARGINS_OUT")
-    if not path and os.path.isdir(os.path.join(ROOT, "gpurun_out")):
-        path = os.path.join(ROOT, "gpurun_out", "parity_margins.json")
     if path:
         with open(path, "w") as f:
             json.dump(M, f, indent=1)
