@@ -243,7 +243,7 @@ radar_status launch_fused(const Shape& s, const void* q, const void* K, const vo
   // registers than the fused kernel has to spare
   if (s.dt == RADAR_F32 && s.d == 128) return RADAR_EUNSUPPORTED;
   const FusedArgs a{&s, q, K, V, omega, summ, sa, out, selected, sel_scores, nullptr,
-                    nullptr, 0, ap, R, part, L.maxwg, st};
+                    nullptr, 0, ap, R, part, L.maxwg, st, nullptr, 0};
   const radar_status r = launch_fused_any(a, false);
   if (r != RADAR_OK || R == 1) return r;
   launch_combine_any(s, part, nullptr, out, sa, L, 1, R, R, st);
@@ -258,7 +258,8 @@ radar_status launch_select(const Shape& s, const void* q, const void* omega,
                            const AppendArgs& ap, hipStream_t st) {
   const FusedArgs a{&s, q, nullptr, nullptr, omega, summ, sa, nullptr, selected,
                     sel_scores, reinterpret_cast<int*>(w + L.uni),
-                    reinterpret_cast<int*>(w + L.ucnt), L.umax, ap, 1, nullptr, 0, st};
+                    reinterpret_cast<int*>(w + L.ucnt), L.umax, ap, 1, nullptr, 0, st,
+                    nullptr, 0};
   return launch_fused_any(a, true);
 }
 

@@ -115,16 +115,14 @@ __global__ __launch_bounds__(256) void k_score(const float* __restrict__ phiq,
     for (int g = 0; g < G; ++g)
 #pragma unroll
       for (int r = 0; r < 16; ++r) part[bt][g][r] = 0.f;
-#pragma unroll 1
-  for (int ch = 0; ch < NCH; ++ch) {     // one chunk's rows live at a time
-    float pq[G][FC];
+  // a chunk's phi(q) features and rows
+  auto load_chunk = [&](int ch, float (&pq)[G][FC], float (&x)[RB][16][FC]) {
 #pragma unroll
     for (int g = 0; g < G; ++g) {
       const float* src = phiq + ((b * Hq + hk * G + g) * N) + ch * 64 * FC + lane * FC;
 #pragma unroll
       for (int e = 0; e < FC; ++e) pq[g][e] = src[e];
     }
-    float x[RB][16][FC];
 #pragma unroll
     for (int bt = 0; bt < RB; ++bt)
 #pragma unroll
@@ -145,9 +143,8 @@ __global__ __launch_bounds__(256) void k_score(const float* __restrict__ phiq,
           x[bt][r][0] = src[0];
         }
       }
-    // with several chunks the compiler would sink each load to its first
-    // use and wait on one load at a time; keep the chunk's loads together
-    if constexpr (NCH > 1) __builtin_amdgcn_sched_barrier(0);
+  };
+  auto add_chunk = [&](const float (&pq)[G][FC], const float (&x)[RB][16][FC]) {
 #pragma unroll
     for (int bt = 0; bt < RB; ++bt)
 #pragma unroll
@@ -159,6 +156,34 @@ __global__ __launch_bounds__(256) void k_score(const float* __restrict__ phiq,
           for (int e = 0; e < FC; ++e) a = fmaf(x[bt][r][e], pq[g][e], a);
           part[bt][g][r] = a;
         }
+  };
+  // Several chunks at G = 4 (four features per lane): two chunks in flight,
+  // the next one's loads issued before this one's products (same products,
+  // same order; 376 registers, one wave per SIMD, as these launches run);
+  // otherwise one chunk's rows live at a time (G = 8 would not fit).
+  constexpr bool kTwo = NCH > 1 && NCH % 2 == 0 && FC == 4 && G == 4;
+  if constexpr (kTwo) {
+    float pqa[G][FC], xa[RB][16][FC], pqb[G][FC], xb[RB][16][FC];
+    load_chunk(0, pqa, xa);
+#pragma unroll 1
+    for (int ch = 0; ch < NCH; ch += 2) {
+      load_chunk(ch + 1, pqb, xb);
+      __builtin_amdgcn_sched_barrier(0);
+      add_chunk(pqa, xa);
+      if (ch + 2 < NCH) load_chunk(ch + 2, pqa, xa);
+      __builtin_amdgcn_sched_barrier(0);
+      add_chunk(pqb, xb);
+    }
+  } else {
+#pragma unroll 1
+    for (int ch = 0; ch < NCH; ++ch) {
+      float pq[G][FC], x[RB][16][FC];
+      load_chunk(ch, pq, x);
+      // with several chunks the compiler would sink each load to its first
+      // use and wait on one load at a time; keep the chunk's loads together
+      if constexpr (NCH > 1) __builtin_amdgcn_sched_barrier(0);
+      add_chunk(pq, x);
+    }
   }
 #pragma unroll
   for (int bt = 0; bt < RB; ++bt) {
