@@ -508,14 +508,19 @@ __device__ void head_topk(const float* __restrict__ src, int n_cand, int k,
 // Union of the group's selections: sel[h * per .. h * per + per) holds the
 // segment ids of head h < G (-1 = none, every other id < kMaxCand). The ids
 // are set in an LDS bitmap (one per head when masks are wanted); the first
-// wave ORs the heads' words, turns the popcounts into prefix offsets, and
-// each lane lists its word's set bits: the distinct ids in ascending order go
-// to uni, each with the mask of the heads that chose it (all heads without
-// masks), and their count to *ucnt. bits: G * kMaxCand / 32 words of LDS.
+// wave ORs the heads' words and turns the popcounts into prefix offsets, and
+// then every thread of the workgroup lists some of the set bits: the
+// distinct ids in ascending order go to uni, each with the mask of the heads
+// that chose it (all heads without masks), and their count to *ucnt. bits:
+// G * kMaxCand / 32 words of LDS. A barrier-synchronised call of the whole
+// workgroup; the caller orders sel's writes before it and uni's reads after.
 constexpr int kBitmapWords = kMaxCand / 32;
 static_assert(kBitmapWords == kWave, "one bitmap word per lane");
 __device__ inline void group_union(const int* sel, unsigned* bits, int G, int per,
                             bool masks, int* uni, int* ucnt) {
+  // each word's union over the maps, and its exclusive prefix of set bits
+  __shared__ uint32_t or_lds[kBitmapWords];
+  __shared__ int pre_lds[kBitmapWords];
   const int tid = threadIdx.x;
   const int nmaps = masks ? G : 1;
   for (int i = tid; i < nmaps * kBitmapWords; i += blockDim.x) bits[i] = 0u;
@@ -527,14 +532,8 @@ __device__ inline void group_union(const int* sel, unsigned* bits, int G, int pe
   }
   __syncthreads();
   if (tid < kWave) {
-    // this lane's word of every head's map, read once (the per-bit head
-    // masks below then need no LDS reads)
-    uint32_t wv[kMaxG];
-#pragma unroll
-    for (int g = 0; g < kMaxG; ++g) wv[g] = g < nmaps ? bits[g * kBitmapWords + tid] : 0u;
     uint32_t word = 0u;
-#pragma unroll
-    for (int g = 0; g < kMaxG; ++g) word |= wv[g];
+    for (int g = 0; g < nmaps; ++g) word |= bits[g * kBitmapWords + tid];
     const int pc = __popc(word);
     // exclusive prefix sum of the popcounts over the 64 lanes
     int incl = pc;
@@ -543,19 +542,24 @@ __device__ inline void group_union(const int* sel, unsigned* bits, int G, int pe
       const int o = __shfl_up(incl, d);
       if (tid >= d) incl += o;
     }
-    int pos = incl - pc;
-    while (word) {
-      const int bit = __ffs(word) - 1;
+    or_lds[tid] = word;
+    pre_lds[tid] = incl - pc;
+    if (tid == kWave - 1) *ucnt = incl;
+  }
+  __syncthreads();
+  // every thread lists some of the set bits: id i sits at its word's
+  // prefix plus the set bits below it in the word (ascending ids)
+  for (int i = tid; i < kBitmapWords * 32; i += blockDim.x) {
+    const int w = i >> 5, bit = i & 31;
+    const uint32_t word = or_lds[w];
+    if ((word >> bit) & 1u) {
       unsigned m = kAllHeads;
       if (masks) {
         m = 0u;
-#pragma unroll
-        for (int g = 0; g < kMaxG; ++g) m |= ((wv[g] >> bit) & 1u) << g;
+        for (int g = 0; g < nmaps; ++g) m |= ((bits[g * kBitmapWords + w] >> bit) & 1u) << g;
       }
-      uni[pos++] = (tid * 32 + bit) | (int)(m << kUniIdBits);
-      word &= word - 1u;
+      uni[pre_lds[w] + __popc(word & ((1u << bit) - 1u))] = i | (int)(m << kUniIdBits);
     }
-    if (tid == kWave - 1) *ucnt = incl;
   }
 }
 
