@@ -165,7 +165,7 @@ __global__ __launch_bounds__(256) void k_build(
         sq += dpp_f<kDppHalfMirror>(sq);
       } else {
         sq = row_sum(sq);
-        if constexpr (CPR == 32) sq += __shfl_xor(sq, 16);
+        if constexpr (CPR == 32) sq = xor_sum<16>(sq);
       }
       if (ch == 0) nrm_lds[buf][row] = sq * s2;
     }
@@ -250,8 +250,8 @@ __global__ __launch_bounds__(256) void k_build(
 #pragma unroll
       for (int f = 0; f < FT; ++f) {
         float v = psum[f];
-        v += __shfl_xor(v, 16);
-        v += __shfl_xor(v, 32);
+        v = xor_sum<16>(v);
+        v = xor_sum<32>(v);
         if (lane < 16) dst[f * 16 + col] = v * out_scale;
         psum[f] = 0.f;
       }

@@ -300,8 +300,8 @@ __global__ __launch_bounds__(512) void k_decode_fused(
         for (int g = 0; g < G; ++g) {
           transpose_reduce<16>(part[g], lane);
           float v = part[g][0];
-          v += __shfl_xor(v, 16);
-          v += __shfl_xor(v, 32);
+          v = xor_sum<16>(v);
+          v = xor_sum<32>(v);
           if (lane < 16 && row < n_cand) sc[g * kFusedMaxCand + row] = v;
         }
       }
@@ -328,8 +328,8 @@ __global__ __launch_bounds__(512) void k_decode_fused(
             }
             transpose_reduce<16>(part, lane);
             float v = part[0];
-            v += __shfl_xor(v, 16);
-            v += __shfl_xor(v, 32);
+            v = xor_sum<16>(v);
+            v = xor_sum<32>(v);
             if (lane < 16 && row < n_cand) sc[g * kFusedMaxCand + row] = v;
           }
         }

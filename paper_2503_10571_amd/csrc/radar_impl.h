@@ -259,17 +259,47 @@ __device__ __forceinline__ float dpp_f(float v) {
   return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xf, 0xf, true));
 }
 
+// Lanes l and l ^ 16 (MASK 16) or l and l ^ 32 (MASK 32) exchange on the
+// vector ALUs: v_permlane16_swap / v_permlane32_swap with both operands the
+// same value leave, in every lane, the pair's two values (the lower lane's
+// first) in the two results.
+template <int MASK>
+__device__ __forceinline__ void xor_pair(float v, float& lo, float& hi) {
+  static_assert(MASK == 16 || MASK == 32, "permlane swap distance");
+  const unsigned u = __float_as_uint(v);
+  if constexpr (MASK == 16) {
+    const auto r = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+    lo = __uint_as_float(r[0]); hi = __uint_as_float(r[1]);
+  } else {
+    const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+    lo = __uint_as_float(r[0]); hi = __uint_as_float(r[1]);
+  }
+}
+// v plus the value of lane l ^ MASK (MASK 16 or 32; the same sum in both
+// lanes of the pair)
+template <int MASK>
+__device__ __forceinline__ float xor_sum(float v) {
+  float lo, hi;
+  xor_pair<MASK>(v, lo, hi);
+  return lo + hi;
+}
+
 // Value of the partner lane in a pairing that differs from this lane in bit
 // MASK. Within a 16-lane row the pairings are DPP moves (mirrors for bits 3
 // and 2, quad swaps for bits 1 and 0); they are only used from the highest
-// bit down, so the lower bits still to be processed never matter.
+// bit down, so the lower bits still to be processed never matter. Bits 4
+// and 5 are lane l ^ MASK, by permlane swaps.
 template <int MASK>
-__device__ __forceinline__ float partner(float x) {
+__device__ __forceinline__ float partner(float x, int lane) {
   if constexpr (MASK == 1) return dpp_f<kDppQuadSwap1>(x);
   else if constexpr (MASK == 2) return dpp_f<kDppQuadSwap2>(x);
   else if constexpr (MASK == 4) return dpp_f<kDppHalfMirror>(x);
   else if constexpr (MASK == 8) return dpp_f<kDppMirror>(x);
-  else return __shfl_xor(x, MASK);
+  else {
+    float lo, hi;
+    xor_pair<MASK>(x, lo, hi);
+    return (lane & MASK) ? lo : hi;
+  }
 }
 
 // One step of a cross-lane transpose-reduce: NV values per lane; paired lanes
@@ -282,7 +312,7 @@ __device__ __forceinline__ void halve(float* v, int lane) {
   for (int i = 0; i < NV / 2; ++i) {
     const float keep = up ? v[i + NV / 2] : v[i];
     const float send = up ? v[i] : v[i + NV / 2];
-    v[i] = keep + partner<MASK>(send);
+    v[i] = keep + partner<MASK>(send, lane);
   }
 }
 
@@ -721,12 +751,18 @@ struct TileAttn {
   // sum the accumulators over the RPI row groups: lanes r = 0 (lane < LPR)
   // then hold dims jj*EPL .. jj*EPL + EPL - 1 of the wave's total
   __device__ __forceinline__ void reduce_rows() {
+    static_for<0, 6>([&](auto bc) {
+      constexpr int msk = 1 << decltype(bc)::value;
+      if constexpr (msk >= LPR) {
 #pragma unroll
-    for (int msk = LPR; msk < kWave; msk <<= 1)
+        for (int g = 0; g < G; ++g)
 #pragma unroll
-      for (int g = 0; g < G; ++g)
-#pragma unroll
-        for (int e = 0; e < EPL; ++e) acc[g][e] += __shfl_xor(acc[g][e], msk);
+          for (int e = 0; e < EPL; ++e) {
+            if constexpr (msk >= 16) acc[g][e] = xor_sum<msk>(acc[g][e]);
+            else acc[g][e] += __shfl_xor(acc[g][e], msk);
+          }
+      }
+    });
   }
 };
 

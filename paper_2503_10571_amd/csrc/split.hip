@@ -192,8 +192,8 @@ __global__ __launch_bounds__(256) void k_score(const float* __restrict__ phiq,
     for (int g = 0; g < G; ++g) {
       transpose_reduce<16>(part[bt][g], lane);
       float v = part[bt][g][0];
-      v += __shfl_xor(v, 16);
-      v += __shfl_xor(v, 32);
+      v = xor_sum<16>(v);
+      v = xor_sum<32>(v);
       if (lane < 16 && row < n_cand)
         scores[(b * Hq + hk * G + g) * (int64_t)nc_cap + row] = v;
     }
