@@ -391,19 +391,37 @@ __device__ __forceinline__ float key_score(u64 key) {
 // atomics (candidates of similar scores share their leading bits, so a
 // histogram over those bits sends every key to one bin) and no ballot per
 // key and bit.
-__device__ __forceinline__ uint32_t wave_and_u32(uint32_t v) {
-#pragma unroll
-  for (int m = 1; m < kWave; m <<= 1) v &= (uint32_t)__shfl_xor((int)v, m);
-  return (uint32_t)__builtin_amdgcn_readfirstlane((int)v);
-}
-__device__ __forceinline__ uint32_t wave_or_u32(uint32_t v) {
-#pragma unroll
-  for (int m = 1; m < kWave; m <<= 1) v |= (uint32_t)__shfl_xor((int)v, m);
-  return (uint32_t)__builtin_amdgcn_readfirstlane((int)v);
-}
 template <int CTRL>
 __device__ __forceinline__ int dpp_i(int v) {
-  return __builtin_amdgcn_update_dpp(v, v, CTRL, 0xf, 0xf, false);
+  return __builtin_amdgcn_mov_dpp(v, CTRL, 0xf, 0xf, true);
+}
+// AND / OR over the 64 lanes, uniform: the 16-lane row by DPP (quad swaps,
+// mirrors), then the rows by permlane swaps
+__device__ __forceinline__ uint32_t wave_and_u32(uint32_t v) {
+  int x = (int)v;
+  x &= dpp_i<kDppQuadSwap1>(x);
+  x &= dpp_i<kDppQuadSwap2>(x);
+  x &= dpp_i<kDppHalfMirror>(x);
+  x &= dpp_i<kDppMirror>(x);
+  float lo, hi;
+  xor_pair<16>(__int_as_float(x), lo, hi);
+  x = __float_as_int(lo) & __float_as_int(hi);
+  xor_pair<32>(__int_as_float(x), lo, hi);
+  x = __float_as_int(lo) & __float_as_int(hi);
+  return (uint32_t)__builtin_amdgcn_readfirstlane(x);
+}
+__device__ __forceinline__ uint32_t wave_or_u32(uint32_t v) {
+  int x = (int)v;
+  x |= dpp_i<kDppQuadSwap1>(x);
+  x |= dpp_i<kDppQuadSwap2>(x);
+  x |= dpp_i<kDppHalfMirror>(x);
+  x |= dpp_i<kDppMirror>(x);
+  float lo, hi;
+  xor_pair<16>(__int_as_float(x), lo, hi);
+  x = __float_as_int(lo) | __float_as_int(hi);
+  xor_pair<32>(__int_as_float(x), lo, hi);
+  x = __float_as_int(lo) | __float_as_int(hi);
+  return (uint32_t)__builtin_amdgcn_readfirstlane(x);
 }
 // sum over the 64 lanes, uniform
 __device__ __forceinline__ int wave_sum_i32(int v) {
