@@ -35,15 +35,16 @@ template <> struct MfmaCfg<float> {      // v_mfma_f32_16x16x4_f32
   typedef float frag_t;
 };
 
-template <typename T, int D>
+template <typename T, int D, int TL>
 struct BuildTile {
   static constexpr int kRowBytes = D * (int)sizeof(T);
   static constexpr int kPitch = kRowBytes + 16;          // LDS row pitch
   static constexpr int kChunksPerRow = kRowBytes / 16;
-  static constexpr int kChunksPerThread = kTile * kChunksPerRow / 256;
+  static constexpr int kChunksPerThread = TL * kChunksPerRow / 256;
 };
 
-template <typename T, int D, int FT>
+// TL: keys per LDS tile (64, or 128 for bf16 keys in segments of >= 128)
+template <typename T, int D, int FT, int TL>
 __global__ __launch_bounds__(256) void k_build(
     const T* __restrict__ K, const void* __restrict__ omega, bool obf,
     float* __restrict__ summ, int n, int c, int64_t cap, int64_t s_cap,
@@ -51,14 +52,14 @@ __global__ __launch_bounds__(256) void k_build(
     float out_scale, int64_t kv_head_stride_rows,
     const int64_t* __restrict__ pos, int Hkv, int n_sink) {
   using MC = MfmaCfg<T>;
-  using BT = BuildTile<T, D>;
+  using BT = BuildTile<T, D, TL>;
   constexpr int KB = D / MC::kK;
   constexpr int CPR = BT::kChunksPerRow;
   constexpr int CPT = BT::kChunksPerThread;
   static_assert(CPT >= 1 && (256 % CPR) == 0, "tile shape");
 
-  __shared__ __attribute__((aligned(16))) unsigned char tile_lds[2][kTile * BT::kPitch];
-  __shared__ float nrm_lds[2][kTile];
+  __shared__ __attribute__((aligned(16))) unsigned char tile_lds[2][TL * BT::kPitch];
+  __shared__ float nrm_lds[2][TL];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -90,7 +91,7 @@ __global__ __launch_bounds__(256) void k_build(
     }
   }
 
-  const int ntiles = (c + kTile - 1) / kTile;
+  const int ntiles = (c + TL - 1) / TL;
   float psum[FT];
 #pragma unroll
   for (int f = 0; f < FT; ++f) psum[f] = 0.f;
@@ -123,8 +124,8 @@ __global__ __launch_bounds__(256) void k_build(
   int pre_valid = 0;
   // tile tl of the item whose rows start at `base`
   auto fetch = [&](const T* base, int tl_) {
-    pre_valid = min(kTile, c - tl_ * kTile);
-    const T* src = base + (int64_t)tl_ * kTile * D;
+    pre_valid = min(TL, c - tl_ * TL);
+    const T* src = base + (int64_t)tl_ * TL * D;
 #pragma unroll
     for (int p = 0; p < CPT; ++p) {
       const int ci = p * 256 + tid;
@@ -176,7 +177,7 @@ __global__ __launch_bounds__(256) void k_build(
     constexpr bool FULL = decltype(full_tag)::value;
     const unsigned char* tb = tile_lds[buf];
 #pragma unroll
-    for (int st = 0; st < kTile / 16; ++st) {
+    for (int st = 0; st < TL / 16; ++st) {
       if (!FULL && st * 16 >= valid) break;
       typename MC::frag_t afrag[KB];
       const unsigned char* arow = tb + (st * 16 + col) * BT::kPitch;
@@ -240,7 +241,7 @@ __global__ __launch_bounds__(256) void k_build(
     const bool more = nitem < n_items;
     if (more) fetch(nbase, ntl);
 
-    if (valid == kTile) compute(buf, valid, std::true_type{});
+    if (valid == TL) compute(buf, valid, std::true_type{});
     else compute(buf, valid, std::false_type{});
 
     if (tl == ntiles - 1) {                // segment complete
@@ -266,15 +267,15 @@ __global__ __launch_bounds__(256) void k_build(
   }
 }
 
-template <typename T, int D, int FT>
-radar_status launch_build_t(const Shape& s, const void* K, const void* omega,
-                            float* summ, int seg_first, int seg_count,
-                            const int64_t* pos, hipStream_t st) {
+template <typename T, int D, int FT, int TL>
+radar_status launch_build_tl(const Shape& s, const void* K, const void* omega,
+                             float* summ, int seg_first, int seg_count,
+                             const int64_t* pos, hipStream_t st) {
   const int slices = s.n / (64 * FT);
   const int64_t items = (int64_t)s.B * s.Hkv * seg_count;
   if (items == 0) return RADAR_OK;
   if (items >= ((int64_t)1 << 31)) return RADAR_EUNSUPPORTED;   // 32-bit item ids
-  auto kern = k_build<T, D, FT>;
+  auto kern = k_build<T, D, FT, TL>;
   int per_cu = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, 256, 0) != hipSuccess || per_cu < 1)
     per_cu = 1;
@@ -289,6 +290,22 @@ radar_status launch_build_t(const Shape& s, const void* K, const void* omega,
                      s.s_cap, seg_first, seg_count, items, s1, s2, out_scale, s.cap,
                      pos, s.Hkv, s.n_sink);
   return launch_status();
+}
+
+// 128-key tiles halve the tile loop's barriers and prefetch rounds per key
+// (same sums in the same order: each lane's column sums run over the same
+// 16-key sub-tiles); for bf16 keys only (fp32 rows at d = 128 would need
+// 136 KB of LDS) and segments of at least 128 keys (shorter ones would run
+// half-empty tiles)
+template <typename T, int D, int FT>
+radar_status launch_build_t(const Shape& s, const void* K, const void* omega,
+                            float* summ, int seg_first, int seg_count,
+                            const int64_t* pos, hipStream_t st) {
+  if constexpr (sizeof(T) == 2) {
+    if (s.c >= 128)
+      return launch_build_tl<T, D, FT, 128>(s, K, omega, summ, seg_first, seg_count, pos, st);
+  }
+  return launch_build_tl<T, D, FT, 64>(s, K, omega, summ, seg_first, seg_count, pos, st);
 }
 
 template <typename T, int D>
