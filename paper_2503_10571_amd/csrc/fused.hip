@@ -252,8 +252,8 @@ __global__ __launch_bounds__(512) void k_decode_fused(
     // ---- 2. scores ------------------------------------------------------
     if constexpr (N > 512) {
       // each 16-row batch in chunks of FC features per lane (chunk ch of
-      // lane l: features ch * 64 * FC + l * FC + e), the layout and order
-      // of the split path's score kernel, so a lane holds one chunk of the
+      // lane l: features ch * 64 * FC + l * FC + e), the chunk layout of
+      // the split path's score kernel, so a lane holds one chunk of the
       // batch's rows at a time
       constexpr int FC = G >= 4 ? 4 : 8;
       constexpr int NCH = FPL / FC;

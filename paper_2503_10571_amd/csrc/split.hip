@@ -79,11 +79,15 @@ __global__ __launch_bounds__(256) void k_phi_q(const T* __restrict__ q,
 // (fewer waves per workgroup when that spreads a small call over more CUs;
 // the waves are independent). Lane l holds FPL = n / 64 features of phi(q)
 // for the G heads of the group, in chunks of at most 8 (n = 1024 and 2048
-// take 2 and 4 chunks, so the rows of a batch fit in registers); each chunk
+// take 2 to 8 chunks, so the rows of a batch fit in registers); each chunk
 // of a row is one contiguous wave load, and all of a batch's rows are loaded
 // before any is reduced. A 16-row batch is transpose-reduced inside each
 // 16-lane row with DPP, then summed over the four rows.
-template <int N, int G>
+// With S > 1 the S waves of a workgroup share one batch of rows instead and
+// each takes NCH / S of the chunks (one round trip to memory instead of
+// NCH / 2 for a wave that walks them all); the waves' row sums are added in
+// LDS in wave order.
+template <int N, int G, int S>
 __global__ __launch_bounds__(256) void k_score(const float* __restrict__ phiq,
                                                const float* __restrict__ summ,
                                                float* __restrict__ scores,
@@ -95,13 +99,19 @@ __global__ __launch_bounds__(256) void k_score(const float* __restrict__ phiq,
   constexpr int FC = FPL <= 8 ? FPL : (G >= 4 ? 4 : 8);
   constexpr int NCH = FPL / FC;            // chunks (1 for n <= 512)
   constexpr int RB = N <= 256 ? 2 : 1;     // 16-row batches per wave
+  static_assert(NCH % S == 0 && (S == 1 || RB == 1), "feature split");
+  constexpr int CPW = NCH / S;             // chunks of each wave
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int64_t bh = blockIdx.y;
   const int64_t b = bh / Hkv, hk = bh % Hkv;
   const int n_cand = seq_span(sa, b).n_cand;
-  const int wrow0 = (blockIdx.x * (blockDim.x >> 6) + wave) * (16 * RB);
-  if (wrow0 >= n_cand) return;             // wave-uniform; no barriers below
+  const int wrow0 = S > 1 ? blockIdx.x * 16
+                          : (blockIdx.x * (blockDim.x >> 6) + wave) * (16 * RB);
+  // wave-uniform, and workgroup-uniform with S > 1 (the waves share rows),
+  // so the barrier below is reached by all waves or by none
+  if (wrow0 >= n_cand) return;
+  const int ch0 = S > 1 ? wave * CPW : 0;  // this wave's first chunk
 
   // chunk ch holds features ch * 64 * FC + lane * FC + e (e < FC) of lane
   // `lane`, so each chunk of a row is one contiguous 64 * FC * 4-byte wave
@@ -161,30 +171,31 @@ __global__ __launch_bounds__(256) void k_score(const float* __restrict__ phiq,
   // the next one's loads issued before this one's products (same products,
   // same order; 376 registers, one wave per SIMD, as these launches run);
   // otherwise one chunk's rows live at a time (G = 8 would not fit).
-  constexpr bool kTwo = NCH > 1 && NCH % 2 == 0 && FC == 4 && G == 4;
+  constexpr bool kTwo = CPW > 1 && CPW % 2 == 0 && FC == 4 && G == 4;
   if constexpr (kTwo) {
     float pqa[G][FC], xa[RB][16][FC], pqb[G][FC], xb[RB][16][FC];
-    load_chunk(0, pqa, xa);
+    load_chunk(ch0, pqa, xa);
 #pragma unroll 1
-    for (int ch = 0; ch < NCH; ch += 2) {
+    for (int ch = ch0; ch < ch0 + CPW; ch += 2) {
       load_chunk(ch + 1, pqb, xb);
       __builtin_amdgcn_sched_barrier(0);
       add_chunk(pqa, xa);
-      if (ch + 2 < NCH) load_chunk(ch + 2, pqa, xa);
+      if (ch + 2 < ch0 + CPW) load_chunk(ch + 2, pqa, xa);
       __builtin_amdgcn_sched_barrier(0);
       add_chunk(pqb, xb);
     }
   } else {
 #pragma unroll 1
-    for (int ch = 0; ch < NCH; ++ch) {
+    for (int ch = ch0; ch < ch0 + CPW; ++ch) {
       float pq[G][FC], x[RB][16][FC];
       load_chunk(ch, pq, x);
       // with several chunks the compiler would sink each load to its first
       // use and wait on one load at a time; keep the chunk's loads together
-      if constexpr (NCH > 1) __builtin_amdgcn_sched_barrier(0);
+      if constexpr (CPW > 1) __builtin_amdgcn_sched_barrier(0);
       add_chunk(pq, x);
     }
   }
+  __shared__ float red[S > 1 ? S : 1][G][16];
 #pragma unroll
   for (int bt = 0; bt < RB; ++bt) {
     const int row = wrow0 + bt * 16 + (lane & 15);
@@ -194,8 +205,24 @@ __global__ __launch_bounds__(256) void k_score(const float* __restrict__ phiq,
       float v = part[bt][g][0];
       v = xor_sum<16>(v);
       v = xor_sum<32>(v);
-      if (lane < 16 && row < n_cand)
-        scores[(b * Hq + hk * G + g) * (int64_t)nc_cap + row] = v;
+      if constexpr (S > 1) {
+        if (lane < 16) red[wave][g][lane] = v;
+      } else {
+        if (lane < 16 && row < n_cand)
+          scores[(b * Hq + hk * G + g) * (int64_t)nc_cap + row] = v;
+      }
+    }
+  }
+  if constexpr (S > 1) {
+    __syncthreads();
+    if (wave == 0 && lane < 16 && wrow0 + lane < n_cand) {
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        float v = red[0][g][lane];
+#pragma unroll
+        for (int w = 1; w < S; ++w) v += red[w][g][lane];
+        scores[(b * Hq + hk * G + g) * (int64_t)nc_cap + wrow0 + lane] = v;
+      }
     }
   }
 }
@@ -611,16 +638,28 @@ void launch_phi_q(const Shape& s, const void* q, const void* omega, float* phiq,
 template <int N, int G>
 void launch_score_ng(const Shape& s, const float* phiq, const float* summ,
                      float* scores, int n_cand, const SeqArgs& sa, hipStream_t st) {
-  constexpr int rows_per_wave = 16 * (N <= 256 ? 2 : 1);
-  // waves per workgroup: 4 when that still gives two workgroups per CU,
-  // else fewer, so that the rows spread over more CUs
-  int wpb = 4;
-  while (wpb > 1 && ceil_div(n_cand, rows_per_wave * wpb) * s.B * s.Hkv < 2 * num_cu())
-    wpb >>= 1;
-  const dim3 grid((unsigned)ceil_div(n_cand, rows_per_wave * wpb), (unsigned)(s.B * s.Hkv));
-  const int nc_cap = (int)std::max<int64_t>(1, s.s_cap);
-  launch(RADAR_K_SCORE, k_score<N, G>, grid, dim3(64 * wpb), 0, st, phiq, summ, scores,
-         s.Hq, s.Hkv, sa, s.s_cap, nc_cap);
+  // above n = 512 the waves of a workgroup split a batch's chunks, two
+  // chunks each (the four features per lane at G = 4 keep two in flight)
+  constexpr int FPL = N / 64;
+  constexpr int NCH = FPL <= 8 ? 1 : FPL / (G >= 4 ? 4 : 8);
+  constexpr int S = NCH >= 4 ? NCH / 2 : 1;
+  if constexpr (S > 1) {
+    const dim3 grid((unsigned)ceil_div(n_cand, 16), (unsigned)(s.B * s.Hkv));
+    const int nc_cap = (int)std::max<int64_t>(1, s.s_cap);
+    launch(RADAR_K_SCORE, k_score<N, G, S>, grid, dim3(64 * S), 0, st, phiq, summ, scores,
+           s.Hq, s.Hkv, sa, s.s_cap, nc_cap);
+  } else {
+    constexpr int rows_per_wave = 16 * (N <= 256 ? 2 : 1);
+    // waves per workgroup: 4 when that still gives two workgroups per CU,
+    // else fewer, so that the rows spread over more CUs
+    int wpb = 4;
+    while (wpb > 1 && ceil_div(n_cand, rows_per_wave * wpb) * s.B * s.Hkv < 2 * num_cu())
+      wpb >>= 1;
+    const dim3 grid((unsigned)ceil_div(n_cand, rows_per_wave * wpb), (unsigned)(s.B * s.Hkv));
+    const int nc_cap = (int)std::max<int64_t>(1, s.s_cap);
+    launch(RADAR_K_SCORE, k_score<N, G, 1>, grid, dim3(64 * wpb), 0, st, phiq, summ, scores,
+           s.Hq, s.Hkv, sa, s.s_cap, nc_cap);
+  }
 }
 
 template <int N>
