@@ -137,11 +137,13 @@ def test_paper_default_16k(path):
 
 @pytest.mark.parametrize("n,G,dtype", [(1024, 1, "bf16"), (2048, 4, "bf16"),
                                          (1024, 4, "f32"), (2048, 1, "f32"),
-                                         (2048, 8, "bf16")])
+                                         (2048, 8, "bf16"), (2048, 2, "bf16")])
 def test_large_feature_counts(n, G, dtype):
     """n = 1024 and 2048 (the paper's default feature count): the score
     passes read each summary row in feature chunks (the split path's score
-    kernel and the fused and select kernels' phase 2)."""
+    kernel and the fused and select kernels' phase 2); with four or more
+    chunks the split path's score kernel spreads a row batch's chunks over
+    2 or 4 waves (n = 1024 at G >= 4, n = 2048 at every G)."""
     wl = Workload(f"n{n}_g{G}", batch=2, n_q_heads=2 * G, n_kv_heads=2, head_dim=128,
                   t0=2100, seg_len=64, top_k=6, n_features=n, window=64, dtype=dtype,
                   steps=6, keys="clustered", planted=2)
@@ -268,6 +270,28 @@ def test_append_equals_rebuild_bitwise():
     radar.build_index(ep.cfg, ep.K, ep.inp.omega, t, fresh)
     torch.cuda.synchronize()
     n_seg = t // wl.seg_len
+    assert torch.equal(fresh[:, :, :n_seg], ep.summ[:, :, :n_seg])
+
+
+@pytest.mark.parametrize("c,d,n", [(129, 128, 256), (191, 64, 512), (255, 128, 64),
+                                   (384, 128, 256)])
+def test_build_tiles_ragged_segments(c, d, n):
+    """bf16 keys in segments of at least 128 go through the index build in
+    128-key tiles: segment lengths that end in a partial tile (1, 63, 127
+    keys) or span three whole tiles, against the oracle's summaries at the
+    prefix and after the appends that close a segment, and appends equal to
+    a one-shot rebuild bit for bit."""
+    steps = c + 2                          # at least one segment closes
+    wl = _edge(f"build_c{c}", t0=6 * c + 5, seg_len=c, window=c, n_features=n,
+               head_dim=d, keys="clustered", batch=2, n_kv_heads=2, n_q_heads=2,
+               top_k=2)
+    ep = _run(wl, steps, check_steps={0, steps - 1})
+    t = wl.t0 + steps
+    fresh = radar.new_summaries(ep.cfg, ep.K.device)
+    radar.build_index(ep.cfg, ep.K, ep.inp.omega, t, fresh)
+    torch.cuda.synchronize()
+    n_seg = t // c
+    assert n_seg == 7
     assert torch.equal(fresh[:, :, :n_seg], ep.summ[:, :, :n_seg])
 
 
